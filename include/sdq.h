@@ -1,0 +1,215 @@
+/*
+ * sdq.h -- C ABI of libsdq: Sigma-Delta quantized linear layers (SDQ-LLM,
+ * arXiv 2510.03275) on AMD Instinct MI355X (gfx950).
+ *
+ * The library encodes fp32 weight matrices into binary or ternary
+ * Sigma-Delta codes (Algorithm 1 without block compensation: block Hadamard
+ * smoothing, Resample up to OSR x the block length, per-row scale,
+ * first-order Sigma-Delta scan) and evaluates y = x W_hat^T directly on the
+ * codes (Fig. 5: the activations are expanded to the oversampled length and
+ * contracted against the codes, additions only in the decode kernel).
+ *
+ * Conventions for every entry point:
+ *  - Pointers named *_dev are device (HBM) pointers, *_host are host pointers.
+ *    All memory is owned by the caller; the library never frees or retains a
+ *    caller pointer.  The library owns only its cached coefficient tables
+ *    (one set per device and (block, M) pair, allocated on first use, released
+ *    by sdq_release_tables).
+ *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  GPU
+ *    work is enqueued asynchronously on it; host-side argument errors are
+ *    returned before anything is enqueued.
+ *  - Matrices are row-major and densely packed unless stated otherwise.
+ *  - Functions return SDQ_OK or a negative sdq_status; sdq_last_error()
+ *    gives a message for the last failure on the calling thread.
+ */
+#ifndef SDQ_H
+#define SDQ_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  SDQ_OK = 0,
+  SDQ_ERR_ARG = -1,        /* null pointer, negative size, bad enum value        */
+  SDQ_ERR_SHAPE = -2,      /* K not a multiple of the block, unsupported block   */
+  SDQ_ERR_OSR = -3,        /* OSR < 1 or M = round(OSR*B) not a multiple of 32   */
+  SDQ_ERR_LEVELS = -4,     /* levels not 2 or 3                                  */
+  SDQ_ERR_NONFINITE = -5,  /* a weight (or an upsampled sample) is NaN or Inf    */
+  SDQ_ERR_WORKSPACE = -6,  /* workspace pointer missing or too small             */
+  SDQ_ERR_HIP = -7,        /* a HIP runtime call failed                          */
+  SDQ_ERR_NOMEM = -8,      /* the coefficient-table cache could not allocate     */
+  SDQ_ERR_UNSUPPORTED = -9 /* a valid request this build does not implement      */
+} sdq_status;
+
+typedef enum { SDQ_F16 = 0, SDQ_BF16 = 1, SDQ_F32 = 2 } sdq_dtype;
+
+/*
+ * Geometry of one encoded linear layer (filled by sdq_layout_init; treat as
+ * read-only).  Notation of the paper: the weight W has d_row = n rows and
+ * d_col = k columns; Algorithm 1 splits the columns into blocks of B and
+ * upsamples each block to M = round(OSR * B) samples (Algorithm 1, SDQuant).
+ */
+typedef struct sdq_layout {
+  int64_t n;               /* rows of W (output features)                        */
+  int64_t k;               /* columns of W (input features), multiple of block   */
+  int32_t block;           /* B: 64, 128 or 256                                  */
+  int32_t m_up;            /* M = round(osr * B), a multiple of 32, M >= B       */
+  int32_t levels;          /* 2: codes in {-1,+1} (Eq. 4); 3: {-1,0,+1} (Eq. 6)  */
+  int32_t bits;            /* bits per stored code: 1 (levels 2), 2 (levels 3)   */
+  int64_t nb;              /* k / block                                          */
+  int64_t k_up;            /* nb * M codes per row (Algorithm 1: osr * d_col)    */
+  int64_t n_pad;           /* n rounded up to a multiple of 64                   */
+  int64_t n_chunks;        /* 16-byte chunks per row = ceil(k_up / codes_per_chunk) */
+  int32_t codes_per_chunk; /* 128 (binary) or 64 (ternary)                       */
+  int32_t reserved;
+} sdq_layout;
+
+/*
+ * Packed code format (output of sdq_quantize, input of sdq_linear):
+ *  - code j of row r is the Sigma-Delta output for sample j % M of block
+ *    j / M (block-major, as Algorithm 1 places block i at columns
+ *    i*osr ... (i+B)*osr of Q_out);
+ *  - 16-byte chunk c of row r (codes c*CPC ... c*CPC+CPC-1, CPC =
+ *    codes_per_chunk) starts at byte 16 * (((r/64) * n_chunks + c) * 64 + r%64):
+ *    the 64 rows of a panel store their chunk c side by side;
+ *  - inside a chunk, position q = j % CPC is in little-endian 32-bit word
+ *    q / (32/bits), field of `bits` bits starting at bit bits*(q % (32/bits));
+ *  - binary field: 1 = +1, 0 = -1.  Ternary field: 00 = 0, 01 = +1, 11 = -1
+ *    (10 is never written and reads as 0);
+ *  - padding codes (j >= k_up) and padding rows (r >= n) are zero bits.
+ * Total size: sdq_codes_bytes() = n_pad * n_chunks * 16 bytes.
+ */
+
+/* Fill *out for an n x k weight at oversampling ratio osr (Section 3.2) with
+ * `levels` code values and block size `block` (0 selects 256).
+ * Errors: SDQ_ERR_ARG (out NULL, n < 0, k <= 0), SDQ_ERR_SHAPE (block not
+ * 64/128/256 or k % block != 0), SDQ_ERR_OSR, SDQ_ERR_LEVELS. */
+sdq_status sdq_layout_init(sdq_layout* out, int64_t n, int64_t k, double osr,
+                           int32_t levels, int32_t block);
+
+/* Bytes of the packed code buffer: n_pad * n_chunks * 16 (0 for a NULL layout). */
+size_t sdq_codes_bytes(const sdq_layout* layout);
+
+/* Compression ratio of Eq. 14, eta = bits * OSR / 16, using the stored bits
+ * per code (1 or 2) and OSR = M / B. */
+double sdq_compression_ratio(const sdq_layout* layout);
+
+/* Device workspace (bytes) sdq_quantize needs for this layout: the rotated
+ * weights, the upsampled rows, per-row maxima and a status word (about
+ * 4 * n_pad * (k + k_up) + 4 * n_pad + 256 bytes). */
+size_t sdq_quantize_workspace_bytes(const sdq_layout* layout);
+
+/*
+ * Encode W into Sigma-Delta codes (Algorithm 1 with Had and SDQuant, no
+ * block compensation; Eq. 7-8 for the scan, Eq. 4 / Eq. 6 for the
+ * quantizer, per-row scale s_r = max |upsampled row|, threshold s_r / 2).
+ *   w_dev        fp32 [n x k] row-major weights (device).
+ *   codes_dev    device buffer of sdq_codes_bytes(layout) bytes, written in
+ *                the packed format above (all bytes, padding included).
+ *   scales_dev   fp32 [n] per-row scales (device).
+ *   workspace    device buffer of at least sdq_quantize_workspace_bytes bytes;
+ *                its contents need no initialisation.
+ * Arithmetic is fp32 with every product and sum rounded separately, in the
+ * order the paper's definitions give, so the codes are bit-exact and
+ * deterministic.  Non-finite weights do not fail the call itself: they set a
+ * flag in the workspace that sdq_quantize_check() reports.
+ * Errors (host-side, nothing enqueued): SDQ_ERR_ARG, SDQ_ERR_WORKSPACE,
+ * SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
+sdq_status sdq_quantize(const float* w_dev, const sdq_layout* layout, void* codes_dev,
+                        float* scales_dev, void* workspace_dev, size_t workspace_bytes,
+                        void* stream);
+
+/* Synchronise `stream` and report the status flag of the last sdq_quantize
+ * that used this workspace: SDQ_OK, or SDQ_ERR_NONFINITE when a weight or an
+ * upsampled sample was NaN / Inf (the codes of such rows are meaningless). */
+sdq_status sdq_quantize_check(const void* workspace_dev, void* stream);
+
+/* Device workspace (bytes) sdq_linear needs for m activation rows: the
+ * expanded activations (m x k_up, fp32 for m <= 16, fp16 otherwise) plus
+ * split-K partial sums and counters. */
+size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
+
+/*
+ * y = x W_hat^T for the encoded layer (Fig. 5 and Algorithm 1 line 6: W_hat is
+ * the decimated, Hadamard-restored reconstruction of the codes).  Computed as
+ * x_tilde = per-block (x_b Had) D^T (D: Resample back to B), then
+ * y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j].
+ *   x_dev        [m x k] activations of type xt (F16, BF16 or F32), row-major.
+ *   m            activation rows, >= 0 (m = 0 is a no-op).  m <= 16 runs the
+ *                decode path (fp32 expansion, additions over the codes);
+ *                larger m runs the prefill path (fp16 expansion, MFMA).
+ *   codes_dev, scales_dev  as written by sdq_quantize for `layout`.
+ *   y_dev        fp32 [m x n] output, row-major, fully overwritten.
+ *   workspace    >= sdq_linear_workspace_bytes(layout, m) bytes; the library
+ *                keeps counters in it that must start zeroed: zero the
+ *                buffer once before its first use (the calls restore them).
+ * Accuracy: max_r |y - y*| / max_r |y*| <= 1e-3 per activation row against the
+ * fp64 definition.  Calls that share a workspace must be ordered (same stream).
+ * Errors: SDQ_ERR_ARG, SDQ_ERR_WORKSPACE, SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
+sdq_status sdq_linear(const void* x_dev, sdq_dtype xt, int64_t m, const void* codes_dev,
+                      const float* scales_dev, const sdq_layout* layout, float* y_dev,
+                      void* workspace_dev, size_t workspace_bytes, void* stream);
+
+/*
+ * MultiOSR (Section 3.4): per-linear OSR from weight variance and size, host
+ * only.  Reading of the prose rule: layer OSR proportional to the inverse of
+ * the layer's parameter-weighted variance, linear OSR inside a layer
+ * proportional to n_params / variance, both clipped to [lo, hi] with scale
+ * factors found by fp64 bisection so the parameter-weighted means hit the
+ * target; then floor to the grid and add one grid step in order of largest
+ * remainder while the model's weighted mean stays <= target.
+ *   var_host[count]       per-linear weight variance (<= 0 maps to hi).
+ *   nparams_host[count]   parameter count of each linear (> 0).
+ *   layer_host[count]     layer index of each linear.
+ *   osr_out_host[count]   result, multiples of `grid` in [lo, hi].
+ * Errors: SDQ_ERR_ARG (null pointers with count > 0, count < 0, a
+ * non-positive parameter count, not 0 < lo <= target <= hi, grid <= 0). */
+sdq_status sdq_multiosr(const double* var_host, const int64_t* nparams_host,
+                        const int32_t* layer_host, int64_t count, double target, double lo,
+                        double hi, double grid, double* osr_out_host);
+
+/* Mean and population variance (two-pass, fp64 accumulation) of `count` fp32
+ * values on the device: the variance input of MultiOSR (Section 3.4).
+ *   out_dev   double[2] = {mean, variance} (device).
+ *   workspace >= sdq_moments_workspace_bytes(count) bytes.
+ * Errors: SDQ_ERR_ARG, SDQ_ERR_WORKSPACE, SDQ_ERR_HIP. */
+size_t sdq_moments_workspace_bytes(int64_t count);
+sdq_status sdq_weight_moments(const float* w_dev, int64_t count, double* out_dev,
+                              void* workspace_dev, size_t workspace_bytes, void* stream);
+
+/* Unpack a packed code buffer (host copy) into int8 codes [n x k_up] in
+ * {-1, 0, +1} (host).  Errors: SDQ_ERR_ARG. */
+sdq_status sdq_unpack_codes(const sdq_layout* layout, const void* codes_host, int8_t* out_host);
+
+/* The fp32 interpolation coefficients the encoder uses: out_host[p] =
+ * fp32(g(p)) for p in [0, block*m_up), with g the periodic-sinc kernel of
+ * the upsampling Resample (1 at p = 0, 0 at other multiples of M,
+ * sin(pi tau) / (B tan(pi tau / B)) at tau = p / M).  Errors: SDQ_ERR_ARG,
+ * SDQ_ERR_SHAPE, SDQ_ERR_OSR. */
+sdq_status sdq_upsample_table(int32_t block, int32_t m_up, float* out_host);
+
+/* Upload the coefficient tables for (block, m_up) on the current device ahead
+ * of time, so that later calls allocate nothing.  Errors: SDQ_ERR_SHAPE,
+ * SDQ_ERR_OSR, SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
+sdq_status sdq_prepare(int32_t block, int32_t m_up);
+
+/* Free every cached coefficient table (all devices).  No call may be in flight. */
+void sdq_release_tables(void);
+
+/* Static description of a status code, and the message of the last failure
+ * on the calling thread. */
+const char* sdq_status_string(sdq_status status);
+const char* sdq_last_error(void);
+
+/* Library version: major * 10000 + minor * 100 + patch. */
+int32_t sdq_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* SDQ_H */

@@ -1,0 +1,306 @@
+// Sigma-Delta weight encoder for gfx950 (Algorithm 1 without block
+// compensation).  Four launches on the caller's stream:
+//
+//   clear      zero the non-finite flag and the per-row maxima;
+//   rotate     per (64-row panel, block): load W, Sylvester FWHT in LDS in the
+//              stage order h = 1, 2, ..., B/2, scale by fp32(1/sqrt(B))
+//              (Section 3.3), store the rotated block rows-contiguous, copy the
+//              samples whose interpolation kernel is a unit impulse
+//              (m % P == 0) into the upsampled buffer, fold |v| into the row max;
+//   upsample   the remaining M - gcd(B, M) samples of every block as dense
+//              sums x_up[m] = sum_t fl(v[t] * g(p(t, m))) in t order from +0.0,
+//              every product and sum rounded separately (the Resample of
+//              Algorithm 1 in closed form).  This is a batched fp32 product
+//              V^T (rows x B) * U (B x M_nz) evaluated as a register-tiled VALU
+//              GEMM whose k-loop runs t = 0 .. B-1 in order, so each output's
+//              accumulation order is exactly the definition's;
+//   scan       per (row, block) chain: first-order Sigma-Delta (Eq. 7-8) with the
+//              row scale s = max|x_up| and the binary (Eq. 4) or ternary (Eq. 6,
+//              threshold s/2) quantizer, packing codes into the panel format.
+//
+// Everything is compiled with floating-point contraction off: no fused
+// multiply-add may merge a product into a sum.
+#include <hip/hip_runtime.h>
+
+#include "sdq_internal.h"
+
+#pragma clang fp contract(off)
+
+namespace sdq {
+namespace {
+
+constexpr int kRotThreads = 256;
+constexpr int kUpBM = 128;        // rows per upsample tile (two panels)
+constexpr int kUpBN = 64;         // non-impulse samples per upsample tile
+constexpr int kUpBK = 32;         // t-chunk staged in LDS
+constexpr int kUpThreads = 128;   // 16 x 8 threads, 8 x 8 outputs each
+constexpr int kScanWaves = 4;
+
+__global__ void clear_kernel(uint32_t* __restrict__ flag, uint32_t* __restrict__ rmax, int64_t n) {
+  const int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
+  if (i == 0) flag[0] = 0u;
+  if (i < n) rmax[i] = 0u;
+}
+
+// One workgroup: 64 rows x one block of B columns.
+template <int B>
+__global__ __launch_bounds__(kRotThreads) void rotate_kernel(
+    const float* __restrict__ w, int64_t n, int64_t k, int64_t n_ws, int64_t k_up, int m_up,
+    int g0, int phases, float inv_sqrt_b, float* __restrict__ v, float* __restrict__ xup,
+    uint32_t* __restrict__ rmax, uint32_t* __restrict__ flag) {
+  constexpr int LD = B + 1;   // padded row stride: column reads hit distinct banks
+  __shared__ float tile[kPanel * LD];
+  const int tid = threadIdx.x;
+  const int64_t panel = blockIdx.x;
+  const int64_t b = blockIdx.y;
+  const int64_t r0 = panel * kPanel;
+  bool bad = false;
+  // Load 64 rows x B columns (coalesced along the row).
+  for (int idx = tid; idx < kPanel * B; idx += kRotThreads) {
+    const int rr = idx / B;
+    const int t = idx % B;
+    const int64_t r = r0 + rr;
+    float val = 0.0f;
+    if (r < n) {
+      val = w[r * k + b * B + t];
+      bad |= !isfinite(val);
+    }
+    tile[rr * LD + t] = val;
+  }
+  if (bad) atomicOr(flag, 1u);
+  __syncthreads();
+  // Fast Walsh-Hadamard transform, stage spans h = 1, 2, ..., B/2.
+  for (int h = 1; h < B; h <<= 1) {
+    for (int idx = tid; idx < kPanel * (B / 2); idx += kRotThreads) {
+      const int rr = idx / (B / 2);
+      const int pr = idx % (B / 2);
+      const int j = (pr / h) * (2 * h) + (pr % h);
+      const float a = tile[rr * LD + j];
+      const float c = tile[rr * LD + j + h];
+      tile[rr * LD + j] = a + c;
+      tile[rr * LD + j + h] = a - c;
+    }
+    __syncthreads();
+  }
+  // Scale, store rows-contiguous per t, copy unit-impulse samples, row max.
+  const int rr = tid % kPanel;
+  const int tq = tid / kPanel;   // 0..3
+  for (int t = tq; t < B; t += kRotThreads / kPanel) {
+    const float val = tile[rr * LD + t] * inv_sqrt_b;
+    tile[rr * LD + t] = val;
+    v[(b * B + t) * n_ws + r0 + rr] = val;
+  }
+  __syncthreads();
+  const int stride = B / g0;
+  float mx = 0.0f;
+  const int64_t xbase = (panel * k_up + b * m_up) * kPanel + rr;
+  for (int i = tq; i < g0; i += kRotThreads / kPanel) {
+    const float val = tile[rr * LD + i * stride];
+    xup[xbase + static_cast<int64_t>(i) * phases * kPanel] = val;
+    mx = fmaxf(mx, fabsf(val));
+  }
+  if (r0 + rr < n) atomicMax(&rmax[r0 + rr], __float_as_uint(mx));
+}
+
+// Batched VALU GEMM over (block, row tile, sample tile).  Thread (tx, ty)
+// owns rows ty*8 .. ty*8+7 and tile columns tx*8 .. tx*8+7.
+__global__ __launch_bounds__(kUpThreads) void upsample_kernel(
+    const float* __restrict__ v, const float* __restrict__ unz, int64_t n, int64_t n_ws,
+    int64_t k_up, int B, int m_up, int phases, int m_nz, int m_nz_pad, float* __restrict__ xup,
+    uint32_t* __restrict__ rmax) {
+  __shared__ float As[kUpBK][kUpBM];
+  __shared__ float Bs[kUpBK][kUpBN];
+  const int tid = threadIdx.x;
+  const int tx = tid % 8;
+  const int ty = tid / 8;
+  const int64_t rt = blockIdx.x;     // row tile
+  const int jt = blockIdx.y;         // sample tile
+  const int64_t b = blockIdx.z;      // block
+  const int64_t r0 = rt * kUpBM;
+  const int j0 = jt * kUpBN;
+  float acc[8][8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i)
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc[i][j] = 0.0f;
+
+  const float* vblk = v + b * B * n_ws;
+  for (int t0 = 0; t0 < B; t0 += kUpBK) {
+    // Stage A: kUpBK x 128 floats, B: kUpBK x 64 floats (float4 loads).
+#pragma unroll
+    for (int q = 0; q < (kUpBK * kUpBM / 4) / kUpThreads; ++q) {
+      const int idx = q * kUpThreads + tid;
+      const int tt = idx / (kUpBM / 4);
+      const int c4 = idx % (kUpBM / 4);
+      const float4 val = *reinterpret_cast<const float4*>(vblk + (t0 + tt) * n_ws + r0 + c4 * 4);
+      *reinterpret_cast<float4*>(&As[tt][c4 * 4]) = val;
+    }
+#pragma unroll
+    for (int q = 0; q < (kUpBK * kUpBN / 4) / kUpThreads; ++q) {
+      const int idx = q * kUpThreads + tid;
+      const int tt = idx / (kUpBN / 4);
+      const int c4 = idx % (kUpBN / 4);
+      const float4 val = *reinterpret_cast<const float4*>(unz + (t0 + tt) * m_nz_pad + j0 + c4 * 4);
+      *reinterpret_cast<float4*>(&Bs[tt][c4 * 4]) = val;
+    }
+    __syncthreads();
+#pragma unroll 4
+    for (int tt = 0; tt < kUpBK; ++tt) {
+      const float4 a0 = *reinterpret_cast<const float4*>(&As[tt][ty * 8]);
+      const float4 a1 = *reinterpret_cast<const float4*>(&As[tt][ty * 8 + 4]);
+      const float4 b0 = *reinterpret_cast<const float4*>(&Bs[tt][tx * 8]);
+      const float4 b1 = *reinterpret_cast<const float4*>(&Bs[tt][tx * 8 + 4]);
+      const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+      const float c[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+#pragma unroll
+      for (int i = 0; i < 8; ++i)
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          const float prod = a[i] * c[j];
+          acc[i][j] = acc[i][j] + prod;
+        }
+    }
+    __syncthreads();
+  }
+  // Store: sample j -> m = (j / (P-1)) * P + j % (P-1) + 1; rows are contiguous.
+  float mx[8];
+#pragma unroll
+  for (int i = 0; i < 8; ++i) mx[i] = 0.0f;
+  const int64_t rbase = r0 + ty * 8;          // 8 rows inside one panel
+  const int64_t panel = rbase / kPanel;
+  const int lane_row = static_cast<int>(rbase % kPanel);
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int jj = j0 + tx * 8 + j;
+    if (jj < m_nz) {
+      const int m = (jj / (phases - 1)) * phases + jj % (phases - 1) + 1;
+      float* dst = xup + (panel * k_up + b * m_up + m) * kPanel + lane_row;
+      *reinterpret_cast<float4*>(dst) = make_float4(acc[0][j], acc[1][j], acc[2][j], acc[3][j]);
+      *reinterpret_cast<float4*>(dst + 4) = make_float4(acc[4][j], acc[5][j], acc[6][j], acc[7][j]);
+#pragma unroll
+      for (int i = 0; i < 8; ++i) mx[i] = fmaxf(mx[i], fabsf(acc[i][j]));
+    }
+  }
+  // Reduce the maxima over the 8 threads (tx) that share these rows.
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    float val = mx[i];
+    val = fmaxf(val, __shfl_xor(val, 1));
+    val = fmaxf(val, __shfl_xor(val, 2));
+    val = fmaxf(val, __shfl_xor(val, 4));
+    mx[i] = val;
+  }
+  if (tx == 0) {
+#pragma unroll
+    for (int i = 0; i < 8; ++i)
+      if (rbase + i < n) atomicMax(&rmax[rbase + i], __float_as_uint(mx[i]));
+  }
+}
+
+// One wave per (panel, block) chain set: lane = row.  Words of 32 / bits codes
+// never straddle blocks because M is a multiple of 32.
+template <int LEVELS>
+__global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
+    const float* __restrict__ xup, const uint32_t* __restrict__ rmax, int64_t n, int64_t nb,
+    int64_t k_up, int m_up, int64_t n_chunks, uint32_t* __restrict__ codes,
+    float* __restrict__ scales, uint32_t* __restrict__ flag) {
+  constexpr int BITS = LEVELS == 2 ? 1 : 2;
+  constexpr int PER_WORD = 32 / BITS;
+  constexpr int WORDS_PER_CHUNK = 4;
+  const int lane = threadIdx.x % 64;
+  const int64_t b = static_cast<int64_t>(blockIdx.y) * kScanWaves + threadIdx.x / 64;
+  const int64_t panel = blockIdx.x;
+  if (b >= nb) return;
+  const int64_t r = panel * kPanel + lane;
+  const bool live = r < n;
+  const float s = live ? __uint_as_float(rmax[r]) : 0.0f;
+  if (live && b == 0) {
+    scales[r] = s;
+    if (!isfinite(s)) atomicOr(flag, 1u);
+  }
+  const float theta = s * 0.5f;
+  const float* src = xup + (panel * k_up + b * m_up) * kPanel + lane;
+  uint32_t* dst_row = codes + (panel * n_chunks * kPanel + lane) * WORDS_PER_CHUNK;
+  float u = 0.0f;
+  int64_t wj = (b * m_up) / PER_WORD;   // first word of this block in the row
+  for (int m0 = 0; m0 < m_up; m0 += PER_WORD, ++wj) {
+    uint32_t word = 0u;
+    if (live) {
+#pragma unroll 8
+      for (int q = 0; q < PER_WORD; ++q) {
+        const float x = src[static_cast<int64_t>(m0 + q) * kPanel];
+        const float vv = u + x;
+        int c;
+        if (LEVELS == 3) c = (vv > theta) ? 1 : ((vv < -theta) ? -1 : 0);
+        else c = (vv >= 0.0f) ? 1 : -1;
+        const float cs = static_cast<float>(c) * s;
+        u = vv - cs;
+        uint32_t f;
+        if (LEVELS == 3) f = c == 0 ? 0u : (c > 0 ? 1u : 3u);
+        else f = c > 0 ? 1u : 0u;
+        word |= f << (BITS * q);
+      }
+    }
+    const int64_t c = wj / WORDS_PER_CHUNK;
+    dst_row[c * kPanel * WORDS_PER_CHUNK + (wj % WORDS_PER_CHUNK)] = word;
+  }
+  if (b == nb - 1) {
+    // Zero the padding words after the last code of the row.
+    const int64_t total_words = n_chunks * WORDS_PER_CHUNK;
+    for (; wj < total_words; ++wj) {
+      const int64_t c = wj / WORDS_PER_CHUNK;
+      dst_row[c * kPanel * WORDS_PER_CHUNK + (wj % WORDS_PER_CHUNK)] = 0u;
+    }
+  }
+}
+
+}  // namespace
+
+sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
+                           float* scales, const QuantWs& ws, hipStream_t stream) {
+  const int64_t n_panels = L->n_pad / kPanel;
+  const int64_t n_ws = quant_ws_rows(L);     // rows covered by the upsample tiles
+  const int B = L->block;
+  const float inv_sqrt_b = static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
+  clear_kernel<<<dim3(static_cast<unsigned>((L->n_pad + 255) / 256)), dim3(256), 0, stream>>>(
+      ws.flag, ws.rmax, L->n_pad);
+  const dim3 rgrid(static_cast<unsigned>(n_ws / kPanel), static_cast<unsigned>(L->nb));
+  switch (B) {
+    case 64:
+      rotate_kernel<64><<<rgrid, dim3(kRotThreads), 0, stream>>>(
+          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, inv_sqrt_b, ws.v, ws.xup,
+          ws.rmax, ws.flag);
+      break;
+    case 128:
+      rotate_kernel<128><<<rgrid, dim3(kRotThreads), 0, stream>>>(
+          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, inv_sqrt_b, ws.v, ws.xup,
+          ws.rmax, ws.flag);
+      break;
+    default:
+      rotate_kernel<256><<<rgrid, dim3(kRotThreads), 0, stream>>>(
+          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, inv_sqrt_b, ws.v, ws.xup,
+          ws.rmax, ws.flag);
+      break;
+  }
+  if (T->m_nz > 0) {
+    const dim3 ugrid(static_cast<unsigned>(n_ws / kUpBM),
+                     static_cast<unsigned>(T->m_nz_pad / kUpBN), static_cast<unsigned>(L->nb));
+    upsample_kernel<<<ugrid, dim3(kUpThreads), 0, stream>>>(
+        ws.v, T->unz, L->n, n_ws, L->k_up, B, L->m_up, T->phases, T->m_nz, T->m_nz_pad, ws.xup,
+        ws.rmax);
+  }
+  const dim3 sgrid(static_cast<unsigned>(n_panels), static_cast<unsigned>((L->nb + kScanWaves - 1) / kScanWaves));
+  if (L->levels == 3)
+    scan_kernel<3><<<sgrid, dim3(64 * kScanWaves), 0, stream>>>(
+        ws.xup, ws.rmax, L->n, L->nb, L->k_up, L->m_up, L->n_chunks, static_cast<uint32_t*>(codes),
+        scales, ws.flag);
+  else
+    scan_kernel<2><<<sgrid, dim3(64 * kScanWaves), 0, stream>>>(
+        ws.xup, ws.rmax, L->n, L->nb, L->k_up, L->m_up, L->n_chunks, static_cast<uint32_t*>(codes),
+        scales, ws.flag);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "encoder launch");
+  return SDQ_OK;
+}
+
+}  // namespace sdq

@@ -1,0 +1,494 @@
+// libsdq host side: argument validation, geometry, coefficient tables,
+// MultiOSR allocation and dispatch to the HIP kernels.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <map>
+#include <mutex>
+#include <numeric>
+#include <string>
+#include <tuple>
+#include <vector>
+
+#include "sdq_internal.h"
+
+namespace sdq {
+
+static thread_local std::string g_last_error;
+
+sdq_status set_error(sdq_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof(buf), fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return st;
+}
+
+sdq_status hip_error(hipError_t e, const char* what) {
+  return set_error(SDQ_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+// ---------------------------------------------------------------------------
+// Coefficients.  The upsampling Resample of Algorithm 1 is the band-limited
+// periodic interpolation of the block; output sample m sits at position
+// m*B/M of the input grid, so its weight on input t is the periodic sinc
+// evaluated at tau = (m*B - t*M)/M (taken mod B).  Decimation (Resample back
+// to B) has the analogous closed form with the folded Nyquist term.
+// ---------------------------------------------------------------------------
+double upsample_kernel(int64_t p, int block, int m_up) {
+  if (p == 0) return 1.0;
+  if (p % m_up == 0) return 0.0;
+  const double tau = static_cast<double>(p) / static_cast<double>(m_up);
+  return std::sin(M_PI * tau) / (static_cast<double>(block) * std::tan(M_PI * tau / block));
+}
+
+double downsample_entry(int64_t m, int64_t t, int block, int m_up) {
+  if (m_up == block) return m == t ? 1.0 : 0.0;
+  const int64_t num = m * block - t * m_up;
+  double val;
+  if (num % m_up == 0) {
+    const int64_t k = num / m_up;
+    val = ((k % block == 0) ? static_cast<double>(block) : 0.0) + ((k % 2 == 0) ? 1.0 : -1.0);
+  } else {
+    const double tau = static_cast<double>(num) / static_cast<double>(m_up);
+    val = std::sin(M_PI * tau) / std::tan(M_PI * tau / block) + std::cos(M_PI * tau);
+  }
+  return val / m_up;
+}
+
+static int64_t gcd64(int64_t a, int64_t b) {
+  while (b) {
+    const int64_t t = a % b;
+    a = b;
+    b = t;
+  }
+  return a;
+}
+
+constexpr int kUpsampleTileN = 64;   // column tile of the upsampling kernel
+
+static std::mutex g_tables_mutex;
+static std::map<std::tuple<int, int, int>, Tables> g_tables;
+
+sdq_status get_tables(int block, int m_up, const Tables** out) {
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_error(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_tables_mutex);
+  auto key = std::make_tuple(dev, block, m_up);
+  auto it = g_tables.find(key);
+  if (it != g_tables.end()) {
+    *out = &it->second;
+    return SDQ_OK;
+  }
+  Tables T;
+  T.block = block;
+  T.m_up = m_up;
+  T.g0 = static_cast<int>(gcd64(block, m_up));
+  T.phases = m_up / T.g0;
+  T.m_nz = m_up - T.g0;
+  T.m_nz_pad = (T.m_nz + kUpsampleTileN - 1) / kUpsampleTileN * kUpsampleTileN;
+  // fp32 kernel values indexed by p = (m*B - t*M) mod (B*M): rounded once from fp64.
+  const int64_t bm = static_cast<int64_t>(block) * m_up;
+  std::vector<float> unz(static_cast<size_t>(block) * std::max(T.m_nz_pad, 1), 0.0f);
+  for (int t = 0; t < block; ++t) {
+    int j = 0;
+    for (int m = 0; m < m_up; ++m) {
+      if (m % T.phases == 0) continue;   // unit-impulse samples are copied, not summed
+      const int64_t p = ((static_cast<int64_t>(m) * block - static_cast<int64_t>(t) * m_up) % bm + bm) % bm;
+      unz[static_cast<size_t>(t) * T.m_nz_pad + j] = static_cast<float>(upsample_kernel(p, block, m_up));
+      ++j;
+    }
+  }
+  std::vector<float> dm(static_cast<size_t>(m_up) * block);
+  for (int m = 0; m < m_up; ++m)
+    for (int t = 0; t < block; ++t)
+      dm[static_cast<size_t>(m) * block + t] = static_cast<float>(downsample_entry(m, t, block, m_up));
+  if (T.m_nz > 0) {
+    e = hipMalloc(&T.unz, unz.size() * sizeof(float));
+    if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
+    e = hipMemcpy(T.unz, unz.data(), unz.size() * sizeof(float), hipMemcpyHostToDevice);
+    if (e != hipSuccess) return hip_error(e, "table upload");
+  }
+  e = hipMalloc(&T.dmat, dm.size() * sizeof(float));
+  if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
+  e = hipMemcpy(T.dmat, dm.data(), dm.size() * sizeof(float), hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_error(e, "table upload");
+  // E^T[m][t] = sum_u Had[t][u] D[m][u]: a Walsh-Hadamard transform of each row
+  // of D (fp64), scaled by 1/sqrt(B), split into two fp16 terms.
+  std::vector<uint16_t> eh(dm.size()), el(dm.size());
+  std::vector<double> row(block);
+  const double inv_sqrt_b = 1.0 / std::sqrt(static_cast<double>(block));
+  for (int m = 0; m < m_up; ++m) {
+    for (int t = 0; t < block; ++t) row[t] = downsample_entry(m, t, block, m_up);
+    for (int h = 1; h < block; h <<= 1)
+      for (int i = 0; i < block; i += 2 * h)
+        for (int j = i; j < i + h; ++j) {
+          const double a = row[j], c = row[j + h];
+          row[j] = a + c;
+          row[j + h] = a - c;
+        }
+    for (int t = 0; t < block; ++t) {
+      const double val = row[t] * inv_sqrt_b;
+      const _Float16 hi = static_cast<_Float16>(val);
+      const _Float16 lo = static_cast<_Float16>(val - static_cast<double>(hi));
+      std::memcpy(&eh[static_cast<size_t>(m) * block + t], &hi, 2);
+      std::memcpy(&el[static_cast<size_t>(m) * block + t], &lo, 2);
+    }
+  }
+  for (uint16_t** dst : {&T.et_hi, &T.et_lo}) {
+    e = hipMalloc(dst, eh.size() * 2);
+    if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
+  }
+  e = hipMemcpy(T.et_hi, eh.data(), eh.size() * 2, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(T.et_lo, el.data(), el.size() * 2, hipMemcpyHostToDevice);
+  if (e != hipSuccess) return hip_error(e, "table upload");
+  auto res = g_tables.emplace(key, T);
+  *out = &res.first->second;
+  return SDQ_OK;
+}
+
+static bool valid_block(int b) { return b == 64 || b == 128 || b == 256; }
+
+static sdq_status check_layout(const sdq_layout* L) {
+  if (!L) return set_error(SDQ_ERR_ARG, "layout is NULL");
+  if (L->n < 0 || L->k <= 0 || !valid_block(L->block) || L->k % L->block ||
+      (L->levels != 2 && L->levels != 3) || L->m_up < L->block || L->m_up % 32 ||
+      L->nb != L->k / L->block || L->k_up != L->nb * L->m_up ||
+      L->bits != (L->levels == 2 ? 1 : 2) ||
+      L->codes_per_chunk != kChunkBytes * 8 / L->bits ||
+      L->n_chunks != (L->k_up + L->codes_per_chunk - 1) / L->codes_per_chunk ||
+      L->n_pad != (L->n + kPanel - 1) / kPanel * kPanel)
+    return set_error(SDQ_ERR_ARG, "layout is not one produced by sdq_layout_init");
+  return SDQ_OK;
+}
+
+size_t quant_ws_layout(const sdq_layout* L, QuantWs* ws, void* base) {
+  char* p = static_cast<char*>(base);
+  size_t off = 0;
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return p ? p + at : nullptr;
+  };
+  QuantWs w;
+  w.flag = reinterpret_cast<uint32_t*>(take(256));
+  w.rmax = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(L->n_pad) * 4));
+  const size_t rows = static_cast<size_t>(quant_ws_rows(L));
+  w.v = reinterpret_cast<float*>(take(rows * L->k * 4));
+  w.xup = reinterpret_cast<float*>(take(rows * L->k_up * 4));
+  if (ws) *ws = w;
+  return off;
+}
+
+}  // namespace sdq
+
+using namespace sdq;
+
+extern "C" {
+
+int32_t sdq_version(void) { return 100; }
+
+const char* sdq_status_string(sdq_status s) {
+  switch (s) {
+    case SDQ_OK: return "ok";
+    case SDQ_ERR_ARG: return "invalid argument";
+    case SDQ_ERR_SHAPE: return "unsupported shape";
+    case SDQ_ERR_OSR: return "unsupported oversampling ratio";
+    case SDQ_ERR_LEVELS: return "levels must be 2 or 3";
+    case SDQ_ERR_NONFINITE: return "non-finite weight";
+    case SDQ_ERR_WORKSPACE: return "workspace missing or too small";
+    case SDQ_ERR_HIP: return "HIP runtime error";
+    case SDQ_ERR_NOMEM: return "out of device memory";
+    case SDQ_ERR_UNSUPPORTED: return "unsupported request";
+  }
+  return "unknown status";
+}
+
+const char* sdq_last_error(void) { return g_last_error.c_str(); }
+
+sdq_status sdq_layout_init(sdq_layout* out, int64_t n, int64_t k, double osr, int32_t levels,
+                           int32_t block) {
+  if (!out) return set_error(SDQ_ERR_ARG, "out is NULL");
+  if (block == 0) block = 256;
+  if (n < 0 || k <= 0) return set_error(SDQ_ERR_ARG, "need n >= 0 and k > 0 (n=%lld k=%lld)",
+                                        (long long)n, (long long)k);
+  if (!valid_block(block)) return set_error(SDQ_ERR_SHAPE, "block must be 64, 128 or 256");
+  if (k % block) return set_error(SDQ_ERR_SHAPE, "k=%lld is not a multiple of the block %d",
+                                  (long long)k, block);
+  if (levels != 2 && levels != 3) return set_error(SDQ_ERR_LEVELS, "levels=%d", levels);
+  if (!(osr >= 1.0) || !(osr <= 8.0))
+    return set_error(SDQ_ERR_OSR, "osr must be within [1, 8]");
+  const double mf = std::nearbyint(osr * block);
+  const int32_t m_up = static_cast<int32_t>(mf);
+  if (m_up < block || m_up % 32)
+    return set_error(SDQ_ERR_OSR, "M = round(osr*B) = %d must be a multiple of 32 and >= B", m_up);
+  sdq_layout L;
+  std::memset(&L, 0, sizeof(L));
+  L.n = n;
+  L.k = k;
+  L.block = block;
+  L.m_up = m_up;
+  L.levels = levels;
+  L.bits = levels == 2 ? 1 : 2;
+  L.nb = k / block;
+  L.k_up = L.nb * m_up;
+  L.n_pad = (n + kPanel - 1) / kPanel * kPanel;
+  L.codes_per_chunk = kChunkBytes * 8 / L.bits;
+  L.n_chunks = (L.k_up + L.codes_per_chunk - 1) / L.codes_per_chunk;
+  *out = L;
+  return SDQ_OK;
+}
+
+size_t sdq_codes_bytes(const sdq_layout* L) {
+  if (!L) return 0;
+  return static_cast<size_t>(L->n_pad) * L->n_chunks * kChunkBytes;
+}
+
+double sdq_compression_ratio(const sdq_layout* L) {
+  if (!L || !L->block) return 0.0;
+  return L->bits * (static_cast<double>(L->m_up) / L->block) / 16.0;
+}
+
+size_t sdq_quantize_workspace_bytes(const sdq_layout* L) {
+  if (check_layout(L) != SDQ_OK) return 0;
+  return quant_ws_layout(L, nullptr, nullptr);
+}
+
+sdq_status sdq_quantize(const float* w, const sdq_layout* L, void* codes, float* scales,
+                        void* ws, size_t ws_bytes, void* stream) {
+  sdq_status st = check_layout(L);
+  if (st != SDQ_OK) return st;
+  if (L->n > 0 && (!w || !codes || !scales))
+    return set_error(SDQ_ERR_ARG, "w, codes and scales must be non-NULL");
+  const size_t need = quant_ws_layout(L, nullptr, nullptr);
+  if (!ws || ws_bytes < need)
+    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (L->n == 0) return SDQ_OK;
+  const Tables* T = nullptr;
+  st = get_tables(L->block, L->m_up, &T);
+  if (st != SDQ_OK) return st;
+  QuantWs qw;
+  quant_ws_layout(L, &qw, ws);
+  return launch_quantize(w, L, T, codes, scales, qw, static_cast<hipStream_t>(stream));
+}
+
+sdq_status sdq_quantize_check(const void* ws, void* stream) {
+  if (!ws) return set_error(SDQ_ERR_ARG, "workspace is NULL");
+  hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_error(e, "hipStreamSynchronize");
+  uint32_t flag = 0;
+  e = hipMemcpy(&flag, ws, sizeof(flag), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_error(e, "reading the status flag");
+  if (flag) return set_error(SDQ_ERR_NONFINITE, "a weight or an upsampled sample is not finite");
+  return SDQ_OK;
+}
+
+size_t sdq_linear_workspace_bytes(const sdq_layout* L, int64_t m) {
+  if (check_layout(L) != SDQ_OK || m < 0) return 0;
+  if (m == 0) return 0;
+  return m <= 16 ? decode_ws_bytes(L, m) : prefill_ws_bytes(L, m);
+}
+
+sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
+                      const float* scales, const sdq_layout* L, float* y, void* ws,
+                      size_t ws_bytes, void* stream) {
+  sdq_status st = check_layout(L);
+  if (st != SDQ_OK) return st;
+  if (m < 0) return set_error(SDQ_ERR_ARG, "m < 0");
+  if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
+  if (m == 0 || L->n == 0) return SDQ_OK;
+  if (!x || !codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+  const size_t need = m <= 16 ? decode_ws_bytes(L, m) : prefill_ws_bytes(L, m);
+  if (!ws || ws_bytes < need)
+    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  const Tables* T = nullptr;
+  st = get_tables(L->block, L->m_up, &T);
+  if (st != SDQ_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (m <= 16) return launch_decode(x, xt, m, codes, scales, L, T, y, ws, ws_bytes, s);
+  return launch_prefill(x, xt, m, codes, scales, L, T, y, ws, ws_bytes, s);
+}
+
+// ---------------------------------------------------------------------------
+// MultiOSR (Section 3.4), host only.
+// ---------------------------------------------------------------------------
+static double weighted_clip(double scale, const std::vector<double>& sc,
+                            const std::vector<double>& wt, double lo, double hi) {
+  double tot = 0.0;
+  for (size_t i = 0; i < sc.size(); ++i) {
+    const double val = std::isinf(sc[i]) ? hi : std::min(std::max(scale * sc[i], lo), hi);
+    tot += wt[i] * val;
+  }
+  return tot;
+}
+
+static std::vector<double> allocate(const std::vector<double>& sc, const std::vector<double>& wt,
+                                    double target, double lo, double hi) {
+  const size_t n = sc.size();
+  if (target <= lo) return std::vector<double>(n, lo);
+  if (target >= hi) return std::vector<double>(n, hi);
+  double wsum = 0.0;
+  for (double w : wt) wsum += w;
+  double min_finite = INFINITY;
+  for (double s : sc)
+    if (!std::isinf(s)) min_finite = std::min(min_finite, s);
+  if (std::isinf(min_finite)) return std::vector<double>(n, hi);
+  double c_lo = 0.0, c_hi = hi / min_finite;
+  const double goal = target * wsum;
+  for (int it = 0; it < 200; ++it) {
+    const double mid = 0.5 * (c_lo + c_hi);
+    if (weighted_clip(mid, sc, wt, lo, hi) < goal) c_lo = mid;
+    else c_hi = mid;
+  }
+  std::vector<double> out(n);
+  for (size_t i = 0; i < n; ++i)
+    out[i] = std::isinf(sc[i]) ? hi : std::min(std::max(c_hi * sc[i], lo), hi);
+  return out;
+}
+
+sdq_status sdq_multiosr(const double* var, const int64_t* np, const int32_t* layer, int64_t count,
+                        double target, double lo, double hi, double grid, double* out) {
+  if (count < 0) return set_error(SDQ_ERR_ARG, "count < 0");
+  if (!(lo > 0) || !(lo <= target) || !(target <= hi) || !(grid > 0))
+    return set_error(SDQ_ERR_ARG, "need 0 < lo <= target <= hi and grid > 0");
+  if (count == 0) return SDQ_OK;
+  if (!var || !np || !layer || !out) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+  for (int64_t j = 0; j < count; ++j)
+    if (np[j] <= 0) return set_error(SDQ_ERR_ARG, "parameter count of linear %lld is <= 0", (long long)j);
+  // Layer level: score 1 / (parameter-weighted variance).
+  std::vector<int32_t> layers(layer, layer + count);
+  std::sort(layers.begin(), layers.end());
+  layers.erase(std::unique(layers.begin(), layers.end()), layers.end());
+  std::vector<double> lay_sc, lay_n;
+  std::vector<std::vector<int64_t>> members(layers.size());
+  for (size_t l = 0; l < layers.size(); ++l) {
+    int64_t n_l = 0;
+    double acc = 0.0;
+    for (int64_t j = 0; j < count; ++j)
+      if (layer[j] == layers[l]) {
+        members[l].push_back(j);
+        n_l += np[j];
+        acc += static_cast<double>(np[j]) * var[j];
+      }
+    const double pooled = acc / static_cast<double>(n_l);
+    lay_n.push_back(static_cast<double>(n_l));
+    lay_sc.push_back(pooled <= 0 ? INFINITY : 1.0 / pooled);
+  }
+  const std::vector<double> lay_osr = allocate(lay_sc, lay_n, target, lo, hi);
+  // Linear level: score n_j / var_j inside each layer.
+  std::vector<double> cont(count);
+  for (size_t l = 0; l < layers.size(); ++l) {
+    std::vector<double> sc, wt;
+    for (int64_t j : members[l]) {
+      sc.push_back(var[j] <= 0 ? INFINITY : static_cast<double>(np[j]) / var[j]);
+      wt.push_back(static_cast<double>(np[j]));
+    }
+    const std::vector<double> v = allocate(sc, wt, lay_osr[l], lo, hi);
+    for (size_t i = 0; i < members[l].size(); ++i) cont[members[l][i]] = v[i];
+  }
+  // Snap: floor to the grid, then add steps by decreasing remainder within the budget.
+  const int64_t k_lo = static_cast<int64_t>(std::ceil(lo / grid - 1e-9));
+  const int64_t k_hi = static_cast<int64_t>(std::floor(hi / grid + 1e-9));
+  std::vector<int64_t> ks(count);
+  std::vector<double> rem(count);
+  int64_t ntot = 0, used = 0;
+  for (int64_t j = 0; j < count; ++j) {
+    const double q = cont[j] / grid;
+    int64_t k = static_cast<int64_t>(std::floor(q + 1e-9));
+    k = std::min(std::max(k, k_lo), k_hi);
+    ks[j] = k;
+    rem[j] = q - static_cast<double>(k);
+    ntot += np[j];
+    used += np[j] * k;
+  }
+  const double budget = target / grid * static_cast<double>(ntot);
+  std::vector<int64_t> order(count);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int64_t a, int64_t b) {
+    if (rem[a] != rem[b]) return rem[a] > rem[b];
+    return a < b;
+  });
+  for (int64_t j : order) {
+    if (ks[j] + 1 <= k_hi && static_cast<double>(used + np[j]) <= budget) {
+      ks[j] += 1;
+      used += np[j];
+    }
+  }
+  for (int64_t j = 0; j < count; ++j) out[j] = static_cast<double>(ks[j]) * grid;
+  return SDQ_OK;
+}
+
+sdq_status sdq_unpack_codes(const sdq_layout* L, const void* codes_host, int8_t* out) {
+  sdq_status st = check_layout(L);
+  if (st != SDQ_OK) return st;
+  if (L->n > 0 && (!codes_host || !out)) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+  const uint32_t* words = static_cast<const uint32_t*>(codes_host);
+  const int bits = L->bits;
+  const int per_word = 32 / bits;
+  const uint32_t mask = (1u << bits) - 1u;
+  for (int64_t r = 0; r < L->n; ++r) {
+    for (int64_t j = 0; j < L->k_up; ++j) {
+      const int64_t c = j / L->codes_per_chunk;
+      const int64_t q = j % L->codes_per_chunk;
+      const int64_t chunk = ((r / kPanel) * L->n_chunks + c) * kPanel + (r % kPanel);
+      const uint32_t wv = words[chunk * 4 + q / per_word];
+      const uint32_t f = (wv >> (bits * (q % per_word))) & mask;
+      int8_t v;
+      if (bits == 1) v = f ? 1 : -1;
+      else v = f == 1 ? 1 : (f == 3 ? -1 : 0);
+      out[r * L->k_up + j] = v;
+    }
+  }
+  return SDQ_OK;
+}
+
+sdq_status sdq_upsample_table(int32_t block, int32_t m_up, float* out) {
+  if (!out) return set_error(SDQ_ERR_ARG, "out is NULL");
+  if (!valid_block(block)) return set_error(SDQ_ERR_SHAPE, "block must be 64, 128 or 256");
+  if (m_up < block || m_up % 32 || m_up > 8 * block) return set_error(SDQ_ERR_OSR, "bad M=%d", m_up);
+  const int64_t bm = static_cast<int64_t>(block) * m_up;
+  for (int64_t p = 0; p < bm; ++p) out[p] = static_cast<float>(upsample_kernel(p, block, m_up));
+  return SDQ_OK;
+}
+
+sdq_status sdq_prepare(int32_t block, int32_t m_up) {
+  if (!valid_block(block)) return set_error(SDQ_ERR_SHAPE, "block must be 64, 128 or 256");
+  if (m_up < block || m_up % 32 || m_up > 8 * block) return set_error(SDQ_ERR_OSR, "bad M=%d", m_up);
+  const Tables* T = nullptr;
+  return get_tables(block, m_up, &T);
+}
+
+void sdq_release_tables(void) {
+  std::lock_guard<std::mutex> lock(g_tables_mutex);
+  for (auto& kv : g_tables) {
+    int cur = 0;
+    (void)hipGetDevice(&cur);
+    (void)hipSetDevice(std::get<0>(kv.first));
+    if (kv.second.unz) (void)hipFree(kv.second.unz);
+    if (kv.second.dmat) (void)hipFree(kv.second.dmat);
+    if (kv.second.et_hi) (void)hipFree(kv.second.et_hi);
+    if (kv.second.et_lo) (void)hipFree(kv.second.et_lo);
+    (void)hipSetDevice(cur);
+  }
+  g_tables.clear();
+}
+
+size_t sdq_moments_workspace_bytes(int64_t count) { return count < 0 ? 0 : moments_ws_bytes(count); }
+
+sdq_status sdq_weight_moments(const float* w, int64_t count, double* out, void* ws, size_t ws_bytes,
+                              void* stream) {
+  if (count <= 0 || !w || !out) return set_error(SDQ_ERR_ARG, "need count > 0 and non-NULL pointers");
+  const size_t need = moments_ws_bytes(count);
+  if (!ws || ws_bytes < need)
+    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  return launch_moments(w, count, out, ws, ws_bytes, static_cast<hipStream_t>(stream));
+}
+
+}  // extern "C"

@@ -1,0 +1,76 @@
+// Internal declarations shared by the libsdq host code and kernel launchers.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstddef>
+#include <cstdint>
+
+#include "../../include/sdq.h"
+
+namespace sdq {
+
+constexpr int kPanel = 64;        // rows per panel of the packed format
+constexpr int kChunkBytes = 16;   // bytes per chunk of the packed format
+
+// Device coefficient tables for one (block, M) pair on one device.
+struct Tables {
+  int block = 0;
+  int m_up = 0;
+  int g0 = 0;          // gcd(B, M): number of samples whose kernel is a unit impulse
+  int phases = 0;      // P = M / g0: samples m with m % P == 0 copy v[(m / P) * (B / g0)]
+  int m_nz = 0;        // M - g0 samples per block computed as dense sums
+  int m_nz_pad = 0;    // m_nz rounded up to the upsample tile width
+  float* unz = nullptr;   // [B][m_nz_pad] fp32 coefficients g(p(t, m_j)), zero padded
+  float* dmat = nullptr;  // [M][B] fp32 decimation matrix D[m][t] (Resample back to B)
+  // E = Had D^T (B x M): x_tilde_b = x_b E.  Stored transposed, [M][B], as an
+  // fp16 pair hi + lo with hi = fp16(E) and lo = fp16(E - hi).
+  uint16_t* et_hi = nullptr;
+  uint16_t* et_lo = nullptr;
+};
+
+// Returns the cached tables for the current device (creating them on first use).
+sdq_status get_tables(int block, int m_up, const Tables** out);
+
+// Host fp64 coefficient helpers (also back the parity entry points).
+double upsample_kernel(int64_t p, int block, int m_up);          // g(p)
+double downsample_entry(int64_t m, int64_t t, int block, int m_up);  // D[m][t]
+
+sdq_status set_error(sdq_status st, const char* fmt, ...);
+sdq_status hip_error(hipError_t e, const char* what);
+
+// Workspace carving for sdq_quantize.
+// n_ws = n rounded up to 128 rows: the row extent of the rotated and
+// upsampled buffers (the upsample kernel works on 128-row tiles).
+struct QuantWs {
+  uint32_t* flag;    // [0]: non-finite flag
+  uint32_t* rmax;    // [n_pad] row maxima as fp32 bit patterns
+  float* v;          // [nb][B][n_ws] rotated weights, rows contiguous
+  float* xup;        // [n_ws / 64][k_up][64] upsampled samples
+};
+inline int64_t quant_ws_rows(const sdq_layout* L) { return (L->n + 127) / 128 * 128; }
+size_t quant_ws_layout(const sdq_layout* L, QuantWs* ws, void* base);
+
+sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
+                           float* scales, const QuantWs& ws, hipStream_t stream);
+
+// Decode path (m <= 16).
+size_t decode_ws_bytes(const sdq_layout* L, int64_t m);
+sdq_status launch_decode(const void* x, sdq_dtype xt, int64_t m, const void* codes,
+                         const float* scales, const sdq_layout* L, const Tables* T, float* y,
+                         void* ws, size_t ws_bytes, hipStream_t stream);
+
+// Prefill path (m > 16).
+size_t prefill_ws_bytes(const sdq_layout* L, int64_t m);
+sdq_status launch_prefill(const void* x, sdq_dtype xt, int64_t m, const void* codes,
+                          const float* scales, const sdq_layout* L, const Tables* T, float* y,
+                          void* ws, size_t ws_bytes, hipStream_t stream);
+
+// Moments (mean, variance) of a device array.
+size_t moments_ws_bytes(int64_t count);
+sdq_status launch_moments(const float* w, int64_t count, double* out, void* ws, size_t ws_bytes,
+                          hipStream_t stream);
+
+inline size_t align_up(size_t x, size_t a) { return (x + a - 1) / a * a; }
+
+}  // namespace sdq

@@ -1,0 +1,166 @@
+"""Host-side checks of the C ABI (no GPU needed): the library loads, exports
+every entry point of include/sdq.h, validates arguments, and its host-only
+functions agree with the oracle."""
+import ctypes
+import os
+import re
+
+import numpy as np
+import pytest
+
+import paper_2510_03275_amd as P
+from paper_2510_03275_amd import binding as Bd
+from oracle import layout as LY
+from oracle import multiosr as MO
+from oracle import resample as R
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    with open(os.path.join(ROOT, "include", "sdq.h")) as f:
+        text = f.read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    names = re.findall(r"\b(sdq_[a-z_0-9]+)\s*\(", text)
+    return sorted(set(names))
+
+
+def test_every_declared_symbol_is_exported():
+    names = _declared_functions()
+    assert len(names) >= 18
+    lib = ctypes.CDLL(Bd.LIB_PATH)
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_layout_struct_size_matches_header():
+    assert ctypes.sizeof(Bd.sdq_layout) == 72
+
+
+@pytest.mark.parametrize("n,k,osr,levels,block,m_up,cpc", [
+    (768, 768, 2.0, 3, 256, 512, 64),
+    (4096, 11008, 1.5, 2, 256, 384, 128),
+    (8192, 28672, 2.0, 3, 256, 512, 64),
+    (1, 256, 1.0, 3, 0, 256, 64),
+    (5, 512, 1.625, 3, 256, 416, 64),
+    (70, 512, 1.5, 2, 64, 96, 128),
+])
+def test_layout_geometry(n, k, osr, levels, block, m_up, cpc):
+    L = P.sdq_layout_init(n, k, osr, levels, block)
+    assert L.m_up == m_up and L.codes_per_chunk == cpc
+    assert L.k_up == (k // L.block) * m_up
+    assert P.sdq_codes_bytes(L) == LY.packed_bytes(n, L.k_up, levels)
+
+
+def test_codes_bytes_of_the_down_proj_workload():
+    L = P.sdq_layout_init(4096, 11008, 1.5, 2)
+    assert P.sdq_codes_bytes(L) == 8_454_144
+
+
+@pytest.mark.parametrize("args,status", [
+    ((10, 300, 2.0, 3, 256), -2),     # K not a multiple of B
+    ((10, 256, 2.0, 3, 100), -2),     # unsupported block
+    ((10, 256, 2.0, 4, 256), -4),     # levels
+    ((10, 256, 0.5, 3, 256), -3),     # OSR < 1
+    ((10, 256, 1.55, 3, 256), -3),    # M not a multiple of 32
+    ((10, 256, float("nan"), 3, 256), -3),
+    ((-1, 256, 2.0, 3, 256), -1),
+    ((10, 0, 2.0, 3, 256), -1),
+])
+def test_layout_rejects(args, status):
+    with pytest.raises(P.SdqError) as ei:
+        P.sdq_layout_init(*args)
+    assert ei.value.status == status
+
+
+def test_quantize_and_linear_reject_bad_arguments_without_gpu_work():
+    L = P.sdq_layout_init(64, 256, 2.0, 3)
+    lib = P.lib()
+    need = lib.sdq_quantize_workspace_bytes(ctypes.byref(L))
+    assert need > 0
+    # workspace too small / missing: rejected before anything is enqueued
+    assert lib.sdq_quantize(ctypes.c_void_p(16), ctypes.byref(L), ctypes.c_void_p(16),
+                            ctypes.c_void_p(16), ctypes.c_void_p(16), need - 1, None) == -6
+    assert lib.sdq_quantize(None, ctypes.byref(L), None, None, ctypes.c_void_p(16), need, None) == -1
+    assert lib.sdq_quantize(None, None, None, None, None, 0, None) == -1
+    bad = Bd.sdq_layout()
+    bad.n, bad.k, bad.block = 64, 256, 256
+    assert lib.sdq_quantize(None, ctypes.byref(bad), None, None, None, 0, None) == -1
+    assert lib.sdq_linear(None, 0, -1, None, None, ctypes.byref(L), None, None, 0, None) == -1
+    assert lib.sdq_linear(None, 7, 1, None, None, ctypes.byref(L), None, None, 0, None) == -1
+    assert lib.sdq_linear(ctypes.c_void_p(16), 0, 1, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                          ctypes.byref(L), ctypes.c_void_p(16), None, 0, None) == -6
+    # m == 0 is a successful no-op
+    assert lib.sdq_linear(None, 0, 0, None, None, ctypes.byref(L), None, None, 0, None) == 0
+    assert lib.sdq_linear_workspace_bytes(ctypes.byref(L), 0) == 0
+    assert lib.sdq_linear_workspace_bytes(ctypes.byref(L), 1) > 0
+    assert lib.sdq_linear_workspace_bytes(ctypes.byref(L), 2048) >= 2048 * 512 * 2
+    assert P.sdq_version() >= 100
+    assert lib.sdq_status_string(-5) == b"non-finite weight"
+
+
+@pytest.mark.parametrize("block,m_up", [(256, 384), (256, 512), (256, 640), (256, 416), (256, 768),
+                                         (128, 192), (128, 256), (64, 96)])
+def test_upsample_table_bit_identical_to_oracle(block, m_up):
+    got = P.sdq_upsample_table(block, m_up)
+    want = R.g_table_f32(block, m_up)
+    assert np.array_equal(got.view(np.uint32), want.view(np.uint32))
+
+
+@pytest.mark.parametrize("levels", [2, 3])
+@pytest.mark.parametrize("n,k,osr", [(1, 256, 2.0), (65, 512, 1.5), (130, 768, 2.5), (3, 512, 1.625)])
+def test_unpack_matches_oracle_packer(levels, n, k, osr):
+    L = P.sdq_layout_init(n, k, osr, levels)
+    rng = np.random.default_rng(n * 7 + levels)
+    vals = [-1, 1] if levels == 2 else [-1, 0, 1]
+    codes = rng.choice(vals, size=(n, L.k_up)).astype(np.int8)
+    buf = LY.pack(codes, levels)
+    assert np.array_equal(P.sdq_unpack_codes(L, buf), codes)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_multiosr_matches_oracle(seed):
+    rng = np.random.default_rng(100 + seed)
+    cnt = int(rng.integers(1, 40))
+    var = np.exp(rng.uniform(np.log(5e-5), np.log(1e-3), cnt))
+    n = rng.integers(1000, 10_000_000, cnt)
+    layers = np.sort(rng.integers(0, 6, cnt))
+    T, lo, hi = [(2.5, 1.5, 3.0), (2.0, 1.0, 4.0), (1.75, 1.5, 2.5)][seed % 3]
+    got = P.sdq_multiosr(var, n, layers, T, lo, hi, 0.125)
+    want = MO.multiosr(list(var), list(int(v) for v in n), list(int(v) for v in layers), T, lo, hi, 0.125)
+    assert np.array_equal(got, np.array(want))
+
+
+def test_multiosr_llama7b_layer_and_70b_stack():
+    import synth
+    for idx in (3, 5):
+        wl = synth.workload(idx)
+        var = [lin.sigma ** 2 for lin in wl.linears]
+        n = [lin.n * lin.k for lin in wl.linears]
+        lay = [lin.layer for lin in wl.linears]
+        T, lo, hi = wl.multiosr
+        got = P.sdq_multiosr(var, n, lay, T, lo, hi)
+        want = MO.multiosr(var, n, lay, T, lo, hi)
+        assert np.array_equal(got, np.array(want))
+        mean = float(np.dot(got, n) / np.sum(n))
+        assert T - 0.125 < mean <= T
+
+
+def test_multiosr_rejects():
+    with pytest.raises(P.SdqError):
+        P.sdq_multiosr([1e-4], [10], [0], 3.5, 1.5, 3.0)
+    with pytest.raises(P.SdqError):
+        P.sdq_multiosr([1e-4], [0], [0], 2.0, 1.5, 3.0)
+
+
+def test_compression_ratio_of_layout():
+    assert abs(P.sdq_compression_ratio(P.sdq_layout_init(8, 512, 2.0, 3)) - 2 * 2.0 / 16) < 1e-15
+    assert abs(P.sdq_compression_ratio(P.sdq_layout_init(8, 512, 1.5, 2)) - 1.5 / 16) < 1e-15
+
+
+def test_single_hip_runtime_in_process():
+    # libsdq must bind to PyTorch's HIP runtime: device pointers and streams
+    # handed over by torch belong to that runtime.
+    import torch  # noqa: F401
+    from synth import gpu  # noqa: F401
+    assert len(Bd.hip_runtimes_loaded()) == 1

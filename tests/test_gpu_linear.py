@@ -1,0 +1,155 @@
+"""GPU parity of sdq_linear (decode GEMV for m <= 16, prefill MFMA GEMM above)
+against the fp64 oracle: per activation row, max_r |y - y*| / max_r |y*| <= 1e-3."""
+import numpy as np
+import pytest
+
+import oracle
+import synth
+from oracle import layout as LY
+from oracle import linear as OL
+from tests.gpu_common import TOL, gpu_encode, host_bytes, require_gpu, to_device_x
+
+pytestmark = pytest.mark.gpu
+
+
+def _oracle_codes_on_device(torch, n, k, osr, levels, seed, block=256):
+    """Codes from the oracle encoder, packed by the oracle packer, uploaded."""
+    import paper_2510_03275_amd as P
+    w = synth.weight_rows(seed, 2, n, k, 0.02, True)
+    r = oracle.encode(w, osr, levels, block)
+    L = P.sdq_layout_init(n, k, osr, levels, block)
+    enc = P.Encoded(L, torch.from_numpy(LY.pack(r.codes, levels)).cuda(), torch.from_numpy(r.scales).cuda())
+    return enc, r
+
+
+def _run_linear(torch, enc, x_dev):
+    import paper_2510_03275_amd as P
+    y = P.linear(x_dev, enc)
+    torch.cuda.synchronize()
+    return y.cpu().numpy().astype(np.float64)
+
+
+SHAPES = [(130, 768, 2.0, 3), (64, 512, 1.5, 2), (100, 512, 1.625, 3), (200, 1024, 2.5, 3),
+          (65, 512, 3.0, 2)]
+
+
+@pytest.mark.parametrize("m", [1, 2, 3, 8, 16, 17, 64, 130])
+@pytest.mark.parametrize("n,k,osr,levels", SHAPES)
+def test_linear_small_f16(n, k, osr, levels, m):
+    torch = require_gpu()
+    enc, r = _oracle_codes_on_device(torch, n, k, osr, levels, seed=n + m)
+    x_dev, x64 = to_device_x(synth.activations_f32(m, 0, m, k), "f16", torch)
+    y = _run_linear(torch, enc, x_dev)
+    y_ref = OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up)
+    err = OL.rel_err_rows(y, y_ref)
+    assert np.all(err <= TOL), err.max()
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("m", [1, 5, 16, 40])
+def test_linear_small_other_dtypes(dtype, m):
+    torch = require_gpu()
+    enc, r = _oracle_codes_on_device(torch, 96, 768, 2.0, 3, seed=7)
+    x_dev, x64 = to_device_x(synth.activations_f32(11, 0, m, 768), dtype, torch)
+    y = _run_linear(torch, enc, x_dev)
+    err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up))
+    assert np.all(err <= TOL), err.max()
+
+
+def test_linear_block_sizes():
+    torch = require_gpu()
+    for block, osr in ((128, 2.0), (64, 1.5)):
+        enc, r = _oracle_codes_on_device(torch, 70, 512, osr, 3, seed=block, block=block)
+        for m in (1, 24):
+            x_dev, x64 = to_device_x(synth.activations_f32(3, 0, m, 512), "f16", torch)
+            y = _run_linear(torch, enc, x_dev)
+            err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, block, r.m_up))
+            assert np.all(err <= TOL), (block, m, err.max())
+
+
+def test_linear_decode_is_deterministic():
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    enc, _ = _oracle_codes_on_device(torch, 4096, 2048, 2.0, 3, seed=1)
+    x_dev, _ = to_device_x(synth.activations_f32(1, 0, 1, 2048), "f16", torch)
+    ws = torch.zeros(P.sdq_linear_workspace_bytes(enc.layout, 1), dtype=torch.uint8, device="cuda")
+    y1 = P.linear(x_dev, enc, workspace=ws)
+    y2 = P.linear(x_dev, enc, workspace=ws)
+    assert torch.equal(y1, y2)
+
+
+def test_linear_empty_batch():
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    enc, _ = _oracle_codes_on_device(torch, 64, 256, 2.0, 3, seed=2)
+    x = torch.empty((0, 256), dtype=torch.float16, device="cuda")
+    assert P.linear(x, enc).shape == (0, 64)
+
+
+def _workload_case(torch, wl, lin, osr, ms, n_sample=32):
+    """GPU: generate W on the device, encode, run the linear at batch m.
+    Oracle: regenerate sampled rows on the host, encode, fp64 linear."""
+    import paper_2510_03275_amd as P
+    from synth import gpu as SG
+    w_dev = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+    enc = gpu_encode(w_dev, osr, wl.levels)
+    del w_dev
+    rng = np.random.default_rng(lin.linear_id + 99)
+    rows = np.unique(np.concatenate([[0, lin.n - 1], rng.choice(lin.n, n_sample, replace=False)]))
+    w_rows = synth.weight_rows(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers, rows=rows)
+    r = oracle.encode(w_rows, osr, wl.levels)
+    for m in ms:
+        x32 = SG.activations_gpu(wl.seed, 100 + m, m, lin.k).cpu().numpy()
+        x_dev, x64 = to_device_x(x32, wl.x_dtype, torch)
+        y = P.linear(x_dev, enc)
+        torch.cuda.synchronize()
+        y_s = y[:, torch.from_numpy(rows).cuda()].cpu().numpy().astype(np.float64)
+        y_ref = OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up)
+        err = OL.rel_err_rows(y_s, y_ref)
+        assert np.all(err <= TOL), (lin.name, m, err.max())
+    torch.cuda.empty_cache()
+
+
+def test_linear_opt125m_q_proj():
+    torch = require_gpu()
+    wl = synth.workload(1)
+    _workload_case(torch, wl, wl.linears[0], wl.osr, wl.batches, n_sample=200)
+
+
+def test_linear_llama7b_down_proj_decode():
+    torch = require_gpu()
+    wl = synth.workload(2)
+    _workload_case(torch, wl, wl.linears[0], wl.osr, wl.batches)
+
+
+@pytest.mark.parametrize("idx", [0, 1, 2])
+def test_linear_llama70b_decode_and_prefill(idx):
+    torch = require_gpu()
+    wl = synth.workload(4)
+    _workload_case(torch, wl, wl.linears[idx], wl.osr, wl.batches + wl.prefill, n_sample=16)
+
+
+def test_linear_llama7b_layer_multiosr():
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    wl = synth.workload(3)
+    var = [lin.sigma ** 2 for lin in wl.linears]
+    n = [lin.n * lin.k for lin in wl.linears]
+    osr = P.sdq_multiosr(var, n, [lin.layer for lin in wl.linears], *wl.multiosr)
+    for lin, o in zip(wl.linears, osr):
+        _workload_case(torch, wl, lin, float(o), wl.batches, n_sample=8)
+
+
+def test_weight_moments_match_oracle():
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    for n, k in ((1, 1), (300, 777), (4096, 4096)):
+        w = synth.weight_rows(n, 0, n, k, 0.02, True) + np.float32(0.5)
+        w_dev = torch.from_numpy(w).cuda()
+        out = torch.zeros(2, dtype=torch.float64, device="cuda")
+        ws = torch.empty(P.sdq_moments_workspace_bytes(w.size), dtype=torch.uint8, device="cuda")
+        P.sdq_weight_moments(w_dev, out, ws)
+        got = out.cpu().numpy()
+        x = w.astype(np.float64)
+        assert abs(got[0] - x.mean()) <= 1e-12 * max(1.0, abs(x.mean()))
+        assert abs(got[1] - oracle.variance_fp64(w)) <= 1e-10 * max(oracle.variance_fp64(w), 1e-30)
