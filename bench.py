@@ -1,0 +1,327 @@
+#!/usr/bin/env python3
+"""Benchmark of the SDQ-LLM hot path on one MI355X.
+
+Headline (one JSON line on stdout): decode throughput of sdq_linear on the
+LLaMA-7B down_proj workload (N=4096 outputs, K=11008 inputs, OSR 1.5, binary
+codes, one fp16 activation row), in GB/s of packed code bytes.
+
+One step = one sdq_linear call = activation expansion + addition-only LUT GEMV
+over the whole layer.  Steps run from HIP graphs (captured through PyTorch) so
+that host launch overhead is not timed, and cycle through enough copies of
+the code buffer to exceed twice the 256 MB last-level cache, so every step
+streams its codes from HBM.  The line also carries:
+
+* roofline  -- the GEMV kernel alone (graph of GEMV launches, HIP events on the
+               launch stream): packed code bytes per launch / average launch time,
+               against the 8 TB/s HBM peak;
+* phases    -- the encoder on the same weight (rows/s, fp32 VALU roofline), the
+               prefill path on the LLaMA-70B 8192x8192 linear at m = 2048 with
+               bf16 activations (TFLOP/s, fp16 MFMA roofline), and MultiOSR on
+               the LLaMA-7B layer's seven linears;
+* cpu_baseline -- the CPU oracle on a bounded sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "sdq_linear decode GB/s (% of HBM peak) and prefill TFLOP/s; rows/s quantized"
+HBM_PEAK_GBS = 8000.0
+MFMA_F16_PEAK_TFLOPS = 2500.0
+# Separately rounded fp32 mul and add (no contraction, no packed fp32):
+# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3 T lane-ops/s.
+VALU_F32_UNFUSED_PEAK_TFLOPS = 256 * 64 * 2.4e9 / 1e12
+MALL_BYTES = 256 * 1024 * 1024
+
+
+def _rotations(nbytes: int) -> int:
+    return max(2, math.ceil(2 * MALL_BYTES / max(nbytes, 1)))
+
+
+def _graph_time(torch, fn_list, replays: int, warm: int = 2):
+    """Capture fn_list (one callable per graph node group) into one graph,
+    replay it `replays` times, return average ms per callable."""
+    g = torch.cuda.CUDAGraph()
+    s = torch.cuda.Stream()
+    s.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(s):
+        for fn in fn_list:   # eager warm-up on the capture stream
+            fn()
+    torch.cuda.current_stream().wait_stream(s)
+    torch.cuda.synchronize()
+    with torch.cuda.graph(g):
+        for fn in fn_list:
+            fn()
+    for _ in range(warm):
+        g.replay()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    start.record()
+    for _ in range(replays):
+        g.replay()
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / (replays * len(fn_list)), g
+
+
+def bench_decode(torch, P, synth, SG, steps: int, warmup: int):
+    wl = synth.workload(2)
+    lin = wl.linears[0]
+    w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+    enc = P.quantize(w, wl.osr, wl.levels)
+    L = enc.layout
+    nbytes = P.sdq_codes_bytes(L)
+    rot = _rotations(nbytes)
+    codes = [enc.codes.clone() for _ in range(rot)]
+    x = SG.activations_gpu(wl.seed, 1, 1, lin.k).to(torch.float16)
+    y = torch.empty((1, lin.n), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.sdq_linear_workspace_bytes(L, 1), dtype=torch.uint8, device="cuda")
+
+    def step(i):
+        return lambda: P.sdq_linear(x, codes[i], enc.scales, L, y, ws)
+
+    # One graph holds one pass over all rotated buffers; K steps = K / rot replays.
+    replays = max(1, steps // rot)
+    steps_run = replays * rot
+    warm_replays = max(1, warmup // rot)
+    ms_step, _ = _graph_time(torch, [step(i) for i in range(rot)], replays, warm_replays)
+
+    # The GEMV alone (x_tilde computed once, left in the workspace).
+    P.sdq_expand_activations(x, L, ws)
+
+    def gemv(i):
+        return lambda: P.sdq_linear_expanded(1, codes[i], enc.scales, L, y, ws)
+
+    ms_gemv, _ = _graph_time(torch, [gemv(i) for i in range(rot)], replays, warm_replays)
+
+    def expand():
+        return P.sdq_expand_activations(x, L, ws)
+
+    ms_exp, _ = _graph_time(torch, [expand] * 16, max(1, replays // 4), 1)
+    torch.cuda.synchronize()
+    del codes
+    torch.cuda.empty_cache()
+    return dict(L=L, enc=enc, w=w, nbytes=nbytes, rot=rot, steps_run=steps_run,
+                ms_step=ms_step, ms_gemv=ms_gemv, ms_expand=ms_exp, wl=wl, lin=lin)
+
+
+def bench_decode_70b(torch, P, synth, SG, replays: int = 20):
+    """Decode at m = 1 on the LLaMA-70B up_proj shape (28672 x 8192, OSR 2, ternary)."""
+    wl = synth.workload(4)
+    lin = wl.linears[1]
+    w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+    enc = P.quantize(w, wl.osr, wl.levels)
+    del w
+    L = enc.layout
+    nbytes = P.sdq_codes_bytes(L)
+    rot = _rotations(nbytes)
+    codes = [enc.codes.clone() for _ in range(rot)]
+    x = SG.activations_gpu(wl.seed, 3, 1, lin.k).to(torch.bfloat16)
+    y = torch.empty((1, lin.n), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.sdq_linear_workspace_bytes(L, 1), dtype=torch.uint8, device="cuda")
+    ms_step, _ = _graph_time(torch, [lambda i=i: P.sdq_linear(x, codes[i], enc.scales, L, y, ws)
+                                     for i in range(rot)], replays, 2)
+    P.sdq_expand_activations(x, L, ws)
+    ms_gemv, _ = _graph_time(torch, [lambda i=i: P.sdq_linear_expanded(1, codes[i], enc.scales, L, y, ws)
+                                     for i in range(rot)], replays, 2)
+    del codes
+    torch.cuda.empty_cache()
+    gemv_gbs = nbytes / (ms_gemv * 1e-3) / 1e9
+    return {"workload": "llama70b_up_proj_28672x8192_osr2_ternary_decode_m1_bf16",
+            "gbs": nbytes / (ms_step * 1e-3) / 1e9, "ms": ms_step, "ms_gemv": ms_gemv,
+            "code_bytes": nbytes, "rotating_code_buffers": rot,
+            "roofline": {"bound": "hbm", "achieved": gemv_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": gemv_gbs / HBM_PEAK_GBS, "traffic": None}}
+
+
+def bench_encoder(torch, P, w, wl, reps: int = 5):
+    L = P.sdq_layout_init(w.shape[0], w.shape[1], wl.osr, wl.levels)
+    codes = torch.empty(P.sdq_codes_bytes(L), dtype=torch.uint8, device="cuda")
+    scales = torch.empty(L.n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.sdq_quantize_workspace_bytes(L), dtype=torch.uint8, device="cuda")
+    P.sdq_quantize(w, L, codes, scales, ws)
+    P.sdq_quantize_check(ws)
+    ms, _ = _graph_time(torch, [lambda: P.sdq_quantize(w, L, codes, scales, ws)] * reps, 3, 1)
+    g0 = math.gcd(L.block, L.m_up)
+    m_nz = L.m_up - g0
+    flops = 2.0 * L.n * L.nb * m_nz * L.block       # separately rounded mul + add per term
+    tflops = flops / (ms * 1e-3) / 1e12
+    del ws
+    return {
+        "workload": "llama7b_down_proj_4096x11008_osr1.5_binary",
+        "rows_per_s": L.n / (ms * 1e-3),
+        "ms": ms,
+        "roofline": {"bound": "alu", "achieved": tflops, "peak": VALU_F32_UNFUSED_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": tflops / VALU_F32_UNFUSED_PEAK_TFLOPS,
+                     "traffic": None, "note": "whole sdq_quantize call (4 kernels); flops = "
+                     "2 * rows * blocks * dense samples per block * B"},
+    }
+
+
+def bench_prefill(torch, P, synth, SG, reps: int = 5):
+    wl = synth.workload(4)
+    lin = wl.linears[0]
+    m = wl.prefill[0]
+    w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+    enc = P.quantize(w, wl.osr, wl.levels)
+    del w
+    L = enc.layout
+    x = SG.activations_gpu(wl.seed, 2, m, lin.k).to(torch.bfloat16)
+    y = torch.empty((m, lin.n), dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.sdq_linear_workspace_bytes(L, m), dtype=torch.uint8, device="cuda")
+    ms_total, _ = _graph_time(torch, [lambda: P.sdq_linear(x, enc.codes, enc.scales, L, y, ws)] * reps, 3, 1)
+    P.sdq_expand_activations(x, L, ws)
+    ms_gemm, _ = _graph_time(torch, [lambda: P.sdq_linear_expanded(m, enc.codes, enc.scales, L, y, ws)] * reps, 3, 1)
+    flops = 2.0 * m * L.n * L.k_up
+    tf_total = flops / (ms_total * 1e-3) / 1e12
+    tf_gemm = flops / (ms_gemm * 1e-3) / 1e12
+    out = {
+        "workload": "llama70b_8192x8192_osr2_ternary_prefill_m2048_bf16",
+        "tflops": tf_total, "ms": ms_total, "ms_gemm": ms_gemm,
+        "roofline": {"bound": "mfma", "achieved": tf_gemm, "peak": MFMA_F16_PEAK_TFLOPS,
+                     "unit": "TFLOP/s", "frac": tf_gemm / MFMA_F16_PEAK_TFLOPS, "traffic": None,
+                     "note": "GEMM kernel alone; flops = 2 * m * N * K_up"},
+    }
+    del ws, y, x, enc
+    torch.cuda.empty_cache()
+    return out
+
+
+def bench_multiosr(torch, P, synth, SG):
+    wl = synth.workload(3)
+    var, nparams = [], []
+    t0 = time.perf_counter()
+    out = torch.zeros(2, dtype=torch.float64, device="cuda")
+    for lin in wl.linears:
+        w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+        ws = torch.empty(P.sdq_moments_workspace_bytes(w.numel()), dtype=torch.uint8, device="cuda")
+        P.sdq_weight_moments(w, out, ws)
+        var.append(float(out[1].item()))
+        nparams.append(lin.n * lin.k)
+    t1 = time.perf_counter()
+    osr = P.sdq_multiosr(var, nparams, [lin.layer for lin in wl.linears], *wl.multiosr)
+    t2 = time.perf_counter()
+    return {"workload": "llama7b_layer_7_linears", "osr": [float(o) for o in osr],
+            "weighted_mean_osr": float(sum(o * n for o, n in zip(osr, nparams)) / sum(nparams)),
+            "moments_s_incl_generation": t1 - t0, "allocate_ms": (t2 - t1) * 1e3}
+
+
+def cpu_baseline(synth, dec, budget_s: float = 12.0):
+    """The oracle on host cores: encode a sample of rows, then its fp64 linear."""
+    import numpy as np
+    import oracle
+    from oracle import linear as OL
+    try:
+        from threadpoolctl import threadpool_info
+        blas_threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:  # noqa: BLE001
+        blas_threads = 1
+    wl, lin, L = dec["wl"], dec["lin"], dec["L"]
+    rows = 64
+    t0 = time.perf_counter()
+    w = synth.weight_rows(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers,
+                          rows=np.arange(rows))
+    r = oracle.encode(w, wl.osr, wl.levels)
+    t_enc = time.perf_counter() - t0
+    x = synth.to_f16(synth.activations_f32(wl.seed, 1, 1, lin.k)).astype(np.float64)
+    reps = 0
+    t1 = time.perf_counter()
+    while True:
+        OL.linear_fp64(x, r.codes, r.scales, L.block, L.m_up)
+        reps += 1
+        if time.perf_counter() - t1 > min(budget_s, 5.0) or reps >= 200:
+            break
+    t_lin = (time.perf_counter() - t1) / reps
+    row_bytes = P_codes_row_bytes(L)
+    return {
+        "value": rows * row_bytes / t_lin / 1e9, "unit": "GB/s", "cores": blas_threads,
+        "kind": "oracle",
+        "sample": f"{rows} of {lin.n} rows of the down_proj layer: oracle encode then its fp64 linear "
+                  f"(reconstruct W_hat by FFT Resample + Hadamard, BLAS product), {reps} repetitions",
+        "oracle_encoder_rows_per_s": rows / t_enc,
+        "host_cpu_count": os.cpu_count(),
+    }
+
+
+def P_codes_row_bytes(L):
+    return L.n_chunks * 16
+
+
+def main() -> int:
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[0])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1280)
+    ap.add_argument("--warmup", type=int, default=128)
+    ap.add_argument("--no-phases", action="store_true", help="skip encoder / prefill / MultiOSR")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU: the SDQ hot path has no multi-GPU step "
+              f"(requested --gpus {args.gpus}, WORLD_SIZE {world})", file=sys.stderr)
+        return 2
+
+    import torch
+    import paper_2510_03275_amd as P
+    import synth
+    from synth import gpu as SG
+
+    assert torch.cuda.is_available(), "bench.py needs a GPU"
+    torch.cuda.set_device(0)
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    dec = bench_decode(torch, P, synth, SG, args.steps, args.warmup)
+    L = dec["L"]
+    gbs = dec["nbytes"] / (dec["ms_step"] * 1e-3) / 1e9
+    gemv_gbs = dec["nbytes"] / (dec["ms_gemv"] * 1e-3) / 1e9
+    line = {
+        "metric": METRIC,
+        "value": gbs,
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": dec["steps_run"],
+        "warmup": args.warmup,
+        "ms_per_step": dec["ms_step"],
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": "llama7b_down_proj_4096x11008_osr1.5_binary_decode_m1",
+            "n": int(L.n), "k": int(L.k), "osr": L.m_up / L.block, "levels": int(L.levels),
+            "m": 1, "x_dtype": "f16", "code_bytes": int(dec["nbytes"]),
+            "rotating_code_buffers": int(dec["rot"]), "hip_graph": True,
+            "percent_of_hbm_peak": 100.0 * gbs / HBM_PEAK_GBS,
+            "ms_expand": dec["ms_expand"], "ms_gemv": dec["ms_gemv"],
+        },
+        "roofline": {"bound": "hbm", "achieved": gemv_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": gemv_gbs / HBM_PEAK_GBS, "traffic": None,
+                     "kernel": "gemv_lut_kernel<1,2>",
+                     "note": "algorithmic bytes = packed codes N * K_up / 8 per launch"},
+    }
+    if not args.no_phases:
+        enc_ph = bench_encoder(torch, P, dec["w"], dec["wl"])
+        del dec["w"]
+        torch.cuda.empty_cache()
+        line["phases"] = {"encoder": enc_ph,
+                          "decode_70b": bench_decode_70b(torch, P, synth, SG),
+                          "prefill": bench_prefill(torch, P, synth, SG),
+                          "multiosr": bench_multiosr(torch, P, synth, SG)}
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(synth, dec)
+    line["wall_s"] = time.perf_counter() - t_start
+    print(json.dumps(line), flush=True)
+    return 0
+
+
+if __name__ == "__main__":
+    sys.exit(main())

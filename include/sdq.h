@@ -129,30 +129,54 @@ sdq_status sdq_quantize(const float* w_dev, const sdq_layout* layout, void* code
 sdq_status sdq_quantize_check(const void* workspace_dev, void* stream);
 
 /* Device workspace (bytes) sdq_linear needs for m activation rows: the
- * expanded activations (m x k_up, fp32 for m <= 16, fp16 otherwise) plus
- * split-K partial sums and counters. */
+ * expanded activations at offset 0 (m x k_up rounded up to whole chunks;
+ * fp32 for m <= 16, fp16 otherwise), then for m <= 16 a fixed block of
+ * split-K counters and the split-K partial sums of this layout. */
 size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
 
 /*
  * y = x W_hat^T for the encoded layer (Fig. 5 and Algorithm 1 line 6: W_hat is
  * the decimated, Hadamard-restored reconstruction of the codes).  Computed as
  * x_tilde = per-block (x_b Had) D^T (D: Resample back to B), then
- * y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j].
+ * y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j].  Equivalent to
+ * sdq_expand_activations followed by sdq_linear_expanded on the same workspace.
  *   x_dev        [m x k] activations of type xt (F16, BF16 or F32), row-major.
  *   m            activation rows, >= 0 (m = 0 is a no-op).  m <= 16 runs the
- *                decode path (fp32 expansion, additions over the codes);
- *                larger m runs the prefill path (fp16 expansion, MFMA).
+ *                decode path (fp32 expansion, additions over the codes, at
+ *                most 1,048,576 rows); larger m runs the prefill path (fp16
+ *                expansion, MFMA).
  *   codes_dev, scales_dev  as written by sdq_quantize for `layout`.
  *   y_dev        fp32 [m x n] output, row-major, fully overwritten.
- *   workspace    >= sdq_linear_workspace_bytes(layout, m) bytes; the library
- *                keeps counters in it that must start zeroed: zero the
- *                buffer once before its first use (the calls restore them).
+ *   workspace    >= sdq_linear_workspace_bytes(layout, m) bytes, no
+ *                initialisation needed.
  * Accuracy: max_r |y - y*| / max_r |y*| <= 1e-3 per activation row against the
- * fp64 definition.  Calls that share a workspace must be ordered (same stream).
- * Errors: SDQ_ERR_ARG, SDQ_ERR_WORKSPACE, SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
+ * fp64 definition.  The decode path splits K across workgroups for large
+ * layers and then adds the partial sums into y with fp32 atomics, so results
+ * may differ between calls in the last bits (relative ~1e-6); the prefill path
+ * and unsplit decodes are bitwise deterministic.  Calls that share a
+ * workspace must be ordered (same stream).
+ * Errors: SDQ_ERR_ARG, SDQ_ERR_SHAPE, SDQ_ERR_WORKSPACE, SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
 sdq_status sdq_linear(const void* x_dev, sdq_dtype xt, int64_t m, const void* codes_dev,
                       const float* scales_dev, const sdq_layout* layout, float* y_dev,
                       void* workspace_dev, size_t workspace_bytes, void* stream);
+
+/* First step of sdq_linear: write x_tilde (the activation expansion of Fig. 5:
+ * per block x_b Had D^T) for m activation rows into the workspace.  The
+ * expansion depends only on (k, block, m_up, levels) of the layout, so one
+ * call can serve several linears that share the input and those four values
+ * (e.g. projections of one hidden state); the workspace must then be large
+ * enough for each of them.  Errors as sdq_linear. */
+sdq_status sdq_expand_activations(const void* x_dev, sdq_dtype xt, int64_t m,
+                                  const sdq_layout* layout, void* workspace_dev,
+                                  size_t workspace_bytes, void* stream);
+
+/* Second step of sdq_linear: y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j] from
+ * the x_tilde that sdq_expand_activations left in the workspace (same m and a
+ * layout with the same k, block, m_up and levels).  m <= 16: addition-only
+ * lookup-table GEMV; otherwise fp16 MFMA GEMM.  Errors as sdq_linear. */
+sdq_status sdq_linear_expanded(int64_t m, const void* codes_dev, const float* scales_dev,
+                               const sdq_layout* layout, float* y_dev, void* workspace_dev,
+                               size_t workspace_bytes, void* stream);
 
 /*
  * MultiOSR (Section 3.4): per-linear OSR from weight variance and size, host

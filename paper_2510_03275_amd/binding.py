@@ -78,6 +78,9 @@ def _load() -> ctypes.CDLL:
         "sdq_linear_workspace_bytes": (ctypes.c_size_t, [L, ctypes.c_int64]),
         "sdq_linear": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, P, P, L, P, P,
                                       ctypes.c_size_t, P]),
+        "sdq_expand_activations": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, L, P,
+                                                  ctypes.c_size_t, P]),
+        "sdq_linear_expanded": (ctypes.c_int, [ctypes.c_int64, P, P, L, P, P, ctypes.c_size_t, P]),
         "sdq_multiosr": (ctypes.c_int, [P, P, P, ctypes.c_int64, ctypes.c_double, ctypes.c_double,
                                         ctypes.c_double, ctypes.c_double, P]),
         "sdq_moments_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
@@ -168,6 +171,18 @@ def sdq_linear(x, codes, scales, layout: sdq_layout, y, workspace, stream=None) 
                            ctypes.byref(layout), _ptr(y), _ptr(workspace), ws_bytes, _stream(stream)))
 
 
+def sdq_expand_activations(x, layout: sdq_layout, workspace, stream=None) -> None:
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.sdq_expand_activations(_ptr(x), _dtype_code(x), x.shape[0], ctypes.byref(layout),
+                                       _ptr(workspace), ws_bytes, _stream(stream)))
+
+
+def sdq_linear_expanded(m: int, codes, scales, layout: sdq_layout, y, workspace, stream=None) -> None:
+    ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
+    _check(_lib.sdq_linear_expanded(m, _ptr(codes), _ptr(scales), ctypes.byref(layout), _ptr(y),
+                                    _ptr(workspace), ws_bytes, _stream(stream)))
+
+
 def sdq_multiosr(var: Sequence[float], nparams: Sequence[int], layer_id: Sequence[int],
                  target: float, lo: float, hi: float, grid: float = 0.125) -> np.ndarray:
     var_a = np.ascontiguousarray(var, dtype=np.float64)
@@ -253,6 +268,6 @@ def linear(x, enc: Encoded, workspace=None, out=None, stream=None):
     y = out if out is not None else torch.empty((m, enc.layout.n), dtype=torch.float32, device=x.device)
     need = sdq_linear_workspace_bytes(enc.layout, m)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
-        workspace = torch.zeros(max(need, 1), dtype=torch.uint8, device=x.device)
+        workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
     sdq_linear(x, enc.codes, enc.scales, enc.layout, y, workspace, stream)
     return y

@@ -1,6 +1,6 @@
 """Builds libsdq.so (HIP kernels + C ABI) in-tree for gfx950 with hipcc.
 
-    python -m paper_2510_03275_amd.build        # or __graft_entry__.build()
+    python paper_2510_03275_amd/build.py        # or __graft_entry__.build()
 
 Every call recompiles all sources.  Device code is built with packed-fp32
 instructions disabled and with floating-point contraction off in the encoder

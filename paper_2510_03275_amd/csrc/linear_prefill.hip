@@ -184,10 +184,8 @@ size_t prefill_ws_bytes(const sdq_layout* L, int64_t m) {
   return align_up(static_cast<size_t>(m) * k_up_pad * 2, 256);
 }
 
-sdq_status launch_prefill(const void* x, sdq_dtype xt, int64_t m, const void* codes,
-                          const float* scales, const sdq_layout* L, const Tables* T, float* y,
-                          void* ws, size_t ws_bytes, hipStream_t stream) {
-  (void)ws_bytes;
+sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
+                                 const Tables* T, void* ws, hipStream_t stream) {
   _Float16* xbuf = static_cast<_Float16*>(ws);
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const dim3 egrid(static_cast<unsigned>(L->nb),
@@ -195,6 +193,15 @@ sdq_status launch_prefill(const void* x, sdq_dtype xt, int64_t m, const void* co
                    static_cast<unsigned>((m + 31) / 32));
   expand_prefill_kernel<<<egrid, dim3(64 * kExpWaves), 0, stream>>>(
       x, xt, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "prefill expansion launch");
+  return SDQ_OK;
+}
+
+sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
+                                   const sdq_layout* L, float* y, void* ws, hipStream_t stream) {
+  const _Float16* xbuf = static_cast<const _Float16*>(ws);
+  const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const dim3 ggrid(static_cast<unsigned>((L->n + kGemmBN - 1) / kGemmBN),
                    static_cast<unsigned>((m + kGemmBM - 1) / kGemmBM));
   if (L->levels == 2)
@@ -204,7 +211,7 @@ sdq_status launch_prefill(const void* x, sdq_dtype xt, int64_t m, const void* co
     gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(
         xbuf, static_cast<const uint32_t*>(codes), scales, m, L->n, L->n_pad, L->n_chunks, k_up_pad, y);
   hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return hip_error(e, "prefill launch");
+  if (e != hipSuccess) return hip_error(e, "prefill GEMM launch");
   return SDQ_OK;
 }
 

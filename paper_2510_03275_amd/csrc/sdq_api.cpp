@@ -106,23 +106,17 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
       ++j;
     }
   }
-  std::vector<float> dm(static_cast<size_t>(m_up) * block);
-  for (int m = 0; m < m_up; ++m)
-    for (int t = 0; t < block; ++t)
-      dm[static_cast<size_t>(m) * block + t] = static_cast<float>(downsample_entry(m, t, block, m_up));
   if (T.m_nz > 0) {
     e = hipMalloc(&T.unz, unz.size() * sizeof(float));
     if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
     e = hipMemcpy(T.unz, unz.data(), unz.size() * sizeof(float), hipMemcpyHostToDevice);
     if (e != hipSuccess) return hip_error(e, "table upload");
   }
-  e = hipMalloc(&T.dmat, dm.size() * sizeof(float));
-  if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
-  e = hipMemcpy(T.dmat, dm.data(), dm.size() * sizeof(float), hipMemcpyHostToDevice);
-  if (e != hipSuccess) return hip_error(e, "table upload");
   // E^T[m][t] = sum_u Had[t][u] D[m][u]: a Walsh-Hadamard transform of each row
-  // of D (fp64), scaled by 1/sqrt(B), split into two fp16 terms.
-  std::vector<uint16_t> eh(dm.size()), el(dm.size());
+  // of D (fp64), scaled by 1/sqrt(B); kept in fp32 and as two fp16 terms.
+  const size_t em = static_cast<size_t>(m_up) * block;
+  std::vector<float> e32(em);
+  std::vector<uint16_t> eh(em), el(em);
   std::vector<double> row(block);
   const double inv_sqrt_b = 1.0 / std::sqrt(static_cast<double>(block));
   for (int m = 0; m < m_up; ++m) {
@@ -136,18 +130,23 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
         }
     for (int t = 0; t < block; ++t) {
       const double val = row[t] * inv_sqrt_b;
+      const size_t at = static_cast<size_t>(m) * block + t;
+      e32[at] = static_cast<float>(val);
       const _Float16 hi = static_cast<_Float16>(val);
       const _Float16 lo = static_cast<_Float16>(val - static_cast<double>(hi));
-      std::memcpy(&eh[static_cast<size_t>(m) * block + t], &hi, 2);
-      std::memcpy(&el[static_cast<size_t>(m) * block + t], &lo, 2);
+      std::memcpy(&eh[at], &hi, 2);
+      std::memcpy(&el[at], &lo, 2);
     }
   }
+  e = hipMalloc(&T.et32, em * 4);
+  if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
   for (uint16_t** dst : {&T.et_hi, &T.et_lo}) {
-    e = hipMalloc(dst, eh.size() * 2);
+    e = hipMalloc(dst, em * 2);
     if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
   }
-  e = hipMemcpy(T.et_hi, eh.data(), eh.size() * 2, hipMemcpyHostToDevice);
-  if (e == hipSuccess) e = hipMemcpy(T.et_lo, el.data(), el.size() * 2, hipMemcpyHostToDevice);
+  e = hipMemcpy(T.et32, e32.data(), em * 4, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(T.et_hi, eh.data(), em * 2, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(T.et_lo, el.data(), em * 2, hipMemcpyHostToDevice);
   if (e != hipSuccess) return hip_error(e, "table upload");
   auto res = g_tables.emplace(key, T);
   *out = &res.first->second;
@@ -296,6 +295,55 @@ size_t sdq_linear_workspace_bytes(const sdq_layout* L, int64_t m) {
   return m <= 16 ? decode_ws_bytes(L, m) : prefill_ws_bytes(L, m);
 }
 
+static sdq_status linear_common(const sdq_layout* L, int64_t m, size_t ws_bytes, const void* ws) {
+  sdq_status st = check_layout(L);
+  if (st != SDQ_OK) return st;
+  if (m < 0) return set_error(SDQ_ERR_ARG, "m < 0");
+  if (m == 0 || L->n == 0) return SDQ_OK;
+  if (m <= 16) {
+    st = decode_supported(L);
+    if (st != SDQ_OK) return st;
+  }
+  const size_t need = m <= 16 ? decode_ws_bytes(L, m) : prefill_ws_bytes(L, m);
+  if (!ws || ws_bytes < need)
+    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  return SDQ_OK;
+}
+
+static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
+                              void* ws, float* y_zero, void* stream) {
+  if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
+  if (!x) return set_error(SDQ_ERR_ARG, "x is NULL");
+  const Tables* T = nullptr;
+  sdq_status st = get_tables(L->block, L->m_up, &T);
+  if (st != SDQ_OK) return st;
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return m <= 16 ? launch_decode_expand(x, xt, m, L, T, ws, y_zero, s)
+                 : launch_prefill_expand(x, xt, m, L, T, ws, s);
+}
+
+static sdq_status contract_impl(int64_t m, const void* codes, const float* scales,
+                                const sdq_layout* L, float* y, void* ws, bool y_zeroed, void* stream) {
+  if (!codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return m <= 16 ? launch_decode_contract(m, codes, scales, L, y, ws, y_zeroed, s)
+                 : launch_prefill_contract(m, codes, scales, L, y, ws, s);
+}
+
+sdq_status sdq_expand_activations(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
+                                  void* ws, size_t ws_bytes, void* stream) {
+  sdq_status st = linear_common(L, m, ws_bytes, ws);
+  if (st != SDQ_OK || m == 0 || L->n == 0) return st;
+  return expand_impl(x, xt, m, L, ws, nullptr, stream);
+}
+
+sdq_status sdq_linear_expanded(int64_t m, const void* codes, const float* scales,
+                               const sdq_layout* L, float* y, void* ws, size_t ws_bytes, void* stream) {
+  sdq_status st = linear_common(L, m, ws_bytes, ws);
+  if (st != SDQ_OK || m == 0 || L->n == 0) return st;
+  return contract_impl(m, codes, scales, L, y, ws, false, stream);
+}
+
 sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
                       const float* scales, const sdq_layout* L, float* y, void* ws,
                       size_t ws_bytes, void* stream) {
@@ -305,15 +353,13 @@ sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
   if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
   if (m == 0 || L->n == 0) return SDQ_OK;
   if (!x || !codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
-  const size_t need = m <= 16 ? decode_ws_bytes(L, m) : prefill_ws_bytes(L, m);
-  if (!ws || ws_bytes < need)
-    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
-  const Tables* T = nullptr;
-  st = get_tables(L->block, L->m_up, &T);
+  st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK) return st;
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (m <= 16) return launch_decode(x, xt, m, codes, scales, L, T, y, ws, ws_bytes, s);
-  return launch_prefill(x, xt, m, codes, scales, L, T, y, ws, ws_bytes, s);
+  // Decode: the expansion also zeroes y when the GEMV will accumulate into it.
+  const bool zero_in_expand = m <= 16 && decode_needs_zero_y(L, m);
+  st = expand_impl(x, xt, m, L, ws, zero_in_expand ? y : nullptr, stream);
+  if (st != SDQ_OK) return st;
+  return contract_impl(m, codes, scales, L, y, ws, true, stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -472,7 +518,7 @@ void sdq_release_tables(void) {
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(std::get<0>(kv.first));
     if (kv.second.unz) (void)hipFree(kv.second.unz);
-    if (kv.second.dmat) (void)hipFree(kv.second.dmat);
+    if (kv.second.et32) (void)hipFree(kv.second.et32);
     if (kv.second.et_hi) (void)hipFree(kv.second.et_hi);
     if (kv.second.et_lo) (void)hipFree(kv.second.et_lo);
     (void)hipSetDevice(cur);

@@ -22,9 +22,10 @@ struct Tables {
   int m_nz = 0;        // M - g0 samples per block computed as dense sums
   int m_nz_pad = 0;    // m_nz rounded up to the upsample tile width
   float* unz = nullptr;   // [B][m_nz_pad] fp32 coefficients g(p(t, m_j)), zero padded
-  float* dmat = nullptr;  // [M][B] fp32 decimation matrix D[m][t] (Resample back to B)
-  // E = Had D^T (B x M): x_tilde_b = x_b E.  Stored transposed, [M][B], as an
-  // fp16 pair hi + lo with hi = fp16(E) and lo = fp16(E - hi).
+  // E = Had D^T (B x M) with D the decimation (Resample back to B), so that
+  // x_tilde_b = x_b E.  Stored transposed, [M][B]: in fp32, and as an fp16
+  // pair hi + lo with hi = fp16(E) and lo = fp16(E - hi).
+  float* et32 = nullptr;
   uint16_t* et_hi = nullptr;
   uint16_t* et_lo = nullptr;
 };
@@ -54,17 +55,25 @@ size_t quant_ws_layout(const sdq_layout* L, QuantWs* ws, void* base);
 sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
                            float* scales, const QuantWs& ws, hipStream_t stream);
 
-// Decode path (m <= 16).
+// Decode path (m <= 16): expansion (fp32 x_tilde) then LUT GEMV.
 size_t decode_ws_bytes(const sdq_layout* L, int64_t m);
-sdq_status launch_decode(const void* x, sdq_dtype xt, int64_t m, const void* codes,
-                         const float* scales, const sdq_layout* L, const Tables* T, float* y,
-                         void* ws, size_t ws_bytes, hipStream_t stream);
+sdq_status decode_supported(const sdq_layout* L);
+// When the GEMV splits K it accumulates into y atomically; y must then start
+// at zero: the expansion zeroes it if handed y (y_zero), else the GEMV launch
+// does (y_zeroed = false).
+bool decode_needs_zero_y(const sdq_layout* L, int64_t m);
+sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
+                                const Tables* T, void* ws, float* y_zero, hipStream_t stream);
+sdq_status launch_decode_contract(int64_t m, const void* codes, const float* scales,
+                                  const sdq_layout* L, float* y, void* ws, bool y_zeroed,
+                                  hipStream_t stream);
 
-// Prefill path (m > 16).
+// Prefill path (m > 16): expansion (fp16 x_tilde) then MFMA GEMM.
 size_t prefill_ws_bytes(const sdq_layout* L, int64_t m);
-sdq_status launch_prefill(const void* x, sdq_dtype xt, int64_t m, const void* codes,
-                          const float* scales, const sdq_layout* L, const Tables* T, float* y,
-                          void* ws, size_t ws_bytes, hipStream_t stream);
+sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
+                                 const Tables* T, void* ws, hipStream_t stream);
+sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
+                                   const sdq_layout* L, float* y, void* ws, hipStream_t stream);
 
 // Moments (mean, variance) of a device array.
 size_t moments_ws_bytes(int64_t count);
