@@ -17,6 +17,8 @@
 // the accumulator layout (row 8*(v/4) + 4*(l/32) + v%4, column l%32 for
 // accumulator v) matter.
 #include <hip/hip_runtime.h>
+
+#include <algorithm>
 #include <hip/hip_fp16.h>
 #include <hip/hip_bf16.h>
 
@@ -29,8 +31,6 @@ typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kExpWaves = 4;          // expand: 32 rows x (4 x 32) samples per workgroup
-constexpr int kGemmBM = 128;          // activation rows per workgroup
-constexpr int kGemmBN = 128;          // weight rows per workgroup
 
 __device__ inline floatx16 mfma32(const half8& a, const half8& b, const floatx16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
@@ -105,74 +105,167 @@ __global__ __launch_bounds__(64 * kExpWaves) void expand_prefill_kernel(
   }
 }
 
-// 8 codes starting at code index kk of weight row n -> fp16 +1 / 0 / -1.
-template <int LEVELS>
-__device__ inline half8 load_codes8(const uint32_t* __restrict__ codes, int64_t n, int64_t n_pad,
-                                    int64_t n_chunks, int64_t kk) {
-  constexpr int BITS = LEVELS == 2 ? 1 : 2;
-  constexpr int CPC = 128 / BITS;
-  constexpr int PER_WORD = 32 / BITS;
-  half8 out;
-  if (n >= n_pad) {
-    for (int q = 0; q < 8; ++q) out[q] = 0;
-    return out;
-  }
-  const int64_t c = kk / CPC;
-  const int qpos = static_cast<int>(kk % CPC);
-  const uint32_t word = codes[(((n / kPanel) * n_chunks + c) * kPanel + n % kPanel) * 4 + qpos / PER_WORD];
-  const uint32_t f = word >> (BITS * (qpos % PER_WORD));
-  uint16_t h[8];
-  for (int q = 0; q < 8; ++q) {
-    if (LEVELS == 2) {
-      h[q] = ((f >> q) & 1u) ? 0x3C00u : 0xBC00u;
-    } else {
-      const uint32_t fld = (f >> (2 * q)) & 3u;
-      h[q] = static_cast<uint16_t>(((fld & 1u) * 0x3C00u) | ((fld >> 1) << 15));
-    }
-  }
-  for (int q = 0; q < 8; ++q) {
-    _Float16 v;
-    __builtin_memcpy(&v, &h[q], 2);
-    out[q] = v;
-  }
-  return out;
+// ---------------------------------------------------------------------------
+// GEMM.  Workgroup tile 256 (activation rows) x 256 (weight rows), k step 64.
+// Four waves side by side along the weight rows, each owning a 256 x 64 tile
+// (8 x 2 accumulator tiles of 32 x 32).  The x_tilde tile is double-buffered
+// in LDS and filled straight from global memory (global_load_lds_dwordx4, no
+// staging registers); its 16-byte groups are XOR-swizzled by row so that the
+// fragment reads of 16 consecutive rows fall on distinct banks.  The codes go
+// from global memory to registers one k step ahead and are expanded to fp16
+// with byte-permute lookups, each expanded fragment feeding eight MFMAs.
+// ---------------------------------------------------------------------------
+constexpr int kBM = 256, kBN = 256, kBK = 64;
+constexpr int kTileHalves = kBM * kBK;      // one LDS buffer (32 KB)
+
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) const void* gbl_void_ptr;
+
+// 16-byte group g of row r is stored in slot g ^ swz(r).
+__device__ inline int swz(int r) { return (r >> 1) & 7; }
+
+// Two ternary codes (4 bits: f0 at bits 0-1, f1 at bits 2-3) -> fp16 pair.
+// v_perm_b32 picks each result byte from the table by its selector byte: the
+// low bytes of both halves use selector 0x0C (constant 0x00), the high bytes
+// use the code field, and table bytes 0..3 of 0xBC003C00 are the fp16 high
+// bytes for fields 00, 01, 10, 11.
+__device__ inline uint32_t tern_pair(uint32_t nib) {
+  const uint32_t sel = 0x000C000Cu | ((nib & 3u) << 8) | ((nib & 0xCu) << 22);
+  return __builtin_amdgcn_perm(0u, 0xBC003C00u, sel);
+}
+
+// Two binary codes (bits 0, 1; 1 = +1) -> fp16 pair; table bytes 0xBC, 0x3C.
+__device__ inline uint32_t bin_pair(uint32_t two) {
+  const uint32_t sel = 0x000C000Cu | ((two & 1u) << 8) | ((two & 2u) << 23);
+  return __builtin_amdgcn_perm(0u, 0x00003CBCu, sel);
 }
 
 template <int LEVELS>
-__global__ __launch_bounds__(256) void gemm_prefill_kernel(
-    const _Float16* __restrict__ xt, const uint32_t* __restrict__ codes,
+__device__ inline half8 expand8(uint32_t bits) {
+  uint32_t d[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q) d[q] = LEVELS == 3 ? tern_pair(bits >> (4 * q)) : bin_pair(bits >> (2 * q));
+  half8 out;
+  __builtin_memcpy(&out, d, 16);
+  return out;
+}
+
+// The 8 codes this lane feeds at k step ks (0..3) of the current 64-code
+// slice, from the slice's words as loaded by load_codes.
+template <int LEVELS>
+__device__ inline uint32_t codes_at(const uint4& c, int ks, int half) {
+  if (LEVELS == 3) {
+    const uint32_t w = ks == 0 ? c.x : ks == 1 ? c.y : ks == 2 ? c.z : c.w;
+    return (w >> (16 * half)) & 0xFFFFu;
+  }
+  const uint32_t w = ks < 2 ? c.x : c.y;
+  return (w >> (16 * (ks & 1) + 8 * half)) & 0xFFu;
+}
+
+// Words holding codes [64*it, 64*it + 64) of weight row col.  Columns past
+// the padded row count read the last row: they only feed outputs that are
+// never stored.
+template <int LEVELS>
+__device__ inline uint4 load_codes(const uint4* __restrict__ codes, int64_t col, int64_t n_pad,
+                                   int64_t n_chunks, int it) {
+  col = col < n_pad ? col : n_pad - 1;
+  const int64_t c = LEVELS == 3 ? it : it / 2;
+  const uint4 q = codes[((col / kPanel) * n_chunks + c) * kPanel + col % kPanel];
+  if (LEVELS == 3) return q;
+  return (it & 1) ? make_uint4(q.z, q.w, 0u, 0u) : make_uint4(q.x, q.y, 0u, 0u);
+}
+
+template <int LEVELS>
+__global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
+    const _Float16* __restrict__ xt, const uint4* __restrict__ codes,
     const float* __restrict__ scales, int64_t m, int64_t n, int64_t n_pad, int64_t n_chunks,
     int64_t k_up_pad, float* __restrict__ y) {
-  const int lane = threadIdx.x % 64;
-  const int wave = threadIdx.x / 64;
-  const int wm = wave / 2, wn = wave % 2;
-  const int64_t i_base = static_cast<int64_t>(blockIdx.y) * kGemmBM + wm * 64;
-  const int64_t n_base = static_cast<int64_t>(blockIdx.x) * kGemmBN + wn * 64;
-  const int kg = (lane / 32) * 8;
-  floatx16 acc[2][2];
-  for (int a = 0; a < 2; ++a)
+  __shared__ __attribute__((aligned(1024))) _Float16 As[2][kTileHalves];
+  const int tid = threadIdx.x;
+  const int lane = tid % 64;
+  const int wave = tid / 64;
+  const int half = lane / 32;
+  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * kBM;
+  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * kBN + wave * 64;
+  const int64_t cols[2] = {n0 + lane % 32, n0 + 32 + lane % 32};
+  const int n_iter = static_cast<int>(k_up_pad / kBK);
+
+  floatx16 acc[8][2];
+#pragma unroll
+  for (int r = 0; r < 8; ++r)
+#pragma unroll
     for (int c = 0; c < 2; ++c)
-      for (int v = 0; v < 16; ++v) acc[a][c][v] = 0.0f;
-  const int64_t rows[2] = {i_base + lane % 32, i_base + 32 + lane % 32};
-  const int64_t cols[2] = {n_base + lane % 32, n_base + 32 + lane % 32};
-  for (int64_t k0 = 0; k0 < k_up_pad; k0 += 16) {
-    half8 af[2], bf[2];
-    for (int a = 0; a < 2; ++a) {
-      if (rows[a] < m) af[a] = *reinterpret_cast<const half8*>(xt + rows[a] * k_up_pad + k0 + kg);
-      else for (int q = 0; q < 8; ++q) af[a][q] = 0;
-    }
-    for (int c = 0; c < 2; ++c) bf[c] = load_codes8<LEVELS>(codes, cols[c], n_pad, n_chunks, k0 + kg);
-    for (int a = 0; a < 2; ++a)
-      for (int c = 0; c < 2; ++c) acc[a][c] = mfma32(af[a], bf[c], acc[a][c]);
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[r][c][v] = 0.0f;
+
+  // Tile fill: wave w fills rows 64 w .. 64 w + 63 with 8 copies of 1 KB (8
+  // rows each); lane l of copy j writes slot l % 8 of row 64 w + 8 j + l / 8,
+  // which holds 16-byte group (l % 8) ^ swz(row).  Rows past m read row m - 1:
+  // they only feed output rows that are not stored.
+  uint32_t a_off[8];                        // element offsets (m * k_up_pad < 2^31)
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const int r = wave * 64 + 8 * j + lane / 8;
+    const int64_t row = m0 + r;
+    a_off[j] = static_cast<uint32_t>((row < m ? row : m - 1) * k_up_pad + 8 * ((lane % 8) ^ swz(r)));
   }
+#define SDQ_FILL_A(BUF, IT)                                                                      \
+  do {                                                                                           \
+    const _Float16* src_ = xt + static_cast<uint32_t>((IT) * kBK);                               \
+    _Float16* dst_ = &As[(BUF)][wave * 64 * kBK];                                                \
+    _Pragma("unroll") for (int j = 0; j < 8; ++j)                                                \
+      __builtin_amdgcn_global_load_lds((gbl_void_ptr)(src_ + a_off[j]),                          \
+                                       (lds_void_ptr)(dst_ + j * 8 * kBK), 16, 0, 0);            \
+  } while (0)
+
+  uint4 c0 = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, 0);
+  uint4 c1 = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, 0);
+  SDQ_FILL_A(0, 0);
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+
+  // Fragment read offsets (halves) of row tile rt, k group g: row r = 32 rt + lane % 32.
+  const int fr = lane % 32;
+  for (int it = 0; it < n_iter; ++it) {
+    const int cur = it & 1;
+    // Prefetch the next k step into the other buffer (the last iteration
+    // refills the idle buffer with its own tile; it is never read again).
+    const int nx = it + 1 < n_iter ? it + 1 : it;
+    SDQ_FILL_A(cur ^ 1, nx);
+    const uint4 n0c = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, nx);
+    const uint4 n1c = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, nx);
+    const _Float16* abuf = As[cur];
+#pragma unroll
+    for (int ks = 0; ks < kBK / 16; ++ks) {
+      const half8 b0 = expand8<LEVELS>(codes_at<LEVELS>(c0, ks, half));
+      const half8 b1 = expand8<LEVELS>(codes_at<LEVELS>(c1, ks, half));
+      const int g = 2 * ks + half;
+#pragma unroll
+      for (int rt = 0; rt < 8; ++rt) {
+        const int r = rt * 32 + fr;
+        const half8 afrag = *reinterpret_cast<const half8*>(abuf + r * kBK + 8 * (g ^ swz(r)));
+        acc[rt][0] = mfma32(afrag, b0, acc[rt][0]);
+        acc[rt][1] = mfma32(afrag, b1, acc[rt][1]);
+      }
+    }
+    c0 = n0c;
+    c1 = n1c;
+    __builtin_amdgcn_s_waitcnt(0);          // this lane's tile copies have landed
+    __syncthreads();                          // ... and every other lane's
+  }
+#undef SDQ_FILL_A
+
+#pragma unroll
   for (int c = 0; c < 2; ++c) {
-    const int64_t nn = cols[c];
-    if (nn >= n) continue;
-    const float s = scales[nn];
-    for (int a = 0; a < 2; ++a)
+    const int64_t col = cols[c];
+    if (col >= n) continue;
+    const float s = scales[col];
+#pragma unroll
+    for (int r = 0; r < 8; ++r)
+#pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int64_t i = i_base + a * 32 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
-        if (i < m) y[i * n + nn] = acc[a][c][v] * s;
+        const int64_t row = m0 + r * 32 + 8 * (v / 4) + 4 * half + (v % 4);
+        if (row < m) y[row * n + col] = acc[r][c][v] * s;
       }
   }
 }
@@ -202,14 +295,21 @@ sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* sc
                                    const sdq_layout* L, float* y, void* ws, hipStream_t stream) {
   const _Float16* xbuf = static_cast<const _Float16*>(ws);
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
-  const dim3 ggrid(static_cast<unsigned>((L->n + kGemmBN - 1) / kGemmBN),
-                   static_cast<unsigned>((m + kGemmBM - 1) / kGemmBM));
-  if (L->levels == 2)
-    gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(
-        xbuf, static_cast<const uint32_t*>(codes), scales, m, L->n, L->n_pad, L->n_chunks, k_up_pad, y);
-  else
-    gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(
-        xbuf, static_cast<const uint32_t*>(codes), scales, m, L->n, L->n_pad, L->n_chunks, k_up_pad, y);
+  // The kernel addresses x_tilde with 32-bit element offsets: launch row
+  // chunks of at most 2^31 elements.
+  const int64_t rows_max = std::max<int64_t>(kBM, ((int64_t{1} << 31) / k_up_pad) / kBM * kBM);
+  for (int64_t r0 = 0; r0 < m; r0 += rows_max) {
+    const int64_t mm = std::min(rows_max, m - r0);
+    const dim3 ggrid(static_cast<unsigned>((L->n + kBN - 1) / kBN), static_cast<unsigned>((mm + kBM - 1) / kBM));
+    const _Float16* xc = xbuf + r0 * k_up_pad;
+    float* yc = y + r0 * L->n;
+    if (L->levels == 2)
+      gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(
+          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc);
+    else
+      gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(
+          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "prefill GEMM launch");
   return SDQ_OK;
