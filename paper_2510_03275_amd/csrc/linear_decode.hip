@@ -5,20 +5,17 @@
 //            group of blocks: its four lanes per sample keep their quarter of
 //            the sample's column of E in registers and reuse it for every block
 //            and activation row of the group (partial dots reduced with
-//            shuffles).  The workgroups also zero the split-K counters.
+//            shuffles).  The workgroups also zero y when the GEMV will split K.
 //   gemv     y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j] with additions only: a
 //            workgroup owns one 64-row panel and one K segment.  Each lane (one
 //            weight row) first issues the loads of its 16-byte code chunks
 //            (coalesced 1 KB per wave), then the workgroup builds, per
 //            activation row, lookup tables of the 16 signed partial sums of
 //            every 4-bit group of codes (4 binary codes or 2 ternary codes), and
-//            each lane adds one table entry per 4 bits.  The segments of a panel
-//            meet in a deterministic hand-off: each stores its partial sums with
-//            device-coherent stores, waits for them to complete, and bumps a
-//            device-scope counter; the workgroup that sees the last count adds
-//            the partials in segment order (device-coherent loads), applies the
-//            row scale, writes y and re-arms the counter.  No cache write-back
-//            and no waiting on other workgroups is involved.
+//            each lane adds one table entry per 4 bits.  When K is split into
+//            several segments, each segment adds its scaled partial sums into y
+//            with fp32 atomics (y was zeroed by the expansion), so the result
+//            can differ between runs in the last bits; a single segment stores.
 #include <hip/hip_runtime.h>
 #include <hip/hip_fp16.h>
 #include <hip/hip_bf16.h>

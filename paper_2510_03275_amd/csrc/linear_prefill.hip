@@ -30,7 +30,7 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kExpWaves = 4;          // expand: 32 rows x (4 x 32) samples per workgroup
+constexpr int kExpWaves = 4;          // expand: 32 rows x (4 x 128) samples per workgroup
 
 __device__ inline floatx16 mfma32(const half8& a, const half8& b, const floatx16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
@@ -65,6 +65,10 @@ __device__ inline void load_x8(const void* x, sdq_dtype xt, int64_t idx, bool ok
   }
 }
 
+// One wave: 32 activation rows x 128 samples (4 accumulator tiles) of one
+// block; a workgroup: 4 waves side by side along the samples.  Per k step of
+// 16 the wave loads one x fragment (8 values per lane) and four E^T hi / lo
+// fragments, next step prefetched.
 __global__ __launch_bounds__(64 * kExpWaves) void expand_prefill_kernel(
     const void* __restrict__ x, sdq_dtype xt, int64_t m, int64_t k, int B, int m_up,
     int64_t k_up, int64_t k_up_pad, const uint16_t* __restrict__ et_hi,
@@ -72,7 +76,7 @@ __global__ __launch_bounds__(64 * kExpWaves) void expand_prefill_kernel(
   const int lane = threadIdx.x % 64;
   const int wave = threadIdx.x / 64;
   const int64_t b = blockIdx.x;
-  const int c0 = (blockIdx.y * kExpWaves + wave) * 32;
+  const int c0 = (blockIdx.y * kExpWaves + wave) * 128;
   const int64_t i0 = static_cast<int64_t>(blockIdx.z) * 32;
   if (b == 0 && blockIdx.y == 0) {
     // Zero the padding columns of these 32 rows.
@@ -86,22 +90,47 @@ __global__ __launch_bounds__(64 * kExpWaves) void expand_prefill_kernel(
   const int64_t row = i0 + lane % 32;
   const int kg = (lane / 32) * 8;
   const bool row_ok = row < m;
-  const bool need_lo = xt != SDQ_F16;
-  floatx16 acc;
-  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
-  const int col = c0 + lane % 32;
+  // fp16 and bf16 activations are exact in fp16 here (bf16 has the shorter
+  // mantissa); only fp32 inputs need their low part.
+  const bool need_lo = xt == SDQ_F32;
+  int cols[4];
+  bool col_ok[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    cols[j] = c0 + 32 * j + lane % 32;
+    col_ok[j] = c0 + 32 * j < m_up;           // M is a multiple of 32
+    if (!col_ok[j]) cols[j] = c0 + lane % 32;
+  }
+  floatx16 acc[4];
+#pragma unroll
+  for (int j = 0; j < 4; ++j)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[j][v] = 0.0f;
   for (int t0 = 0; t0 < B; t0 += 16) {
     half8 ahi, alo;
     load_x8(x, xt, row * k + b * B + t0 + kg, row_ok, ahi, alo);
-    const half8 bhi = *reinterpret_cast<const half8*>(et_hi + static_cast<int64_t>(col) * B + t0 + kg);
-    const half8 blo = *reinterpret_cast<const half8*>(et_lo + static_cast<int64_t>(col) * B + t0 + kg);
-    acc = mfma32(ahi, bhi, acc);
-    acc = mfma32(ahi, blo, acc);
-    if (need_lo) acc = mfma32(alo, bhi, acc);
+    half8 bh[4], bl[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t off = static_cast<int64_t>(cols[j]) * B + t0 + kg;
+      bh[j] = *reinterpret_cast<const half8*>(et_hi + off);
+      bl[j] = *reinterpret_cast<const half8*>(et_lo + off);
+    }
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      acc[j] = mfma32(ahi, bh[j], acc[j]);
+      acc[j] = mfma32(ahi, bl[j], acc[j]);
+      if (need_lo) acc[j] = mfma32(alo, bh[j], acc[j]);
+    }
   }
-  for (int v = 0; v < 16; ++v) {
-    const int64_t i = i0 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
-    if (i < m) xt_out[i * k_up_pad + b * m_up + col] = static_cast<_Float16>(acc[v]);
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    if (!col_ok[j]) continue;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) {
+      const int64_t i = i0 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
+      if (i < m) xt_out[i * k_up_pad + b * m_up + cols[j]] = static_cast<_Float16>(acc[j][v]);
+    }
   }
 }
 
@@ -282,7 +311,7 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
   _Float16* xbuf = static_cast<_Float16*>(ws);
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const dim3 egrid(static_cast<unsigned>(L->nb),
-                   static_cast<unsigned>((L->m_up / 32 + kExpWaves - 1) / kExpWaves),
+                   static_cast<unsigned>((L->m_up / 128 + (L->m_up % 128 ? 1 : 0) + kExpWaves - 1) / kExpWaves),
                    static_cast<unsigned>((m + 31) / 32));
   expand_prefill_kernel<<<egrid, dim3(64 * kExpWaves), 0, stream>>>(
       x, xt, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf);
