@@ -35,9 +35,12 @@ sys.path.insert(0, ROOT)
 METRIC = "sdq_linear decode GB/s (% of HBM peak) and prefill TFLOP/s; rows/s quantized"
 HBM_PEAK_GBS = 8000.0
 MFMA_F16_PEAK_TFLOPS = 2500.0
-# Separately rounded fp32 mul and add (no contraction, no packed fp32):
-# 256 CUs x 4 SIMDs x 16 lanes x 2.4 GHz = 39.3 T lane-ops/s.
-VALU_F32_UNFUSED_PEAK_TFLOPS = 256 * 64 * 2.4e9 / 1e12
+# Separately rounded fp32 mul and add: the published 157.3 TFLOP/s fp32 vector
+# peak is 256 CUs x 2.4 GHz x 128 lanes x 2 flops (fused multiply-add); a
+# lane-op that is a plain mul or add is one flop, so the same lanes give
+# 78.6 TFLOP/s.  (Unpacked v_mul_f32 issues at half that lane rate on gfx950,
+# which caps a mul + add stream at about 2/3 of it.)
+VALU_F32_UNFUSED_PEAK_TFLOPS = 256 * 128 * 2.4e9 / 1e12
 MALL_BYTES = 256 * 1024 * 1024
 
 
@@ -94,11 +97,12 @@ def bench_decode(torch, P, synth, SG, steps: int, warmup: int):
     warm_replays = max(1, warmup // rot)
     ms_step, _ = _graph_time(torch, [step(i) for i in range(rot)], replays, warm_replays)
 
-    # The GEMV alone (x_tilde computed once, left in the workspace).
+    # The GEMV alone (x_tilde computed once, left in the workspace; accumulate
+    # mode so that no y-zeroing launch sits between the GEMV launches).
     P.sdq_expand_activations(x, L, ws)
 
     def gemv(i):
-        return lambda: P.sdq_linear_expanded(1, codes[i], enc.scales, L, y, ws)
+        return lambda: P.sdq_linear_expanded(1, codes[i], enc.scales, L, y, ws, accumulate=True)
 
     ms_gemv, _ = _graph_time(torch, [gemv(i) for i in range(rot)], replays, warm_replays)
 
@@ -130,7 +134,8 @@ def bench_decode_70b(torch, P, synth, SG, replays: int = 20):
     ms_step, _ = _graph_time(torch, [lambda i=i: P.sdq_linear(x, codes[i], enc.scales, L, y, ws)
                                      for i in range(rot)], replays, 2)
     P.sdq_expand_activations(x, L, ws)
-    ms_gemv, _ = _graph_time(torch, [lambda i=i: P.sdq_linear_expanded(1, codes[i], enc.scales, L, y, ws)
+    ms_gemv, _ = _graph_time(torch, [lambda i=i: P.sdq_linear_expanded(1, codes[i], enc.scales, L, y, ws,
+                                                                       accumulate=True)
                                      for i in range(rot)], replays, 2)
     del codes
     torch.cuda.empty_cache()

@@ -146,7 +146,9 @@ size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
  *                most 1,048,576 rows); larger m runs the prefill path (fp16
  *                expansion, MFMA).
  *   codes_dev, scales_dev  as written by sdq_quantize for `layout`.
- *   y_dev        fp32 [m x n] output, row-major, fully overwritten.
+ *   y_dev        fp32 [m x n] output, row-major.
+ *   accumulate   0: y = x W_hat^T (y fully overwritten);  nonzero: y += x W_hat^T
+ *                (e.g. a residual add fused into the projection).
  *   workspace    >= sdq_linear_workspace_bytes(layout, m) bytes, no
  *                initialisation needed.
  * Accuracy: max_r |y - y*| / max_r |y*| <= 1e-3 per activation row against the
@@ -158,7 +160,8 @@ size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
  * Errors: SDQ_ERR_ARG, SDQ_ERR_SHAPE, SDQ_ERR_WORKSPACE, SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
 sdq_status sdq_linear(const void* x_dev, sdq_dtype xt, int64_t m, const void* codes_dev,
                       const float* scales_dev, const sdq_layout* layout, float* y_dev,
-                      void* workspace_dev, size_t workspace_bytes, void* stream);
+                      int32_t accumulate, void* workspace_dev, size_t workspace_bytes,
+                      void* stream);
 
 /* First step of sdq_linear: write x_tilde (the activation expansion of Fig. 5:
  * per block x_b Had D^T) for m activation rows into the workspace.  The
@@ -173,10 +176,11 @@ sdq_status sdq_expand_activations(const void* x_dev, sdq_dtype xt, int64_t m,
 /* Second step of sdq_linear: y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j] from
  * the x_tilde that sdq_expand_activations left in the workspace (same m and a
  * layout with the same k, block, m_up and levels).  m <= 16: addition-only
- * lookup-table GEMV; otherwise fp16 MFMA GEMM.  Errors as sdq_linear. */
+ * lookup-table GEMV; otherwise fp16 MFMA GEMM.  accumulate as in sdq_linear.
+ * Errors as sdq_linear. */
 sdq_status sdq_linear_expanded(int64_t m, const void* codes_dev, const float* scales_dev,
-                               const sdq_layout* layout, float* y_dev, void* workspace_dev,
-                               size_t workspace_bytes, void* stream);
+                               const sdq_layout* layout, float* y_dev, int32_t accumulate,
+                               void* workspace_dev, size_t workspace_bytes, void* stream);
 
 /*
  * MultiOSR (Section 3.4): per-linear OSR from weight variance and size, host

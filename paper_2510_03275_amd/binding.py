@@ -76,11 +76,12 @@ def _load() -> ctypes.CDLL:
         "sdq_quantize": (ctypes.c_int, [P, L, P, P, P, ctypes.c_size_t, P]),
         "sdq_quantize_check": (ctypes.c_int, [P, P]),
         "sdq_linear_workspace_bytes": (ctypes.c_size_t, [L, ctypes.c_int64]),
-        "sdq_linear": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, P, P, L, P, P,
-                                      ctypes.c_size_t, P]),
+        "sdq_linear": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, P, P, L, P, ctypes.c_int32,
+                                      P, ctypes.c_size_t, P]),
         "sdq_expand_activations": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, L, P,
                                                   ctypes.c_size_t, P]),
-        "sdq_linear_expanded": (ctypes.c_int, [ctypes.c_int64, P, P, L, P, P, ctypes.c_size_t, P]),
+        "sdq_linear_expanded": (ctypes.c_int, [ctypes.c_int64, P, P, L, P, ctypes.c_int32, P,
+                                               ctypes.c_size_t, P]),
         "sdq_multiosr": (ctypes.c_int, [P, P, P, ctypes.c_int64, ctypes.c_double, ctypes.c_double,
                                         ctypes.c_double, ctypes.c_double, P]),
         "sdq_moments_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
@@ -164,11 +165,13 @@ def sdq_linear_workspace_bytes(layout: sdq_layout, m: int) -> int:
     return int(_lib.sdq_linear_workspace_bytes(ctypes.byref(layout), m))
 
 
-def sdq_linear(x, codes, scales, layout: sdq_layout, y, workspace, stream=None) -> None:
+def sdq_linear(x, codes, scales, layout: sdq_layout, y, workspace, stream=None,
+               accumulate: bool = False) -> None:
     m = x.shape[0] if x.dim() == 2 else 0
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_lib.sdq_linear(_ptr(x), _dtype_code(x), m, _ptr(codes), _ptr(scales),
-                           ctypes.byref(layout), _ptr(y), _ptr(workspace), ws_bytes, _stream(stream)))
+                           ctypes.byref(layout), _ptr(y), int(bool(accumulate)), _ptr(workspace),
+                           ws_bytes, _stream(stream)))
 
 
 def sdq_expand_activations(x, layout: sdq_layout, workspace, stream=None) -> None:
@@ -177,10 +180,12 @@ def sdq_expand_activations(x, layout: sdq_layout, workspace, stream=None) -> Non
                                        _ptr(workspace), ws_bytes, _stream(stream)))
 
 
-def sdq_linear_expanded(m: int, codes, scales, layout: sdq_layout, y, workspace, stream=None) -> None:
+def sdq_linear_expanded(m: int, codes, scales, layout: sdq_layout, y, workspace, stream=None,
+                        accumulate: bool = False) -> None:
     ws_bytes = 0 if workspace is None else workspace.numel() * workspace.element_size()
     _check(_lib.sdq_linear_expanded(m, _ptr(codes), _ptr(scales), ctypes.byref(layout), _ptr(y),
-                                    _ptr(workspace), ws_bytes, _stream(stream)))
+                                    int(bool(accumulate)), _ptr(workspace), ws_bytes,
+                                    _stream(stream)))
 
 
 def sdq_multiosr(var: Sequence[float], nparams: Sequence[int], layer_id: Sequence[int],
@@ -259,15 +264,20 @@ def quantize(w, osr: float, levels: int, block: int = 256, workspace=None, check
     return Encoded(layout, codes, scales)
 
 
-def linear(x, enc: Encoded, workspace=None, out=None, stream=None):
-    """y = x W_hat^T for a device activation [m, k] (fp16, bf16 or fp32)."""
+def linear(x, enc: Encoded, workspace=None, out=None, stream=None, accumulate: bool = False):
+    """y = x W_hat^T for a device activation [m, k] (fp16, bf16 or fp32).
+
+    With accumulate=True the product is added into `out` (which must be given).
+    """
     import torch
     if not x.is_cuda or not x.is_contiguous() or x.dim() != 2 or x.shape[1] != enc.layout.k:
         raise ValueError("x must be a contiguous device tensor [m, k]")
     m = x.shape[0]
+    if accumulate and out is None:
+        raise ValueError("accumulate=True needs out")
     y = out if out is not None else torch.empty((m, enc.layout.n), dtype=torch.float32, device=x.device)
     need = sdq_linear_workspace_bytes(enc.layout, m)
     if workspace is None or workspace.numel() * workspace.element_size() < need:
         workspace = torch.empty(max(need, 1), dtype=torch.uint8, device=x.device)
-    sdq_linear(x, enc.codes, enc.scales, enc.layout, y, workspace, stream)
+    sdq_linear(x, enc.codes, enc.scales, enc.layout, y, workspace, stream, accumulate)
     return y

@@ -208,7 +208,7 @@ template <int LEVELS>
 __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     const _Float16* __restrict__ xt, const uint4* __restrict__ codes,
     const float* __restrict__ scales, int64_t m, int64_t n, int64_t n_pad, int64_t n_chunks,
-    int64_t k_up_pad, float* __restrict__ y) {
+    int64_t k_up_pad, float* __restrict__ y, int accumulate) {
   __shared__ __attribute__((aligned(1024))) _Float16 As[2][kTileHalves];
   const int tid = threadIdx.x;
   const int lane = tid % 64;
@@ -294,7 +294,10 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int64_t row = m0 + r * 32 + 8 * (v / 4) + 4 * half + (v % 4);
-        if (row < m) y[row * n + col] = acc[r][c][v] * s;
+        if (row < m) {
+          const float val = acc[r][c][v] * s;
+          y[row * n + col] = accumulate ? y[row * n + col] + val : val;
+        }
       }
   }
 }
@@ -321,7 +324,8 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
 }
 
 sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
-                                   const sdq_layout* L, float* y, void* ws, hipStream_t stream) {
+                                   const sdq_layout* L, float* y, bool accumulate, void* ws,
+                                   hipStream_t stream) {
   const _Float16* xbuf = static_cast<const _Float16*>(ws);
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   // The kernel addresses x_tilde with 32-bit element offsets: launch row
@@ -334,10 +338,12 @@ sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* sc
     float* yc = y + r0 * L->n;
     if (L->levels == 2)
       gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(
-          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc);
+          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc,
+          accumulate ? 1 : 0);
     else
       gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(
-          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc);
+          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc,
+          accumulate ? 1 : 0);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "prefill GEMM launch");

@@ -115,7 +115,8 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
   // E^T[m][t] = sum_u Had[t][u] D[m][u]: a Walsh-Hadamard transform of each row
   // of D (fp64), scaled by 1/sqrt(B); kept in fp32 and as two fp16 terms.
   const size_t em = static_cast<size_t>(m_up) * block;
-  std::vector<float> e32(em);
+  T.m_pad = (m_up + 63) / 64 * 64;
+  std::vector<float> edec(static_cast<size_t>(T.m_pad) * block, 0.0f);
   std::vector<uint16_t> eh(em), el(em);
   std::vector<double> row(block);
   const double inv_sqrt_b = 1.0 / std::sqrt(static_cast<double>(block));
@@ -131,20 +132,20 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
     for (int t = 0; t < block; ++t) {
       const double val = row[t] * inv_sqrt_b;
       const size_t at = static_cast<size_t>(m) * block + t;
-      e32[at] = static_cast<float>(val);
+      edec[(static_cast<size_t>(t / 4) * T.m_pad + m) * 4 + t % 4] = static_cast<float>(val);
       const _Float16 hi = static_cast<_Float16>(val);
       const _Float16 lo = static_cast<_Float16>(val - static_cast<double>(hi));
       std::memcpy(&eh[at], &hi, 2);
       std::memcpy(&el[at], &lo, 2);
     }
   }
-  e = hipMalloc(&T.et32, em * 4);
+  e = hipMalloc(&T.edec, edec.size() * 4);
   if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
   for (uint16_t** dst : {&T.et_hi, &T.et_lo}) {
     e = hipMalloc(dst, em * 2);
     if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
   }
-  e = hipMemcpy(T.et32, e32.data(), em * 4, hipMemcpyHostToDevice);
+  e = hipMemcpy(T.edec, edec.data(), edec.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(T.et_hi, eh.data(), em * 2, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(T.et_lo, el.data(), em * 2, hipMemcpyHostToDevice);
   if (e != hipSuccess) return hip_error(e, "table upload");
@@ -323,11 +324,12 @@ static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_
 }
 
 static sdq_status contract_impl(int64_t m, const void* codes, const float* scales,
-                                const sdq_layout* L, float* y, void* ws, bool y_zeroed, void* stream) {
+                                const sdq_layout* L, float* y, bool accumulate, void* ws,
+                                bool y_ready, void* stream) {
   if (!codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return m <= 16 ? launch_decode_contract(m, codes, scales, L, y, ws, y_zeroed, s)
-                 : launch_prefill_contract(m, codes, scales, L, y, ws, s);
+  return m <= 16 ? launch_decode_contract(m, codes, scales, L, y, accumulate, ws, y_ready, s)
+                 : launch_prefill_contract(m, codes, scales, L, y, accumulate, ws, s);
 }
 
 sdq_status sdq_expand_activations(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
@@ -338,15 +340,16 @@ sdq_status sdq_expand_activations(const void* x, sdq_dtype xt, int64_t m, const 
 }
 
 sdq_status sdq_linear_expanded(int64_t m, const void* codes, const float* scales,
-                               const sdq_layout* L, float* y, void* ws, size_t ws_bytes, void* stream) {
+                               const sdq_layout* L, float* y, int32_t accumulate, void* ws,
+                               size_t ws_bytes, void* stream) {
   sdq_status st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK || m == 0 || L->n == 0) return st;
-  return contract_impl(m, codes, scales, L, y, ws, false, stream);
+  return contract_impl(m, codes, scales, L, y, accumulate != 0, ws, false, stream);
 }
 
 sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
-                      const float* scales, const sdq_layout* L, float* y, void* ws,
-                      size_t ws_bytes, void* stream) {
+                      const float* scales, const sdq_layout* L, float* y, int32_t accumulate,
+                      void* ws, size_t ws_bytes, void* stream) {
   sdq_status st = check_layout(L);
   if (st != SDQ_OK) return st;
   if (m < 0) return set_error(SDQ_ERR_ARG, "m < 0");
@@ -355,11 +358,11 @@ sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
   if (!x || !codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
   st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK) return st;
-  // Decode: the expansion also zeroes y when the GEMV will accumulate into it.
-  const bool zero_in_expand = m <= 16 && decode_needs_zero_y(L, m);
+  // Decode: the expansion also zeroes y when the GEMV will add into it.
+  const bool zero_in_expand = !accumulate && m <= 16 && decode_needs_zero_y(L, m);
   st = expand_impl(x, xt, m, L, ws, zero_in_expand ? y : nullptr, stream);
   if (st != SDQ_OK) return st;
-  return contract_impl(m, codes, scales, L, y, ws, true, stream);
+  return contract_impl(m, codes, scales, L, y, accumulate != 0, ws, true, stream);
 }
 
 // ---------------------------------------------------------------------------
@@ -518,7 +521,7 @@ void sdq_release_tables(void) {
     (void)hipGetDevice(&cur);
     (void)hipSetDevice(std::get<0>(kv.first));
     if (kv.second.unz) (void)hipFree(kv.second.unz);
-    if (kv.second.et32) (void)hipFree(kv.second.et32);
+    if (kv.second.edec) (void)hipFree(kv.second.edec);
     if (kv.second.et_hi) (void)hipFree(kv.second.et_hi);
     if (kv.second.et_lo) (void)hipFree(kv.second.et_lo);
     (void)hipSetDevice(cur);

@@ -23,9 +23,13 @@ struct Tables {
   int m_nz_pad = 0;    // m_nz rounded up to the upsample tile width
   float* unz = nullptr;   // [B][m_nz_pad] fp32 coefficients g(p(t, m_j)), zero padded
   // E = Had D^T (B x M) with D the decimation (Resample back to B), so that
-  // x_tilde_b = x_b E.  Stored transposed, [M][B]: in fp32, and as an fp16
-  // pair hi + lo with hi = fp16(E) and lo = fp16(E - hi).
-  float* et32 = nullptr;
+  // x_tilde_b = x_b E.  Two copies:
+  //   edec   fp32, groups of four t: edec[((t / 4) * m_pad + m) * 4 + t % 4] =
+  //          E[t][m], columns m_up .. m_pad-1 zero (m_pad = M rounded up to 64);
+  //   et_hi, et_lo  transposed [M][B] as an fp16 pair hi + lo with
+  //          hi = fp16(E) and lo = fp16(E - hi).
+  int m_pad = 0;
+  float* edec = nullptr;
   uint16_t* et_hi = nullptr;
   uint16_t* et_lo = nullptr;
 };
@@ -59,21 +63,23 @@ sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T,
 size_t decode_ws_bytes(const sdq_layout* L, int64_t m);
 sdq_status decode_supported(const sdq_layout* L);
 // When the GEMV splits K it accumulates into y atomically; y must then start
-// at zero: the expansion zeroes it if handed y (y_zero), else the GEMV launch
-// does (y_zeroed = false).
+// at zero (or hold the values to accumulate onto): the expansion zeroes it if
+// handed y (y_zero), else the GEMV launch does unless y_ready is set.
 bool decode_needs_zero_y(const sdq_layout* L, int64_t m);
 sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
                                 const Tables* T, void* ws, float* y_zero, hipStream_t stream);
+// accumulate: y += result instead of y = result.
 sdq_status launch_decode_contract(int64_t m, const void* codes, const float* scales,
-                                  const sdq_layout* L, float* y, void* ws, bool y_zeroed,
-                                  hipStream_t stream);
+                                  const sdq_layout* L, float* y, bool accumulate, void* ws,
+                                  bool y_ready, hipStream_t stream);
 
 // Prefill path (m > 16): expansion (fp16 x_tilde) then MFMA GEMM.
 size_t prefill_ws_bytes(const sdq_layout* L, int64_t m);
 sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
                                  const Tables* T, void* ws, hipStream_t stream);
 sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
-                                   const sdq_layout* L, float* y, void* ws, hipStream_t stream);
+                                   const sdq_layout* L, float* y, bool accumulate, void* ws,
+                                   hipStream_t stream);
 
 // Moments (mean, variance) of a device array.
 size_t moments_ws_bytes(int64_t count);

@@ -86,12 +86,15 @@ def test_quantize_and_linear_reject_bad_arguments_without_gpu_work():
     bad = Bd.sdq_layout()
     bad.n, bad.k, bad.block = 64, 256, 256
     assert lib.sdq_quantize(None, ctypes.byref(bad), None, None, None, 0, None) == -1
-    assert lib.sdq_linear(None, 0, -1, None, None, ctypes.byref(L), None, None, 0, None) == -1
-    assert lib.sdq_linear(None, 7, 1, None, None, ctypes.byref(L), None, None, 0, None) == -1
+    assert lib.sdq_linear(None, 0, -1, None, None, ctypes.byref(L), None, 0, None, 0, None) == -1
+    assert lib.sdq_linear(None, 7, 1, None, None, ctypes.byref(L), None, 0, None, 0, None) == -1
     assert lib.sdq_linear(ctypes.c_void_p(16), 0, 1, ctypes.c_void_p(16), ctypes.c_void_p(16),
-                          ctypes.byref(L), ctypes.c_void_p(16), None, 0, None) == -6
+                          ctypes.byref(L), ctypes.c_void_p(16), 0, None, 0, None) == -6
+    assert lib.sdq_linear_expanded(1, ctypes.c_void_p(16), ctypes.c_void_p(16), ctypes.byref(L),
+                                   ctypes.c_void_p(16), 1, None, 0, None) == -6
     # m == 0 is a successful no-op
-    assert lib.sdq_linear(None, 0, 0, None, None, ctypes.byref(L), None, None, 0, None) == 0
+    assert lib.sdq_linear(None, 0, 0, None, None, ctypes.byref(L), None, 0, None, 0, None) == 0
+    assert lib.sdq_linear(None, 0, 0, None, None, ctypes.byref(L), None, 1, None, 0, None) == 0
     assert lib.sdq_linear_workspace_bytes(ctypes.byref(L), 0) == 0
     assert lib.sdq_linear_workspace_bytes(ctypes.byref(L), 1) > 0
     assert lib.sdq_linear_workspace_bytes(ctypes.byref(L), 2048) >= 2048 * 512 * 2

@@ -78,8 +78,10 @@ def test_linear_decode_repeatable():
     y1 = P.linear(x_dev, enc, workspace=ws)
     y2 = P.linear(x_dev, enc, workspace=ws)
     assert torch.max(torch.abs(y1 - y2)).item() <= 1e-6 * torch.max(torch.abs(y1)).item()
-    small, _ = _oracle_codes_on_device(torch, 256, 256, 2.0, 3, seed=2)   # 8 chunks: one segment
-    xs, _ = to_device_x(synth.activations_f32(1, 0, 1, 256), "f16", torch)
+    # K = 64 at block 64, OSR 2: 128 ternary codes = 2 chunks, the smallest K segment
+    small, _ = _oracle_codes_on_device(torch, 256, 64, 2.0, 3, seed=2, block=64)
+    assert small.layout.n_chunks <= 2
+    xs, _ = to_device_x(synth.activations_f32(1, 0, 1, 64), "f16", torch)
     assert torch.equal(P.linear(xs, small), P.linear(xs, small))
 
 
@@ -101,6 +103,34 @@ def test_split_entry_points_share_one_expansion():
         for y, r in ((ya, ra), (yb, rb)):
             ref = OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up)
             assert np.all(OL.rel_err_rows(y.cpu().numpy().astype(np.float64), ref) <= TOL)
+
+
+@pytest.mark.parametrize("n,k,m", [(256, 256, 1), (4096, 2048, 1), (300, 1024, 5), (300, 1024, 40)])
+def test_linear_accumulate(n, k, m):
+    # accumulate=1 adds x W_hat^T onto y: decode with one K segment (plain
+    # read-modify-write), decode split over K (atomics onto y), prefill.
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    enc, r = _oracle_codes_on_device(torch, n, k, 2.0, 3, seed=n + k + m)
+    x_dev, x64 = to_device_x(synth.activations_f32(31, 0, m, k), "f16", torch)
+    y_plain = P.linear(x_dev, enc)
+    y0 = torch.from_numpy(synth.activations_f32(32, 0, m, n)).cuda()
+    y = y0.clone()
+    P.linear(x_dev, enc, out=y, accumulate=True)
+    expect = y0 + y_plain
+    torch.cuda.synchronize()
+    assert torch.max(torch.abs(y - expect)).item() <= 1e-5 * torch.max(torch.abs(expect)).item()
+    # the accumulated product still meets the tolerance against the oracle
+    err = OL.rel_err_rows((y - y0).cpu().numpy().astype(np.float64),
+                          OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up))
+    assert np.all(err <= TOL), err.max()
+    # the split entry point accumulates the same way
+    ws = torch.empty(P.sdq_linear_workspace_bytes(enc.layout, m), dtype=torch.uint8, device="cuda")
+    P.sdq_expand_activations(x_dev, enc.layout, ws)
+    y2 = y0.clone()
+    P.sdq_linear_expanded(m, enc.codes, enc.scales, enc.layout, y2, ws, accumulate=True)
+    torch.cuda.synchronize()
+    assert torch.max(torch.abs(y2 - expect)).item() <= 1e-5 * torch.max(torch.abs(expect)).item()
 
 
 def test_linear_empty_batch():
