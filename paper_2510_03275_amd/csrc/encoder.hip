@@ -2,8 +2,8 @@
 // compensation).  Four launches on the caller's stream:
 //
 //   clear      zero the non-finite flag and the per-row maxima;
-//   rotate     per (64-row panel, block): load W, Sylvester FWHT in LDS in the
-//              stage order h = 1, 2, ..., B/2, scale by fp32(1/sqrt(B))
+//   rotate     per (64-row panel, block): load W, Sylvester FWHT in registers in
+//              the stage order h = 1, 2, ..., B/2, scale by fp32(1/sqrt(B))
 //              (Section 3.3), store the rotated block rows-contiguous, copy the
 //              samples whose interpolation kernel is a unit impulse
 //              (m % P == 0) into the upsampled buffer, fold |v| into the row max;
@@ -42,64 +42,109 @@ __global__ void clear_kernel(uint32_t* __restrict__ flag, uint32_t* __restrict__
   if (i < n) rmax[i] = 0u;
 }
 
-// One workgroup: 64 rows x one block of B columns.
+// One workgroup: 64 rows x one block of B columns, four lanes per row.  Lane
+// (row, q) holds the B/4 elements t = 16 j + 4 q + e (j < B/16, e < 4) of its
+// row, loaded as float4 (a wave reads 64 contiguous bytes of each of its 16
+// rows per load).  The transform runs in registers in the stage order
+// h = 1, 2 (bits of e), 4, 8 (bits of q: partner lanes xor 1, 2), 16, ...,
+// B/2 (bits of j); every stage pairs the same elements and rounds the same
+// sums and differences as the textbook loop, so the result is bit-identical.
 template <int B>
 __global__ __launch_bounds__(kRotThreads) void rotate_kernel(
     const float* __restrict__ w, int64_t n, int64_t k, int64_t n_ws, int64_t k_up, int m_up,
     int g0, int phases, float inv_sqrt_b, float* __restrict__ v, float* __restrict__ xup,
     uint32_t* __restrict__ rmax, uint32_t* __restrict__ flag) {
-  constexpr int LD = B + 1;   // padded row stride: column reads hit distinct banks
-  __shared__ float tile[kPanel * LD];
+  constexpr int J = B / 16;
   const int tid = threadIdx.x;
+  const int q = tid & 3;
+  const int rl = tid >> 2;                      // row within the panel
   const int64_t panel = blockIdx.x;
   const int64_t b = blockIdx.y;
-  const int64_t r0 = panel * kPanel;
+  const int64_t r = panel * kPanel + rl;
+  float x[J][4];
   bool bad = false;
-  // Load 64 rows x B columns (coalesced along the row).
-  for (int idx = tid; idx < kPanel * B; idx += kRotThreads) {
-    const int rr = idx / B;
-    const int t = idx % B;
-    const int64_t r = r0 + rr;
-    float val = 0.0f;
-    if (r < n) {
-      val = w[r * k + b * B + t];
-      bad |= !isfinite(val);
+  if (r < n) {
+    const float4* src = reinterpret_cast<const float4*>(w + r * k + b * B) + q;
+#pragma unroll
+    for (int j = 0; j < J; ++j) {
+      const float4 t4 = src[4 * j];
+      x[j][0] = t4.x; x[j][1] = t4.y; x[j][2] = t4.z; x[j][3] = t4.w;
     }
-    tile[rr * LD + t] = val;
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) bad |= !isfinite(x[j][e]);
+  } else {
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) x[j][e] = 0.0f;   // padding rows: zeros
   }
   if (bad) atomicOr(flag, 1u);
-  __syncthreads();
-  // Fast Walsh-Hadamard transform, stage spans h = 1, 2, ..., B/2.
-  for (int h = 1; h < B; h <<= 1) {
-    for (int idx = tid; idx < kPanel * (B / 2); idx += kRotThreads) {
-      const int rr = idx / (B / 2);
-      const int pr = idx % (B / 2);
-      const int j = (pr / h) * (2 * h) + (pr % h);
-      const float a = tile[rr * LD + j];
-      const float c = tile[rr * LD + j + h];
-      tile[rr * LD + j] = a + c;
-      tile[rr * LD + j + h] = a - c;
-    }
-    __syncthreads();
+  // h = 1, 2: inside the float4.
+#pragma unroll
+  for (int j = 0; j < J; ++j) {
+    float a = x[j][0], c = x[j][1];
+    x[j][0] = a + c; x[j][1] = a - c;
+    a = x[j][2]; c = x[j][3];
+    x[j][2] = a + c; x[j][3] = a - c;
+    a = x[j][0]; c = x[j][2];
+    x[j][0] = a + c; x[j][2] = a - c;
+    a = x[j][1]; c = x[j][3];
+    x[j][1] = a + c; x[j][3] = a - c;
   }
-  // Scale, store rows-contiguous per t, copy unit-impulse samples, row max.
-  const int rr = tid % kPanel;
-  const int tq = tid / kPanel;   // 0..3
-  for (int t = tq; t < B; t += kRotThreads / kPanel) {
-    const float val = tile[rr * LD + t] * inv_sqrt_b;
-    tile[rr * LD + t] = val;
-    v[(b * B + t) * n_ws + r0 + rr] = val;
+  // h = 4, 8: across the row's four lanes (quad permutations).  The lower
+  // element of a pair keeps own + partner, the upper one partner + (-own)
+  // (= partner - own exactly).
+#pragma unroll
+  for (int bit = 1; bit <= 2; bit <<= 1) {
+    const bool lower = (q & bit) == 0;
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int own = __float_as_int(x[j][e]);
+        // quad_perm [1,0,3,2] (xor 1) or [2,3,0,1] (xor 2)
+        const float o = __int_as_float(bit == 1 ? __builtin_amdgcn_mov_dpp(own, 0xB1, 0xF, 0xF, false)
+                                                : __builtin_amdgcn_mov_dpp(own, 0x4E, 0xF, 0xF, false));
+        const float mine = lower ? x[j][e] : -x[j][e];
+        x[j][e] = o + mine;
+      }
   }
-  __syncthreads();
-  const int stride = B / g0;
+  // h = 16 .. B/2: across j, in registers.
+#pragma unroll
+  for (int hj = 1; hj < J; hj <<= 1)
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+      if ((j & hj) == 0)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const float a = x[j][e], c = x[j + hj][e];
+          x[j][e] = a + c;
+          x[j + hj][e] = a - c;
+        }
+  // Scale; store rows-contiguous per t; copy the unit-impulse samples
+  // (t = i * B / g0 feeds sample m = i * P); fold their |v| into the row max.
+  const int stride_mask = B / g0 - 1;          // B / g0 is a power of two
+  const int stride_shift = __builtin_ctz(B / g0);
+  float* vq = v + (b * B + 4 * q) * n_ws + r;
+  float* xq = xup + (panel * k_up + b * m_up) * kPanel + rl;
   float mx = 0.0f;
-  const int64_t xbase = (panel * k_up + b * m_up) * kPanel + rr;
-  for (int i = tq; i < g0; i += kRotThreads / kPanel) {
-    const float val = tile[rr * LD + i * stride];
-    xup[xbase + static_cast<int64_t>(i) * phases * kPanel] = val;
-    mx = fmaxf(mx, fabsf(val));
-  }
-  if (r0 + rr < n) atomicMax(&rmax[r0 + rr], __float_as_uint(mx));
+#pragma unroll
+  for (int j = 0; j < J; ++j)
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const int t = 16 * j + 4 * q + e;
+      const float val = x[j][e] * inv_sqrt_b;
+      vq[static_cast<int64_t>(16 * j + e) * n_ws] = val;
+      if ((t & stride_mask) == 0) {
+        xq[static_cast<int64_t>((t >> stride_shift) * phases) * kPanel] = val;
+        mx = fmaxf(mx, fabsf(val));
+      }
+    }
+  mx = fmaxf(mx, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(mx), 0xB1, 0xF, 0xF, false)));
+  mx = fmaxf(mx, __int_as_float(__builtin_amdgcn_mov_dpp(__float_as_int(mx), 0x4E, 0xF, 0xF, false)));
+  if (q == 0 && r < n) atomicMax(&rmax[r], __float_as_uint(mx));
 }
 
 // Batched VALU GEMM over (block, row tile, sample tile).  Thread (tx, ty)
