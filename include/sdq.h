@@ -141,10 +141,13 @@ size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
  * y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j].  Equivalent to
  * sdq_expand_activations followed by sdq_linear_expanded on the same workspace.
  *   x_dev        [m x k] activations of type xt (F16, BF16 or F32), row-major.
- *   m            activation rows, >= 0 (m = 0 is a no-op).  m <= 16 runs the
- *                decode path (fp32 expansion, additions over the codes, at
- *                most 1,048,576 rows); larger m runs the prefill path (fp16
- *                expansion, MFMA).
+ *   m            activation rows, >= 0 (m = 0 is a no-op).  m = 1: fp32
+ *                expansion and a GEMV with additions only over the codes;
+ *                2 <= m <= 16: the expansion quantised to 24-bit fixed point
+ *                and an exact int8 x int8 -> int32 matrix-core contraction
+ *                against the codes (blocks that do not start on a 16-byte code
+ *                chunk use the addition GEMV instead); larger m: the prefill
+ *                path (fp16 expansion, fp16 matrix cores).
  *   codes_dev, scales_dev  as written by sdq_quantize for `layout`.
  *   y_dev        fp32 [m x n] output, row-major.
  *   accumulate   0: y = x W_hat^T (y fully overwritten);  nonzero: y += x W_hat^T

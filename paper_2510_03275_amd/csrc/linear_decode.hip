@@ -1,20 +1,29 @@
-// Decode path of sdq_linear (m <= 16 activation rows), two launches:
+// Decode path of sdq_linear (m <= 16 activation rows), two launches each.
 //
+// One activation row (addition-only):
 //   expand   x_tilde_b = x_b E for every block b, E = Had D^T (B x M, fp32; D is
 //            the Resample back to B).  A workgroup owns 64 output samples of
 //            one block (one wave per quarter of t, E held in registers) and
 //            all activation rows.  The workgroups also zero y when the GEMV
 //            will split K.
 //   gemv     y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j] with additions only: a
-//            workgroup owns one 64-row panel and one K segment.  Each lane (one
-//            weight row) first issues the loads of its 16-byte code chunks
-//            (coalesced 1 KB per wave), then the workgroup builds, per
-//            activation row, lookup tables of the 16 signed partial sums of
-//            every 4-bit group of codes (4 binary codes or 2 ternary codes), and
-//            each lane adds one table entry per 4 bits.  When K is split into
-//            several segments, each segment adds its scaled partial sums into y
-//            with fp32 atomics (y was zeroed by the expansion), so the result
-//            can differ between runs in the last bits; a single segment stores.
+//            workgroup owns one K segment and four 64-row panels (one per
+//            wave, lane = weight row).  It first issues the loads of its
+//            16-byte code chunks (coalesced 1 KB per wave), then builds the
+//            segment's lookup tables of the 16 signed partial sums of every
+//            4-bit group of codes (4 binary codes or 2 ternary codes), and each
+//            lane adds one table entry per 4 bits.
+// Two to sixteen rows (integer matrix cores; blocks must start on a chunk):
+//   expand   the same x_tilde, quantised per (row, block) to 24-bit fixed
+//            point and written as three signed-byte planes;
+//   gemv     codes expanded to int8 {-1, 0, +1} by a byte permute and
+//            contracted against the planes with v_mfma_i32_16x16x64_i8 (exact
+//            int32 sums), dequantised per block.  The cost barely grows with
+//            the row count, where the table GEMV's grows linearly.
+// When K is split over workgroups, each adds its scaled partial sums into y
+// with fp32 atomics (y zeroed by the expansion, or holding the values to
+// accumulate onto), so results can differ between runs in the last bits; an
+// unsplit layer stores.
 #include <hip/hip_runtime.h>
 #include <hip/hip_fp16.h>
 #include <hip/hip_bf16.h>
@@ -22,6 +31,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <algorithm>
+#include <string>
 
 #include "sdq_internal.h"
 
@@ -99,6 +109,258 @@ __global__ __launch_bounds__(kExpThreads) void expand_decode_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Integer-MFMA decode: x_tilde as 24-bit fixed point in three signed-byte
+// planes, codes expanded to int8 {-1, 0, +1}, exact int32 accumulation.
+//
+// Per (activation row i, block b) the scale is S = max_t |x_b[t]| * e1max / Q
+// with e1max >= max_m sum_t |E[t][m]|, so |x_tilde_b| <= Q * S and the rounded
+// value q = rint(x_tilde / S) splits into bytes h, m, l in [-128, 127] with
+// q = 65536 h + 256 m + l.  Every workgroup of a block computes the same S
+// from the same staged block (a max is order independent).
+//
+// k-steps of 64 codes (v_mfma_i32_16x16x64_i8: lane l holds row l % 16 and
+// the 16 bytes of k-group kg = l / 16).  Blocks must start on a code chunk
+// (binary M % 128 == 0, ternary M % 64 == 0); inside a chunk the codes map to
+// (step, kg, dword di, byte beta) as the byte permute produces them from the
+// chunk's word kg:
+//   ternary  one step per chunk,  code 16 kg + di + 4 beta      (fields di + 4 beta)
+//   binary   two steps s per chunk, code 32 kg + 4 s + di + 8 beta  (bits 4 s + di + 8 beta)
+// A = planes: row p = 4 a + t (activation row a of the plane group, plane t:
+// h, m, l, zero), stored per step and plane group as 64 lanes x 16 bytes.
+constexpr float kQ = 8257536.0f;    // 2^23 - 2^17: leaves |h| <= 126
+constexpr int kStep = 64;           // codes per MFMA k-step
+
+template <int LEVELS>
+__device__ inline int chunk_code(int s, int kg, int di, int beta) {
+  return LEVELS == 2 ? 32 * kg + 4 * s + di + 8 * beta : 16 * kg + di + 4 * beta;
+}
+
+__device__ inline uint32_t plane_byte(int q, int t) {
+  const int l = ((q + 128) & 255) - 128;
+  const int q1 = (q - l) >> 8;
+  const int mm = ((q1 + 128) & 255) - 128;
+  const int h = (q1 - mm) >> 8;
+  const int v = t == 0 ? h : (t == 1 ? mm : (t == 2 ? l : 0));
+  return static_cast<uint32_t>(v) & 255u;
+}
+
+// One workgroup: 64 samples of one block, all m rows; as the fp32 expansion,
+// then quantised and written as planes (256 * npg dwords per workgroup).
+template <int B, int LEVELS>
+__global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
+    const void* __restrict__ x, sdq_dtype xt, int m, int npg, int64_t k, int64_t nb, int m_up,
+    int m_pad, const float4* __restrict__ edec, float e1max, uint32_t* __restrict__ planes,
+    float* __restrict__ sx, float* __restrict__ y_zero, int64_t y_count) {
+  constexpr int TQ = B / 4;
+  __shared__ float xs[kMaxDecodeRows][B];
+  __shared__ float red[4][kMaxDecodeRows][64];
+  __shared__ int qv[kMaxDecodeRows][64];
+  __shared__ float xmax[kMaxDecodeRows];
+  const int tid = threadIdx.x;
+  const int lane = tid % 64;
+  const int w = tid / 64;
+  const int o = blockIdx.x * 64 + lane;
+  const int64_t b = blockIdx.y;
+  float4 e[TQ / 4];
+  const float4* ep = edec + static_cast<int64_t>(w * (TQ / 4)) * m_pad + o;
+#pragma unroll
+  for (int q = 0; q < TQ / 4; ++q) e[q] = ep[static_cast<int64_t>(q) * m_pad];
+  for (int idx = tid; idx < m * B; idx += kExpThreads) {
+    const int i = idx / B, t = idx % B;
+    xs[i][t] = load_x(x, xt, static_cast<int64_t>(i) * k + b * B + t);
+  }
+  const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t n_wg = static_cast<int64_t>(gridDim.x) * gridDim.y;
+  if (y_zero)
+    for (int64_t i = wg * kExpThreads + tid; i < y_count; i += n_wg * kExpThreads) y_zero[i] = 0.0f;
+  __syncthreads();
+  // max |x_b| per row: wave w handles rows w, w + 4, ...
+  for (int i = w; i < m; i += 4) {
+    float mx = 0.0f;
+    for (int t = lane; t < B; t += 64) mx = fmaxf(mx, fabsf(xs[i][t]));
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    if (lane == 0) xmax[i] = mx;
+  }
+  for (int i = 0; i < m; ++i) {
+    const float4* xr = reinterpret_cast<const float4*>(&xs[i][w * TQ]);
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+    for (int q = 0; q < TQ / 4; ++q) {
+      const float4 v = xr[q];
+      a0 += e[q].x * v.x;
+      a1 += e[q].y * v.y;
+      a2 += e[q].z * v.z;
+      a3 += e[q].w * v.w;
+    }
+    red[w][i][lane] = (a0 + a1) + (a2 + a3);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < m * 64; idx += kExpThreads) {
+    const int i = idx / 64, l = idx % 64;
+    const float val = (red[0][i][l] + red[1][i][l]) + (red[2][i][l] + red[3][i][l]);
+    const float bound = xmax[i] * e1max;
+    qv[i][l] = bound > 0.0f ? __float2int_rn(val * (kQ / bound)) : 0;
+    if (blockIdx.x == 0 && l == 0) sx[static_cast<int64_t>(i) * nb + b] = bound / kQ;
+  }
+  __syncthreads();
+  // This workgroup's samples: codes [J0, J0 + 64) of the layer, J0 a multiple of 64.
+  constexpr int kCpc = LEVELS == 2 ? 128 : 64;             // codes per chunk
+  const int64_t j0 = b * m_up + static_cast<int64_t>(blockIdx.x) * 64;
+  const int64_t chunk = j0 / kCpc;
+  const int half = static_cast<int>((j0 % kCpc) / 64);    // binary: which half of the chunk
+  for (int idx = tid; idx < 256 * npg; idx += kExpThreads) {
+    const int di = idx % 4;
+    const int p = (idx / 4) % 16;
+    int s, kg, pg;
+    if (LEVELS == 2) {          // kg in {2 half, 2 half + 1}, both steps of the chunk
+      kg = 2 * half + (idx / 64) % 2;
+      pg = (idx / 128) % npg;
+      s = idx / (128 * npg);
+    } else {                    // all four kg, the chunk's one step
+      kg = (idx / 64) % 4;
+      pg = idx / 256;
+      s = 0;
+    }
+    const int a = pg * 4 + p / 4;
+    const int t = p % 4;
+    uint32_t word = 0;
+    if (a < m && t < 3) {
+#pragma unroll
+      for (int beta = 0; beta < 4; ++beta)
+        word |= plane_byte(qv[a][chunk_code<LEVELS>(s, kg, di, beta) - 64 * half], t) << (8 * beta);
+    }
+    const int64_t step = LEVELS == 2 ? 2 * chunk + s : chunk;
+    planes[((step * npg + pg) * 64 + kg * 16 + p) * 4 + di] = word;
+  }
+}
+
+// One workgroup: one 64-row panel and 4 * bpw consecutive blocks, wave w
+// taking blocks w * bpw .. w * bpw + bpw - 1 of them (the workgroup reads one
+// contiguous stretch of the panel's chunks; consecutive workgroups continue
+// it).  Per block, CH chunks per load batch; each chunk is loaded lane = row
+// (1 KB per load), then a 4 x 4 transpose of 16-lane groups (permlane swaps)
+// leaves word kg of row 16 cg + c in register cg of lane 16 kg + c: the B
+// operand of the MFMA on column group cg.  The four waves' partial sums meet
+// in LDS and leave with one atomic add (or store) per output.
+template <int LEVELS, int NPG, int CH>
+__global__ __launch_bounds__(256) void gemv_mfma_kernel(
+    const uint4* __restrict__ codes, const float* __restrict__ scales,
+    const uint4* __restrict__ planes, const float* __restrict__ sx, int m, int64_t n,
+    int64_t n_chunks, int64_t nb, int m_up, int bpw, int n_split, int accumulate,
+    float* __restrict__ y) {
+  typedef int v4i __attribute__((ext_vector_type(4)));
+  constexpr uint32_t kTable = LEVELS == 2 ? 0x000001FFu : 0xFF000100u;   // code -> int8
+  constexpr uint32_t kMask = LEVELS == 2 ? 0x01010101u : 0x03030303u;
+  constexpr int kBits = LEVELS == 2 ? 1 : 2;
+  constexpr int SPC = LEVELS == 2 ? 2 : 1;          // k-steps per chunk
+  constexpr int kCpc = LEVELS == 2 ? 128 : 64;
+  __shared__ float red[4][NPG * 4][64];
+  const int lane = threadIdx.x % 64;
+  const int wave = threadIdx.x / 64;
+  const int64_t panel = blockIdx.y;
+  const int kg = lane / 16;
+  const int cpb = m_up / kCpc;                      // chunks per block
+  const uint4* cbase = codes + panel * n_chunks * kPanel + lane;
+  float accf[NPG][4];
+#pragma unroll
+  for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) accf[pg][cg] = 0.0f;
+  const int64_t b_begin = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * bpw;
+  const int64_t b_end = min<int64_t>(nb, b_begin + bpw);
+  for (int64_t b = b_begin; b < b_end; ++b) {
+    v4i acc[NPG][4];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+      for (int cg = 0; cg < 4; ++cg) acc[pg][cg] = v4i{0, 0, 0, 0};
+    const int64_t c_block = b * cpb;
+    for (int c0 = 0; c0 < cpb; c0 += CH) {
+      uint4 q[CH];
+      uint4 av[CH][SPC][NPG];
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        // A chunk past the block end (CH not dividing it) gets zero planes:
+        // no branch, the accumulators stay in place.
+        const bool live = c0 + j < cpb;
+        const int64_t ch = c_block + min(c0 + j, cpb - 1);
+        q[j] = cbase[ch * kPanel];
+#pragma unroll
+        for (int s = 0; s < SPC; ++s)
+#pragma unroll
+          for (int pg = 0; pg < NPG; ++pg) {
+            const uint4 v = planes[((ch * SPC + s) * NPG + pg) * 64 + lane];
+            av[j][s][pg] = live ? v : make_uint4(0u, 0u, 0u, 0u);
+          }
+      }
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        uint32_t r0 = q[j].x, r1 = q[j].y, r2 = q[j].z, r3 = q[j].w;
+        {
+          const auto s02 = __builtin_amdgcn_permlane32_swap(r0, r2, false, false);
+          const auto s13 = __builtin_amdgcn_permlane32_swap(r1, r3, false, false);
+          r0 = s02[0]; r2 = s02[1]; r1 = s13[0]; r3 = s13[1];
+          const auto s01 = __builtin_amdgcn_permlane16_swap(r0, r1, false, false);
+          const auto s23 = __builtin_amdgcn_permlane16_swap(r2, r3, false, false);
+          r0 = s01[0]; r1 = s01[1]; r2 = s23[0]; r3 = s23[1];
+        }
+        const uint32_t wcg[4] = {r0, r1, r2, r3};
+#pragma unroll
+        for (int s = 0; s < SPC; ++s)
+#pragma unroll
+          for (int cg = 0; cg < 4; ++cg) {
+            const uint32_t wv = wcg[cg];
+            v4i bop;
+#pragma unroll
+            for (int di = 0; di < 4; ++di) {
+              const int d = LEVELS == 2 ? 4 * s + di : di;
+              bop[di] = static_cast<int>(__builtin_amdgcn_perm(0u, kTable, (wv >> (kBits * d)) & kMask));
+            }
+#pragma unroll
+            for (int pg = 0; pg < NPG; ++pg) {
+              const uint4 a4 = av[j][s][pg];
+              const v4i aop = {static_cast<int>(a4.x), static_cast<int>(a4.y), static_cast<int>(a4.z),
+                               static_cast<int>(a4.w)};
+              acc[pg][cg] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop, bop, acc[pg][cg], 0, 0, 0);
+            }
+          }
+      }
+    }
+    // Block done: dequantise with the block's scale of this lane's activation row.
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      const int a = pg * 4 + kg;
+      const float sxv = a < m ? sx[static_cast<int64_t>(a) * nb + b] : 0.0f;
+#pragma unroll
+      for (int cg = 0; cg < 4; ++cg) {
+        const float v = (static_cast<float>(acc[pg][cg][0]) * 65536.0f +
+                         static_cast<float>(acc[pg][cg][1]) * 256.0f) +
+                        static_cast<float>(acc[pg][cg][2]);
+        accf[pg][cg] += sxv * v;
+      }
+    }
+  }
+  // Combine the four waves; output (pg, cg, lane): activation row 4 pg + lane / 16,
+  // weight row 16 cg + lane % 16 of the panel.
+#pragma unroll
+  for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) red[wave][pg * 4 + cg][lane] = accf[pg][cg];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < NPG * 4 * 64; idx += 256) {
+    const int pc = idx / 64, l = idx % 64;
+    const int a = (pc / 4) * 4 + l / 16;
+    const int64_t r = panel * kPanel + 16 * (pc % 4) + l % 16;
+    if (a >= m || r >= n) continue;
+    const float val = ((red[0][pc][l] + red[1][pc][l]) + (red[2][pc][l] + red[3][pc][l])) * scales[r];
+    float* yp = &y[static_cast<int64_t>(a) * n + r];
+    if (n_split > 1) unsafeAtomicAdd(yp, val);
+    else *yp = accumulate ? *yp + val : val;
+  }
+}
+
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
   for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < count;
        i += static_cast<int64_t>(gridDim.x) * blockDim.x)
@@ -133,7 +395,7 @@ template <int MR, int LEVELS, int SEG>
 __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
     const uint4* __restrict__ codes, const float* __restrict__ scales,
     const float* __restrict__ xt, int m, int64_t n, int64_t n_panels, int64_t n_chunks,
-    int64_t k_up_pad, int n_segs, int accumulate, float* __restrict__ y) {
+    int64_t k_up_pad, int n_segs, int segs_fast, int accumulate, float* __restrict__ y) {
   constexpr int CPG = LEVELS == 2 ? 4 : 2;            // codes per 4-bit group
   constexpr int kGroups = SEG * kGroupsPerChunk;       // groups per activation row
   constexpr int kRowFloats = kGroups * 16;             // table floats per activation row
@@ -148,9 +410,9 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
-  const int64_t panel = static_cast<int64_t>(blockIdx.x) * kGemvWaves + wave;
+  const int64_t panel = static_cast<int64_t>(segs_fast ? blockIdx.y : blockIdx.x) * kGemvWaves + wave;
   const bool panel_ok = panel < n_panels;
-  const int seg = blockIdx.y;
+  const int seg = segs_fast ? blockIdx.x : blockIdx.y;
   const int64_t c0 = static_cast<int64_t>(seg) * SEG;
   const int nch = static_cast<int>(min<int64_t>(SEG, n_chunks - c0));
   const int64_t code0 = c0 * kGroupsPerChunk * CPG;   // first code of the segment
@@ -272,19 +534,115 @@ int segs_for(const sdq_layout* L, int seg) {
   return static_cast<int>((L->n_chunks + seg - 1) / seg);
 }
 
+// Decode variants: one activation row runs the addition-only table GEMV;
+// 2..16 rows run the integer-MFMA contraction, whose cost hardly grows with
+// the row count (it needs blocks that start on a code chunk, else the table
+// GEMV runs).  SDQ_DECODE_PATH=lut or =mfma forces one (a tuning and
+// cross-check aid; mfma still needs chunk-aligned blocks).
+bool use_mfma(const sdq_layout* L, int64_t m) {
+  if (L->m_up % (L->levels == 2 ? 128 : 64) != 0) return false;
+  static const char* env = std::getenv("SDQ_DECODE_PATH");
+  if (env && std::string(env) == "lut") return false;
+  if (env && std::string(env) == "mfma") return true;
+  return m >= 2;
+}
+
+int npg_for(int64_t m) { return static_cast<int>((m + 3) / 4); }
+
+// Blocks per wave of the MFMA GEMV (each split over K costs one atomic add per
+// output); SDQ_MFMA_BPW overrides.
+int mfma_bpw(const sdq_layout* L) {
+  static const char* env = std::getenv("SDQ_MFMA_BPW");
+  if (env) {
+    const int v = std::atoi(env);
+    if (v >= 1) return v;
+  }
+  (void)L;
+  return 1;
+}
+
+// Workgroups along K per panel (each covers 4 * bpw blocks).
+int mfma_splits(const sdq_layout* L) {
+  const int bpw = mfma_bpw(L);
+  return static_cast<int>((L->nb + 4 * bpw - 1) / (4 * bpw));
+}
+
 struct DecodeWs {
-  float* xt;
+  float* xt;          // table path: x_tilde, m x k_up_pad fp32
+  uint32_t* planes;   // MFMA path: fixed-point planes, (k_up / 32) x npg x 512 bytes
+  float* sx;          // MFMA path: per (row, block) plane scale, m x nb fp32
   size_t bytes;
 };
 
-// Workspace: x_tilde (m x k_up_pad fp32) at offset 0, so one expansion can
-// serve several linears that share its (k, block, M, levels).
+// Workspace: the expansion output at offset 0, so one expansion can serve
+// several linears that share its (k, block, M, levels).
 DecodeWs carve(const sdq_layout* L, int64_t m, void* base) {
-  const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
-  DecodeWs w;
-  w.xt = static_cast<float*>(base);
-  w.bytes = align_up(static_cast<size_t>(m) * k_up_pad * 4, 256);
+  DecodeWs w{};
+  char* p = static_cast<char*>(base);
+  if (use_mfma(L, m)) {
+    const size_t pl = align_up(static_cast<size_t>(L->k_up / kStep) * npg_for(m) * 1024, 256);
+    w.planes = reinterpret_cast<uint32_t*>(p);
+    w.sx = reinterpret_cast<float*>(p + pl);
+    w.bytes = pl + align_up(static_cast<size_t>(m) * L->nb * 4, 256);
+  } else {
+    const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
+    w.xt = reinterpret_cast<float*>(p);
+    w.bytes = align_up(static_cast<size_t>(m) * k_up_pad * 4, 256);
+  }
   return w;
+}
+
+// Chunks loaded per batch: the largest allowed size that divides the block's
+// chunks (all of them at once when they fit), within a register budget that
+// shrinks with the number of plane groups.
+int pick_ch(int cpb, int npg, int levels) {
+  const int cap_steps = npg == 1 ? 16 : (npg == 2 ? 8 : 4);
+  const int cap = std::max(1, cap_steps / (levels == 2 ? 2 : 1));
+  static const int allowed1[] = {8, 6, 4, 3, 2, 1};
+  static const int allowed2[] = {4, 2, 1};
+  const int* al = npg == 1 ? allowed1 : allowed2;
+  const int na = npg == 1 ? 6 : 3;
+  for (int i = 0; i < na; ++i)
+    if (al[i] <= cap && cpb % al[i] == 0) return al[i];
+  return 1;
+}
+
+template <int LEVELS, int NPG, int CH>
+void launch_mfma_ch(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
+                    int64_t m, float* y, bool accumulate, hipStream_t stream) {
+  const int64_t n_panels = L->n_pad / kPanel;
+  const int bpw = mfma_bpw(L);
+  const int splits = mfma_splits(L);
+  // K groups fastest: consecutive workgroups sweep one panel's chunks.
+  const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(n_panels));
+  gemv_mfma_kernel<LEVELS, NPG, CH><<<grid, dim3(256), 0, stream>>>(
+      static_cast<const uint4*>(codes), scales, reinterpret_cast<const uint4*>(w.planes), w.sx,
+      static_cast<int>(m), L->n, L->n_chunks, L->nb, L->m_up, bpw, splits, accumulate ? 1 : 0, y);
+}
+
+template <int LEVELS>
+void launch_mfma_levels(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
+                        int64_t m, float* y, bool acc, hipStream_t stream) {
+  const int npg = npg_for(m);
+  const int cpb = L->m_up / (LEVELS == 2 ? 128 : 64);
+  const int ch = pick_ch(cpb, npg, LEVELS);
+#define SDQ_CH(NPG_, CH_)                                                         \
+  if (ch == CH_) return launch_mfma_ch<LEVELS, NPG_, CH_>(w, codes, scales, L, m, y, acc, stream)
+  switch (npg) {
+    case 1:
+      SDQ_CH(1, 8); SDQ_CH(1, 6); SDQ_CH(1, 4); SDQ_CH(1, 3); SDQ_CH(1, 2);
+      return launch_mfma_ch<LEVELS, 1, 1>(w, codes, scales, L, m, y, acc, stream);
+    case 2:
+      SDQ_CH(2, 4); SDQ_CH(2, 2);
+      return launch_mfma_ch<LEVELS, 2, 1>(w, codes, scales, L, m, y, acc, stream);
+    case 3:
+      SDQ_CH(3, 4); SDQ_CH(3, 2);
+      return launch_mfma_ch<LEVELS, 3, 1>(w, codes, scales, L, m, y, acc, stream);
+    default:
+      SDQ_CH(4, 4); SDQ_CH(4, 2);
+      return launch_mfma_ch<LEVELS, 4, 1>(w, codes, scales, L, m, y, acc, stream);
+  }
+#undef SDQ_CH
 }
 
 template <int MR, int LEVELS, int SEG>
@@ -292,11 +650,17 @@ void launch_gemv_seg(const DecodeWs& w, const void* codes, const float* scales, 
                      int64_t m, float* y, bool accumulate, hipStream_t stream) {
   const int64_t n_panels = L->n_pad / kPanel;
   const int n_segs = segs_for(L, SEG);
-  const dim3 grid(static_cast<unsigned>((n_panels + kGemvWaves - 1) / kGemvWaves),
-                  static_cast<unsigned>(n_segs));
+  // Large layers: segments fastest, so consecutive workgroups sweep the same
+  // panels' chunks.  Small ones (the whole grid resident at once): panel
+  // groups fastest, so neighbours share a segment's samples.  (Measured.)
+  const unsigned pgroups = static_cast<unsigned>((n_panels + kGemvWaves - 1) / kGemvWaves);
+  const bool segs_fast = static_cast<int64_t>(pgroups) * n_segs > 2048;
+  const dim3 grid = segs_fast ? dim3(static_cast<unsigned>(n_segs), pgroups)
+                              : dim3(pgroups, static_cast<unsigned>(n_segs));
   gemv_lut_kernel<MR, LEVELS, SEG><<<grid, dim3(64 * kGemvWaves), 0, stream>>>(
       static_cast<const uint4*>(codes), scales, w.xt, static_cast<int>(m), L->n, n_panels,
-      L->n_chunks, L->n_chunks * L->codes_per_chunk, n_segs, accumulate ? 1 : 0, y);
+      L->n_chunks, L->n_chunks * L->codes_per_chunk, n_segs, segs_fast ? 1 : 0,
+      accumulate ? 1 : 0, y);
 }
 
 template <int MR, int LEVELS>
@@ -334,6 +698,7 @@ sdq_status decode_supported(const sdq_layout* L) {
 }
 
 bool decode_needs_zero_y(const sdq_layout* L, int64_t m) {
+  if (use_mfma(L, m)) return mfma_splits(L) > 1;
   return segs_for(L, pick_seg(L, round_mr(m))) > 1;
 }
 
@@ -344,6 +709,30 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const int64_t y_count = y_zero ? m * L->n : 0;
   const dim3 egrid(static_cast<unsigned>(T->m_pad / 64), static_cast<unsigned>(L->nb));
+  if (use_mfma(L, m)) {
+    const int npg = npg_for(m);
+#define SDQ_PLANES(BB, LV)                                                                       \
+  expand_planes_kernel<BB, LV><<<egrid, dim3(kExpThreads), 0, stream>>>(                         \
+      x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad,                           \
+      reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, y_zero, y_count)
+    if (L->levels == 2) {
+      switch (B) {
+        case 64: SDQ_PLANES(64, 2); break;
+        case 128: SDQ_PLANES(128, 2); break;
+        default: SDQ_PLANES(256, 2); break;
+      }
+    } else {
+      switch (B) {
+        case 64: SDQ_PLANES(64, 3); break;
+        case 128: SDQ_PLANES(128, 3); break;
+        default: SDQ_PLANES(256, 3); break;
+      }
+    }
+#undef SDQ_PLANES
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_error(e, "decode expansion launch");
+    return SDQ_OK;
+  }
 #define SDQ_EXPAND(BB)                                                                          \
   expand_decode_kernel<BB><<<egrid, dim3(kExpThreads), 0, stream>>>(                            \
       x, xt, static_cast<int>(m), L->k, L->m_up, T->m_pad, L->k_up, k_up_pad,                   \
@@ -368,8 +757,14 @@ sdq_status launch_decode_contract(int64_t m, const void* codes, const float* sca
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 4096));
     fill_zero_kernel<<<dim3(blocks), dim3(256), 0, stream>>>(y, count);
   }
-  if (L->levels == 2) launch_gemv<2>(w, codes, scales, L, m, y, accumulate, stream);
-  else launch_gemv<3>(w, codes, scales, L, m, y, accumulate, stream);
+  if (use_mfma(L, m)) {
+    if (L->levels == 2) launch_mfma_levels<2>(w, codes, scales, L, m, y, accumulate, stream);
+    else launch_mfma_levels<3>(w, codes, scales, L, m, y, accumulate, stream);
+  } else if (L->levels == 2) {
+    launch_gemv<2>(w, codes, scales, L, m, y, accumulate, stream);
+  } else {
+    launch_gemv<3>(w, codes, scales, L, m, y, accumulate, stream);
+  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "decode GEMV launch");
   return SDQ_OK;

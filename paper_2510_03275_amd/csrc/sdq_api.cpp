@@ -120,6 +120,7 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
   std::vector<uint16_t> eh(em), el(em);
   std::vector<double> row(block);
   const double inv_sqrt_b = 1.0 / std::sqrt(static_cast<double>(block));
+  double e1max = 0.0;   // max over samples m of sum_t |fp32(E[t][m])|
   for (int m = 0; m < m_up; ++m) {
     for (int t = 0; t < block; ++t) row[t] = downsample_entry(m, t, block, m_up);
     for (int h = 1; h < block; h <<= 1)
@@ -129,16 +130,22 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
           row[j] = a + c;
           row[j + h] = a - c;
         }
+    double col1 = 0.0;
     for (int t = 0; t < block; ++t) {
       const double val = row[t] * inv_sqrt_b;
       const size_t at = static_cast<size_t>(m) * block + t;
       edec[(static_cast<size_t>(t / 4) * T.m_pad + m) * 4 + t % 4] = static_cast<float>(val);
+      col1 += std::fabs(static_cast<double>(static_cast<float>(val)));
       const _Float16 hi = static_cast<_Float16>(val);
       const _Float16 lo = static_cast<_Float16>(val - static_cast<double>(hi));
       std::memcpy(&eh[at], &hi, 2);
       std::memcpy(&el[at], &lo, 2);
     }
+    e1max = std::max(e1max, col1);
   }
+  // Rounded up to fp32 (with a relative margin) so that |x_b E[:, m]| <=
+  // max|x_b| * e1max holds for the device's fp32 sums.
+  T.e1max = std::nextafter(static_cast<float>(e1max * (1.0 + 1e-6)), INFINITY);
   e = hipMalloc(&T.edec, edec.size() * 4);
   if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
   for (uint16_t** dst : {&T.et_hi, &T.et_lo}) {

@@ -29,6 +29,7 @@ struct Tables {
   //   et_hi, et_lo  transposed [M][B] as an fp16 pair hi + lo with
   //          hi = fp16(E) and lo = fp16(E - hi).
   int m_pad = 0;
+  float e1max = 0.0f;  // >= max over m of sum_t |E[t][m]| (fp32 table values)
   float* edec = nullptr;
   uint16_t* et_hi = nullptr;
   uint16_t* et_lo = nullptr;

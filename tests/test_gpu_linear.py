@@ -60,7 +60,7 @@ def test_linear_block_sizes():
     torch = require_gpu()
     for block, osr in ((128, 2.0), (64, 1.5)):
         enc, r = _oracle_codes_on_device(torch, 70, 512, osr, 3, seed=block, block=block)
-        for m in (1, 24):
+        for m in (1, 5, 24):
             x_dev, x64 = to_device_x(synth.activations_f32(3, 0, m, 512), "f16", torch)
             y = _run_linear(torch, enc, x_dev)
             err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, block, r.m_up))
