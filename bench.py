@@ -43,6 +43,40 @@ MFMA_F16_PEAK_TFLOPS = 2500.0
 VALU_F32_UNFUSED_PEAK_TFLOPS = 256 * 128 * 2.4e9 / 1e12
 MALL_BYTES = 256 * 1024 * 1024
 
+# HBM traffic per launch from two rocprofv3 --pmc passes over `bench.py
+# --traffic-probe` (FETCH_SIZE, then WRITE_SIZE, KiB per dispatch), scaled by
+# what the same counters read for a 268,435,456-byte device copy.  Valid only
+# for the kernel sources they were taken with: a source whose hash differs
+# reports traffic null.
+TRAFFIC_FETCH_SCALE = 1.999752
+TRAFFIC_WRITE_SCALE = 1.000000
+TRAFFIC_SOURCES = {
+    "linear_decode.hip": "1396260a89117de1573a646c170482208d66cb37ab77c608b55b009953aea801",
+    "linear_prefill.hip": "17fcd707c1f4254908b58d13a9ad7416bcb6d46f241e773013e901049af3dfcd",
+}
+TRAFFIC_KIB = {   # kernel -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB)
+    "gemv_lut_kernel<1,2,2>": ("linear_decode.hip", 4420.38, 1040.0),
+    "gemv_lut_kernel<1,3,8>": ("linear_decode.hip", 57920.97, 3584.0),
+    "gemm_prefill_kernel<3>": ("linear_prefill.hip", 319083.56, 65536.0),
+}
+
+
+def traffic_bytes(kernel: str):
+    """Scaled HBM bytes per launch of `kernel`, or None if its source changed."""
+    import hashlib
+    entry = TRAFFIC_KIB.get(kernel)
+    if entry is None:
+        return None
+    src, fetch_kib, write_kib = entry
+    path = os.path.join(ROOT, "paper_2510_03275_amd", "csrc", src)
+    try:
+        digest = hashlib.sha256(open(path, "rb").read()).hexdigest()
+    except OSError:
+        return None
+    if digest != TRAFFIC_SOURCES[src]:
+        return None
+    return 1024.0 * (fetch_kib * TRAFFIC_FETCH_SCALE + write_kib * TRAFFIC_WRITE_SCALE)
+
 
 def _rotations(nbytes: int) -> int:
     return max(2, math.ceil(2 * MALL_BYTES / max(nbytes, 1)))
@@ -144,7 +178,9 @@ def bench_decode_70b(torch, P, synth, SG, replays: int = 20):
             "gbs": nbytes / (ms_step * 1e-3) / 1e9, "ms": ms_step, "ms_gemv": ms_gemv,
             "code_bytes": nbytes, "rotating_code_buffers": rot,
             "roofline": {"bound": "hbm", "achieved": gemv_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                         "frac": gemv_gbs / HBM_PEAK_GBS, "traffic": None}}
+                         "frac": gemv_gbs / HBM_PEAK_GBS,
+                         "traffic": traffic_bytes("gemv_lut_kernel<1,3,8>"),
+                         "kernel": "gemv_lut_kernel<1,3,8>"}}
 
 
 def bench_encoder(torch, P, w, wl, reps: int = 5):
@@ -192,8 +228,10 @@ def bench_prefill(torch, P, synth, SG, reps: int = 5):
         "workload": "llama70b_8192x8192_osr2_ternary_prefill_m2048_bf16",
         "tflops": tf_total, "ms": ms_total, "ms_gemm": ms_gemm,
         "roofline": {"bound": "mfma", "achieved": tf_gemm, "peak": MFMA_F16_PEAK_TFLOPS,
-                     "unit": "TFLOP/s", "frac": tf_gemm / MFMA_F16_PEAK_TFLOPS, "traffic": None,
-                     "note": "GEMM kernel alone; flops = 2 * m * N * K_up"},
+                     "unit": "TFLOP/s", "frac": tf_gemm / MFMA_F16_PEAK_TFLOPS,
+                     "traffic": traffic_bytes("gemm_prefill_kernel<3>"),
+                     "kernel": "gemm_prefill_kernel<3>",
+                     "note": "GEMM kernel alone; flops = 2 * m * N * K_up; traffic in HBM bytes per launch"},
     }
     del ws, y, x, enc
     torch.cuda.empty_cache()
@@ -256,6 +294,41 @@ def cpu_baseline(synth, dec, budget_s: float = 12.0):
     }
 
 
+def traffic_probe(torch, P, synth, SG) -> None:
+    """A short eager run for hardware-counter passes: one 256 MiB device copy of
+    known size (to scale FETCH_SIZE / WRITE_SIZE), then four launches each of
+    the headline GEMV, the 70B up_proj GEMV and the prefill GEMM (their
+    expansions run once before).  Prints what it ran; the counters come from
+    rocprofv3 --pmc around this process."""
+    nbytes = 256 << 20
+    a = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    b.copy_(a)
+    torch.cuda.synchronize()
+    del a, b
+    print(f"copy: {nbytes} bytes", flush=True)
+    for wl_i, lin_i, m, xdt, label in ((2, 0, 1, torch.float16, "headline down_proj m=1"),
+                                       (4, 1, 1, torch.bfloat16, "70B up_proj m=1"),
+                                       (4, 0, 2048, torch.bfloat16, "70B 8192x8192 m=2048")):
+        wl = synth.workload(wl_i)
+        lin = wl.linears[lin_i]
+        w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+        enc = P.quantize(w, wl.osr, wl.levels)
+        del w
+        L = enc.layout
+        x = SG.activations_gpu(wl.seed, 5, m, lin.k).to(xdt)
+        y = torch.zeros((m, lin.n), dtype=torch.float32, device="cuda")
+        ws = torch.empty(P.sdq_linear_workspace_bytes(L, m), dtype=torch.uint8, device="cuda")
+        P.sdq_expand_activations(x, L, ws)
+        for _ in range(4):
+            P.sdq_linear_expanded(m, enc.codes, enc.scales, L, y, ws, accumulate=True)
+        torch.cuda.synchronize()
+        print(f"{label}: code bytes {P.sdq_codes_bytes(L)}, 4 launches", flush=True)
+        del enc, x, y, ws
+        torch.cuda.empty_cache()
+
+
 def P_codes_row_bytes(L):
     return L.n_chunks * 16
 
@@ -267,6 +340,8 @@ def main() -> int:
     ap.add_argument("--warmup", type=int, default=128)
     ap.add_argument("--no-phases", action="store_true", help="skip encoder / prefill / MultiOSR")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--traffic-probe", action="store_true",
+                    help="short eager run for rocprofv3 --pmc passes (prints no JSON line)")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -282,6 +357,9 @@ def main() -> int:
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
     torch.cuda.synchronize()
+    if args.traffic_probe:
+        traffic_probe(torch, P, synth, SG)
+        return 0
     t_start = time.perf_counter()
     dec = bench_decode(torch, P, synth, SG, args.steps, args.warmup)
     L = dec["L"]
@@ -309,9 +387,10 @@ def main() -> int:
             "ms_expand": dec["ms_expand"], "ms_gemv": dec["ms_gemv"],
         },
         "roofline": {"bound": "hbm", "achieved": gemv_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gemv_gbs / HBM_PEAK_GBS, "traffic": None,
-                     "kernel": "gemv_lut_kernel<1,2>",
-                     "note": "algorithmic bytes = packed codes N * K_up / 8 per launch"},
+                     "frac": gemv_gbs / HBM_PEAK_GBS, "traffic": traffic_bytes("gemv_lut_kernel<1,2,2>"),
+                     "kernel": "gemv_lut_kernel<1,2,2>",
+                     "note": "algorithmic bytes = packed codes N * K_up / 8 per launch; traffic = "
+                             "counted HBM bytes per launch (fetch + write)"},
     }
     if not args.no_phases:
         enc_ph = bench_encoder(torch, P, dec["w"], dec["wl"])

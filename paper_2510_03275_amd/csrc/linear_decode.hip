@@ -512,11 +512,11 @@ int round_mr(int64_t m) {
   return 16;
 }
 
-// Chunks per K segment.  Larger segments amortise the table build and halve
-// the atomics per step up, smaller ones give more workgroups; the largest
-// segment that still yields about four workgroups per CU wins (measured on
-// MI355X at m = 1: 4096 x 11008 picks 2, 28672 x 8192 picks 8).  Tables of
-// MR rows x SEG chunks must fit 64 KB.
+// Chunks per K segment of the table GEMV.  Larger segments amortise the table
+// build and cut the atomics per output, smaller ones give more workgroups; the
+// largest segment that still yields about four workgroups per CU wins
+// (measured on MI355X at m = 1: 4096 x 11008 picks 2, 28672 x 8192 picks 8).
+// Tables of MR rows x SEG chunks must fit 64 KB.
 int pick_seg(const sdq_layout* L, int mr) {
   static const char* env = std::getenv("SDQ_GEMV_SEG");   // tuning aid: 2, 4 or 8
   const int max_seg = mr >= 16 ? 2 : (mr >= 8 ? 4 : 8);
