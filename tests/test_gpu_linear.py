@@ -133,6 +133,31 @@ def test_linear_accumulate(n, k, m):
     assert torch.max(torch.abs(y2 - expect)).item() <= 1e-5 * torch.max(torch.abs(expect)).item()
 
 
+@pytest.mark.parametrize("n,k,osr,levels", [(4096, 2048, 1.5, 2), (3000, 1024, 2.0, 3), (256, 64, 2.0, 3)])
+def test_decode_repeated_inputs_on_one_workspace(n, k, osr, levels):
+    # Successive one-row calls on one workspace with different inputs each see
+    # their own x_tilde, and agree with the split entry points.
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    block = 64 if k == 64 else 256
+    enc, r = _oracle_codes_on_device(torch, n, k, osr, levels, seed=n + k, block=block)
+    ws = torch.empty(P.sdq_linear_workspace_bytes(enc.layout, 1), dtype=torch.uint8, device="cuda")
+    y = torch.empty((1, n), dtype=torch.float32, device="cuda")
+    y2 = torch.empty((1, n), dtype=torch.float32, device="cuda")
+    for it in range(6):
+        x_dev, x64 = to_device_x(synth.activations_f32(40 + it, 0, 1, k), "f16", torch)
+        P.linear(x_dev, enc, workspace=ws, out=y)
+        ws2 = torch.empty_like(ws)
+        P.sdq_expand_activations(x_dev, enc.layout, ws2)
+        P.sdq_linear_expanded(1, enc.codes, enc.scales, enc.layout, y2, ws2)
+        torch.cuda.synchronize()
+        ref = OL.linear_fp64(x64, r.codes, r.scales, block, r.m_up)
+        got = y.cpu().numpy().astype(np.float64)
+        assert np.all(np.isfinite(got)), it
+        assert np.all(OL.rel_err_rows(got, ref) <= TOL), it
+        assert torch.max(torch.abs(y - y2)).item() <= 1e-6 * torch.max(torch.abs(y2)).item(), it
+
+
 def test_linear_empty_batch():
     torch = require_gpu()
     import paper_2510_03275_amd as P
