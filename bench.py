@@ -16,8 +16,9 @@ streams its codes from HBM.  The line also carries:
                against the 8 TB/s HBM peak;
 * phases    -- the encoder on the same weight (rows/s, fp32 VALU roofline), the
                prefill path on the LLaMA-70B 8192x8192 linear at m = 2048 with
-               bf16 activations (TFLOP/s, fp16 MFMA roofline), and MultiOSR on
-               the LLaMA-7B layer's seven linears;
+               bf16 activations (TFLOP/s, fp16 MFMA roofline), MultiOSR on
+               the LLaMA-7B layer's seven linears, and the 80-layer LLaMA-70B
+               stack (560 linears quantised, one token through all of them);
 * cpu_baseline -- the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -257,6 +258,65 @@ def bench_multiosr(torch, P, synth, SG):
             "moments_s_incl_generation": t1 - t0, "allocate_ms": (t2 - t1) * 1e3}
 
 
+def bench_stack(torch, P, synth, SG, replays: int = 3):
+    """The 80-layer LLaMA-70B stack: MultiOSR from the measured variances of all
+    560 linears, every linear quantised on the device (codes kept resident),
+    then one decoded token (m = 1, and m = 8) through all 560 sdq_linear calls
+    in one graph."""
+    wl = synth.workload(5)
+    t0 = time.perf_counter()
+    out = torch.zeros(2, dtype=torch.float64, device="cuda")
+    mws = None
+    var = []
+    for lin in wl.linears:
+        w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+        need = P.sdq_moments_workspace_bytes(w.numel())
+        if mws is None or mws.numel() < need:
+            mws = torch.empty(need, dtype=torch.uint8, device="cuda")
+        P.sdq_weight_moments(w, out, mws)
+        var.append(float(out[1].item()))
+        del w
+    del mws
+    osr = P.sdq_multiosr(var, [lin.n * lin.k for lin in wl.linears], [lin.layer for lin in wl.linears],
+                         *wl.multiosr)
+    t1 = time.perf_counter()
+    encs = []
+    for lin, o in zip(wl.linears, osr):
+        w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+        encs.append(P.quantize(w, float(o), wl.levels))
+        del w
+    torch.cuda.synchronize()
+    t2 = time.perf_counter()
+    code_bytes = sum(P.sdq_codes_bytes(e.layout) for e in encs)
+    res = {"workload": "llama70b_stack_80x7_multiosr_ternary", "linears": len(encs),
+           "weighted_mean_osr": float(sum(float(o) * lin.n * lin.k for o, lin in zip(osr, wl.linears))
+                                      / sum(lin.n * lin.k for lin in wl.linears)),
+           "code_bytes": int(code_bytes),
+           "variances_and_allocation_s": t1 - t0,
+           "generate_and_quantize_s": t2 - t1,
+           "params": int(sum(lin.n * lin.k for lin in wl.linears))}
+    torch.cuda.empty_cache()
+    for m in wl.batches:
+        xs = {k: SG.activations_gpu(wl.seed, 300 + k % 97, m, k).to(torch.float16)
+              for k in {e.layout.k for e in encs}}
+        ys = {n: torch.empty((m, n), dtype=torch.float32, device="cuda") for n in {e.layout.n for e in encs}}
+        ws = torch.empty(max(P.sdq_linear_workspace_bytes(e.layout, m) for e in encs), dtype=torch.uint8,
+                         device="cuda")
+        fns = [lambda e=e: P.sdq_linear(xs[e.layout.k], e.codes, e.scales, e.layout, ys[e.layout.n], ws)
+               for e in encs]
+        ms_call, g = _graph_time(torch, fns, replays, 1)
+        del g
+        ms_token = ms_call * len(fns)
+        res[f"m{m}"] = {"ms_per_token_step": ms_token, "tokens_per_s": m * 1e3 / ms_token,
+                        "gbs": code_bytes / (ms_token * 1e-3) / 1e9,
+                        "frac_of_hbm_peak": code_bytes / (ms_token * 1e-3) / 1e9 / HBM_PEAK_GBS}
+        del xs, ys, ws
+        torch.cuda.empty_cache()
+    del encs
+    torch.cuda.empty_cache()
+    return res
+
+
 def cpu_baseline(synth, dec, budget_s: float = 12.0):
     """The oracle on host cores: encode a sample of rows, then its fp64 linear."""
     import numpy as np
@@ -400,6 +460,10 @@ def main() -> int:
                           "decode_70b": bench_decode_70b(torch, P, synth, SG),
                           "prefill": bench_prefill(torch, P, synth, SG),
                           "multiosr": bench_multiosr(torch, P, synth, SG)}
+        try:
+            line["phases"]["stack_70b"] = bench_stack(torch, P, synth, SG)
+        except Exception as exc:  # noqa: BLE001 -- report, keep the headline line
+            line["phases"]["stack_70b"] = {"error": repr(exc)}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(synth, dec)
     line["wall_s"] = time.perf_counter() - t_start
