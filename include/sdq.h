@@ -145,8 +145,7 @@ size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
  *                expansion and a GEMV with additions only over the codes;
  *                2 <= m <= 16: the expansion quantised to 24-bit fixed point
  *                and an exact int8 x int8 -> int32 matrix-core contraction
- *                against the codes (blocks that do not start on a 16-byte code
- *                chunk use the addition GEMV instead); larger m: the prefill
+ *                against the codes; larger m: the prefill
  *                path (fp16 expansion, fp16 matrix cores).
  *   codes_dev, scales_dev  as written by sdq_quantize for `layout`.
  *   y_dev        fp32 [m x n] output, row-major.

@@ -120,10 +120,14 @@ __global__ __launch_bounds__(kExpThreads) void expand_decode_kernel(
 // from the same staged block (a max is order independent).
 //
 // k-steps of 64 codes (v_mfma_i32_16x16x64_i8: lane l holds row l % 16 and
-// the 16 bytes of k-group kg = l / 16).  Blocks must start on a code chunk
-// (binary M % 128 == 0, ternary M % 64 == 0); inside a chunk the codes map to
-// (step, kg, dword di, byte beta) as the byte permute produces them from the
-// chunk's word kg:
+// the 16 bytes of k-group kg = l / 16).  The planes are laid out per block:
+// block b owns cpb chunk slots, slot j holding the samples of code chunk
+// floor(b M / chunk) + j that belong to block b and zeros elsewhere, so a
+// block that starts or ends inside a chunk (M not a multiple of the chunk)
+// shares that chunk's codes with its neighbour but not its planes, and every
+// k-step sums one block only; cpb is the most chunks any block touches.
+// Inside a chunk the codes map to (step, kg, dword di, byte beta) as the byte
+// permute produces them from the chunk's word kg:
 //   ternary  one step per chunk,  code 16 kg + di + 4 beta      (fields di + 4 beta)
 //   binary   two steps s per chunk, code 32 kg + 4 s + di + 8 beta  (bits 4 s + di + 8 beta)
 // A = planes: row p = 4 a + t (activation row a of the plane group, plane t:
@@ -145,12 +149,14 @@ __device__ inline uint32_t plane_byte(int q, int t) {
   return static_cast<uint32_t>(v) & 255u;
 }
 
-// One workgroup: 64 samples of one block, all m rows; as the fp32 expansion,
-// then quantised and written as planes (256 * npg dwords per workgroup).
+// One workgroup: one 64-code segment u of block b's chunk slots (code
+// positions floor(b M / chunk) * chunk + 64 u + [0, 64)), all m rows; the
+// samples of block b among them by the fp32 expansion, the rest zero; then
+// quantised and written as planes (256 * npg dwords per workgroup).
 template <int B, int LEVELS>
 __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
     const void* __restrict__ x, sdq_dtype xt, int m, int npg, int64_t k, int64_t nb, int m_up,
-    int m_pad, const float4* __restrict__ edec, float e1max, uint32_t* __restrict__ planes,
+    int m_pad, int cpb, const float4* __restrict__ edec, float e1max, uint32_t* __restrict__ planes,
     float* __restrict__ sx, float* __restrict__ y_zero, int64_t y_count) {
   constexpr int TQ = B / 4;
   __shared__ float xs[kMaxDecodeRows][B];
@@ -160,10 +166,14 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int w = tid / 64;
-  const int o = blockIdx.x * 64 + lane;
+  constexpr int kCpc = LEVELS == 2 ? 128 : 64;             // codes per chunk
   const int64_t b = blockIdx.y;
+  const int64_t c_first = b * m_up / kCpc;                  // block b's first code chunk
+  const int64_t g0 = c_first * kCpc + static_cast<int64_t>(blockIdx.x) * 64;
+  const int o = static_cast<int>(g0 + lane - b * m_up);    // this lane's sample within block b
+  const bool in_block = o >= 0 && o < m_up;
   float4 e[TQ / 4];
-  const float4* ep = edec + static_cast<int64_t>(w * (TQ / 4)) * m_pad + o;
+  const float4* ep = edec + static_cast<int64_t>(w * (TQ / 4)) * m_pad + (in_block ? o : 0);
 #pragma unroll
   for (int q = 0; q < TQ / 4; ++q) e[q] = ep[static_cast<int64_t>(q) * m_pad];
   for (int idx = tid; idx < m * B; idx += kExpThreads) {
@@ -201,15 +211,14 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
     const int i = idx / 64, l = idx % 64;
     const float val = (red[0][i][l] + red[1][i][l]) + (red[2][i][l] + red[3][i][l]);
     const float bound = xmax[i] * e1max;
-    qv[i][l] = bound > 0.0f ? __float2int_rn(val * (kQ / bound)) : 0;
+    const int ol = static_cast<int>(g0 + l - b * m_up);
+    qv[i][l] = bound > 0.0f && ol >= 0 && ol < m_up ? __float2int_rn(val * (kQ / bound)) : 0;
     if (blockIdx.x == 0 && l == 0) sx[static_cast<int64_t>(i) * nb + b] = bound / kQ;
   }
   __syncthreads();
-  // This workgroup's samples: codes [J0, J0 + 64) of the layer, J0 a multiple of 64.
-  constexpr int kCpc = LEVELS == 2 ? 128 : 64;             // codes per chunk
-  const int64_t j0 = b * m_up + static_cast<int64_t>(blockIdx.x) * 64;
-  const int64_t chunk = j0 / kCpc;
-  const int half = static_cast<int>((j0 % kCpc) / 64);    // binary: which half of the chunk
+  // Chunk slot of these 64 codes, and (binary) which half of the chunk they are.
+  const int64_t slot = b * cpb + static_cast<int64_t>(blockIdx.x) / (kCpc / 64);
+  const int half = static_cast<int>(blockIdx.x % (kCpc / 64));
   for (int idx = tid; idx < 256 * npg; idx += kExpThreads) {
     const int di = idx % 4;
     const int p = (idx / 4) % 16;
@@ -231,7 +240,7 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
       for (int beta = 0; beta < 4; ++beta)
         word |= plane_byte(qv[a][chunk_code<LEVELS>(s, kg, di, beta) - 64 * half], t) << (8 * beta);
     }
-    const int64_t step = LEVELS == 2 ? 2 * chunk + s : chunk;
+    const int64_t step = LEVELS == 2 ? 2 * slot + s : slot;
     planes[((step * npg + pg) * 64 + kg * 16 + p) * 4 + di] = word;
   }
 }
@@ -248,7 +257,7 @@ template <int LEVELS, int NPG, int CH>
 __global__ __launch_bounds__(256) void gemv_mfma_kernel(
     const uint4* __restrict__ codes, const float* __restrict__ scales,
     const uint4* __restrict__ planes, const float* __restrict__ sx, int m, int64_t n,
-    int64_t n_chunks, int64_t nb, int m_up, int bpw, int n_split, int accumulate,
+    int64_t n_chunks, int64_t nb, int m_up, int cpb, int bpw, int n_split, int accumulate,
     float* __restrict__ y) {
   typedef int v4i __attribute__((ext_vector_type(4)));
   constexpr uint32_t kTable = LEVELS == 2 ? 0x000001FFu : 0xFF000100u;   // code -> int8
@@ -261,7 +270,6 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
   const int wave = threadIdx.x / 64;
   const int64_t panel = blockIdx.y;
   const int kg = lane / 16;
-  const int cpb = m_up / kCpc;                      // chunks per block
   const uint4* cbase = codes + panel * n_chunks * kPanel + lane;
   float accf[NPG][4];
 #pragma unroll
@@ -276,22 +284,24 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
     for (int pg = 0; pg < NPG; ++pg)
 #pragma unroll
       for (int cg = 0; cg < 4; ++cg) acc[pg][cg] = v4i{0, 0, 0, 0};
-    const int64_t c_block = b * cpb;
+    const int64_t c_first = b * m_up / kCpc;        // block b's first code chunk
     for (int c0 = 0; c0 < cpb; c0 += CH) {
       uint4 q[CH];
       uint4 av[CH][SPC][NPG];
 #pragma unroll
       for (int j = 0; j < CH; ++j) {
-        // A chunk past the block end (CH not dividing it) gets zero planes:
-        // no branch, the accumulators stay in place.
+        // A slot past the block's last (CH not dividing cpb) gets zero planes:
+        // no branch, the accumulators stay in place.  Slots the block does not
+        // reach hold zero planes; their code loads stay inside the layer.
         const bool live = c0 + j < cpb;
-        const int64_t ch = c_block + min(c0 + j, cpb - 1);
-        q[j] = cbase[ch * kPanel];
+        const int jj = min(c0 + j, cpb - 1);
+        q[j] = cbase[min<int64_t>(c_first + jj, n_chunks - 1) * kPanel];
+        const int64_t slot = b * cpb + jj;
 #pragma unroll
         for (int s = 0; s < SPC; ++s)
 #pragma unroll
           for (int pg = 0; pg < NPG; ++pg) {
-            const uint4 v = planes[((ch * SPC + s) * NPG + pg) * 64 + lane];
+            const uint4 v = planes[((slot * SPC + s) * NPG + pg) * 64 + lane];
             av[j][s][pg] = live ? v : make_uint4(0u, 0u, 0u, 0u);
           }
       }
@@ -536,11 +546,9 @@ int segs_for(const sdq_layout* L, int seg) {
 
 // Decode variants: one activation row runs the addition-only table GEMV;
 // 2..16 rows run the integer-MFMA contraction, whose cost hardly grows with
-// the row count (it needs blocks that start on a code chunk, else the table
-// GEMV runs).  SDQ_DECODE_PATH=lut or =mfma forces one (a tuning and
-// cross-check aid; mfma still needs chunk-aligned blocks).
+// the row count.  SDQ_DECODE_PATH=lut or =mfma forces one (a tuning and
+// cross-check aid).
 bool use_mfma(const sdq_layout* L, int64_t m) {
-  if (L->m_up % (L->levels == 2 ? 128 : 64) != 0) return false;
   static const char* env = std::getenv("SDQ_DECODE_PATH");
   if (env && std::string(env) == "lut") return false;
   if (env && std::string(env) == "mfma") return true;
@@ -548,6 +556,20 @@ bool use_mfma(const sdq_layout* L, int64_t m) {
 }
 
 int npg_for(int64_t m) { return static_cast<int>((m + 3) / 4); }
+
+// Chunk slots per block in the plane layout: the most code chunks any block
+// touches (M / chunk when blocks start on chunks).
+int mfma_cpb(const sdq_layout* L) {
+  const int64_t cpc = L->levels == 2 ? 128 : 64;
+  int64_t most = 0;
+  for (int64_t b = 0; b < L->nb; ++b) {
+    const int64_t first = b * L->m_up / cpc;
+    const int64_t end = ((b + 1) * L->m_up + cpc - 1) / cpc;
+    most = std::max(most, end - first);
+    if (L->m_up % cpc == 0) break;                 // every block alike
+  }
+  return static_cast<int>(most);
+}
 
 // Blocks per wave of the MFMA GEMV (each split over K costs one atomic add per
 // output); SDQ_MFMA_BPW overrides.
@@ -569,7 +591,7 @@ int mfma_splits(const sdq_layout* L) {
 
 struct DecodeWs {
   float* xt;          // table path: x_tilde, m x k_up_pad fp32
-  uint32_t* planes;   // MFMA path: fixed-point planes, (k_up / 32) x npg x 512 bytes
+  uint32_t* planes;   // MFMA path: fixed-point planes, nb x cpb x (chunk / 64) k-steps x npg x 1 KB
   float* sx;          // MFMA path: per (row, block) plane scale, m x nb fp32
   size_t bytes;
 };
@@ -580,7 +602,8 @@ DecodeWs carve(const sdq_layout* L, int64_t m, void* base) {
   DecodeWs w{};
   char* p = static_cast<char*>(base);
   if (use_mfma(L, m)) {
-    const size_t pl = align_up(static_cast<size_t>(L->k_up / kStep) * npg_for(m) * 1024, 256);
+    const size_t steps = static_cast<size_t>(L->nb) * mfma_cpb(L) * (L->levels == 2 ? 2 : 1);
+    const size_t pl = align_up(steps * npg_for(m) * 1024, 256);
     w.planes = reinterpret_cast<uint32_t*>(p);
     w.sx = reinterpret_cast<float*>(p + pl);
     w.bytes = pl + align_up(static_cast<size_t>(m) * L->nb * 4, 256);
@@ -617,15 +640,15 @@ void launch_mfma_ch(const DecodeWs& w, const void* codes, const float* scales, c
   const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(n_panels));
   gemv_mfma_kernel<LEVELS, NPG, CH><<<grid, dim3(256), 0, stream>>>(
       static_cast<const uint4*>(codes), scales, reinterpret_cast<const uint4*>(w.planes), w.sx,
-      static_cast<int>(m), L->n, L->n_chunks, L->nb, L->m_up, bpw, splits, accumulate ? 1 : 0, y);
+      static_cast<int>(m), L->n, L->n_chunks, L->nb, L->m_up, mfma_cpb(L), bpw, splits,
+      accumulate ? 1 : 0, y);
 }
 
 template <int LEVELS>
 void launch_mfma_levels(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
                         int64_t m, float* y, bool acc, hipStream_t stream) {
   const int npg = npg_for(m);
-  const int cpb = L->m_up / (LEVELS == 2 ? 128 : 64);
-  const int ch = pick_ch(cpb, npg, LEVELS);
+  const int ch = pick_ch(mfma_cpb(L), npg, LEVELS);
 #define SDQ_CH(NPG_, CH_)                                                         \
   if (ch == CH_) return launch_mfma_ch<LEVELS, NPG_, CH_>(w, codes, scales, L, m, y, acc, stream)
   switch (npg) {
@@ -711,9 +734,11 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
   const dim3 egrid(static_cast<unsigned>(T->m_pad / 64), static_cast<unsigned>(L->nb));
   if (use_mfma(L, m)) {
     const int npg = npg_for(m);
+    const int cpb = mfma_cpb(L);
+    const dim3 pgrid(static_cast<unsigned>(cpb * (L->levels == 2 ? 2 : 1)), static_cast<unsigned>(L->nb));
 #define SDQ_PLANES(BB, LV)                                                                       \
-  expand_planes_kernel<BB, LV><<<egrid, dim3(kExpThreads), 0, stream>>>(                         \
-      x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad,                           \
+  expand_planes_kernel<BB, LV><<<pgrid, dim3(kExpThreads), 0, stream>>>(                         \
+      x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad, cpb,                      \
       reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, y_zero, y_count)
     if (L->levels == 2) {
       switch (B) {

@@ -67,6 +67,23 @@ def test_linear_block_sizes():
             assert np.all(err <= TOL), (block, m, err.max())
 
 
+@pytest.mark.parametrize("block,osr,levels", [(64, 1.5, 2), (64, 2.5, 3), (128, 1.25, 2),
+                                               (256, 2.125, 3), (256, 1.875, 2)])
+def test_linear_decode_blocks_inside_chunks(block, osr, levels):
+    # M = OSR * block not a multiple of the code chunk (64 ternary, 128 binary
+    # codes): blocks start and end inside chunks, and at block 64 binary a
+    # block is shorter than one chunk.
+    torch = require_gpu()
+    k = 8 * block
+    enc, r = _oracle_codes_on_device(torch, 130, k, osr, levels, seed=block + levels, block=block)
+    assert r.m_up % (128 if levels == 2 else 64) != 0
+    for m in (1, 2, 4, 9, 16):
+        x_dev, x64 = to_device_x(synth.activations_f32(17, 0, m, k), "f16", torch)
+        y = _run_linear(torch, enc, x_dev)
+        err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, block, r.m_up))
+        assert np.all(err <= TOL), (block, osr, levels, m, err.max())
+
+
 def test_linear_decode_repeatable():
     # Split-K decode adds partials with fp32 atomics: repeat calls agree to
     # rounding; a layer with a single K segment is bitwise repeatable.
