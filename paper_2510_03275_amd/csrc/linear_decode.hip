@@ -469,6 +469,7 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
     for (int e = 0; e < kSpan; e += 4)
       *reinterpret_cast<float4*>(dst + e) = build_quad<LEVELS>(xs, (e0 + e) / 4);
   }
+  __builtin_amdgcn_sched_barrier(0);     // the table is written before any code word is waited for
   __syncthreads();
 
   // 3. Lookups.
@@ -489,13 +490,11 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
         for (int i = 0; i < MR; ++i)
           acc[i] += *reinterpret_cast<const float*>(lbytes + (i * kRowFloats + (c * kGroupsPerChunk + wi * 8 + nib) * 16) * 4 + off);
       }
-      // With several activation rows, make each word's sums complete before
-      // the next word's table reads (otherwise the compiler sinks the adds
-      // and keeps every read live: register pressure).
-      if (MR > 1) {
+      // Make each word's sums complete before the next word's table reads
+      // (otherwise the compiler sinks the adds and keeps every read live:
+      // register pressure).
 #pragma unroll
-        for (int i = 0; i < MR; ++i) asm volatile("" : "+v"(acc[i]));
-      }
+      for (int i = 0; i < MR; ++i) asm volatile("" : "+v"(acc[i]));
     }
   }
 
@@ -503,6 +502,11 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
   //    row, otherwise an atomic add into y (zeroed beforehand, or holding the
   //    values to accumulate onto).
   const int64_t r = panel * kPanel + lane;
+  // A use of the code registers on every lane: otherwise the compiler sinks
+  // the code loads into the live-lane branch below, past the table build and
+  // its barrier, and the code stream starts only after the tables are built.
+#pragma unroll
+  for (int c = 0; c < SEG; ++c) asm volatile("" ::"v"(q[c].x));
   if (!panel_ok || r >= n) return;
   const float s = scales[r];
 #pragma unroll
