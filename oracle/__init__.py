@@ -8,8 +8,9 @@ share no code.
 
 Contents (each function cites the passage it follows):
 
-* ``hadamard``    -- Sylvester Hadamard matrices (Section 3.3, Eq. 13) and the
-                     fp32 fast Walsh-Hadamard transform used for block smoothing;
+* ``hadamard``    -- Sylvester Hadamard matrices (Section 3.3, Eq. 13), the
+                     fp32 fast Walsh-Hadamard transform used for block smoothing,
+                     and the choices of Had (Sylvester, sign-randomised, none);
 * ``resample``    -- the FFT ``Resample`` function of Algorithm 1 and the
                      closed forms of its up- and down-sampling matrices;
 * ``sigma_delta`` -- the binary / ternary quantizers (Eq. 3-6) and the

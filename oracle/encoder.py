@@ -3,7 +3,8 @@
 For every row r of W (N x K) and every block b of B consecutive columns
 (Algorithm 1, the loop over i = 0, B, 2B, ...):
 
-1. smoothing: v = W[r, bB:(b+1)B] * Had (Section 3.3; ``hadamard.rotate_blocks_f32``);
+1. smoothing: v = W[r, bB:(b+1)B] * Had (Section 3.3; ``hadamard.rotate_blocks_f32``;
+   Had is the Sylvester matrix, its sign-randomised form or the identity);
 2. ``SDQuant`` first resamples the block to M = round(OSR * B) samples
    (Algorithm 1, ``Resample(W, n * d_col)``), evaluated here in its closed form
    as a plain sum in fp32: x_up[m] = sum_t fl(v[t] * g32[p(t, m)]), added in
@@ -26,7 +27,7 @@ from dataclasses import dataclass
 
 import numpy as np
 
-from .hadamard import rotate_blocks_f32
+from .hadamard import HAD_SYLVESTER, rotate_blocks_f32
 from .resample import g_table_f32, phase_index
 from .sigma_delta import scan_f32
 
@@ -55,8 +56,11 @@ def upsample_f32(v: np.ndarray, block: int, m_up: int) -> np.ndarray:
     return acc
 
 
-def encode(w: np.ndarray, osr: float, levels: int, block: int = 256) -> EncodeResult:
-    """Encode fp32 weights W (N x K) into Sigma-Delta codes and per-row scales."""
+def encode(w: np.ndarray, osr: float, levels: int, block: int = 256,
+           hadamard: int = HAD_SYLVESTER, signs=None) -> EncodeResult:
+    """Encode fp32 weights W (N x K) into Sigma-Delta codes and per-row scales.
+
+    ``hadamard`` and ``signs`` select Had (``hadamard.rotate_blocks_f32``)."""
     w = np.asarray(w, dtype=np.float32)
     if w.ndim != 2:
         raise ValueError("W must be 2-D")
@@ -71,7 +75,7 @@ def encode(w: np.ndarray, osr: float, levels: int, block: int = 256) -> EncodeRe
     if m_up < block:
         raise ValueError("OSR below 1")
     nb = k // block
-    v = rotate_blocks_f32(w.reshape(n, nb, block))          # step 1
+    v = rotate_blocks_f32(w.reshape(n, nb, block), hadamard, signs)   # step 1
     x_up = upsample_f32(v, block, m_up)                      # step 2, (n, nb, M)
     s = np.max(np.abs(x_up).reshape(n, -1), axis=1).astype(np.float32) if n else \
         np.zeros(0, np.float32)                              # step 3
@@ -79,10 +83,11 @@ def encode(w: np.ndarray, osr: float, levels: int, block: int = 256) -> EncodeRe
     return EncodeResult(codes.reshape(n, nb * m_up), s, m_up, block)   # step 5
 
 
-def upsampled_rows_f32(w: np.ndarray, osr: float, block: int = 256) -> np.ndarray:
+def upsampled_rows_f32(w: np.ndarray, osr: float, block: int = 256,
+                       hadamard: int = HAD_SYLVESTER, signs=None) -> np.ndarray:
     """Steps 1-2 only: the fp32 upsampled rotated rows (N, nb*M), for tests."""
     w = np.asarray(w, dtype=np.float32)
     n, k = w.shape
     m_up = m_up_for(osr, block)
-    v = rotate_blocks_f32(w.reshape(n, k // block, block))
+    v = rotate_blocks_f32(w.reshape(n, k // block, block), hadamard, signs)
     return upsample_f32(v, block, m_up).reshape(n, -1)

@@ -3,12 +3,34 @@
 Section 3.3 defines a Hadamard matrix by H H^T = n I and builds it with the
 Sylvester recursion H_2k = [[H_k, H_k], [H_k, -H_k]] (Eq. 13).  Algorithm 1
 (line 6) multiplies each B-column weight block by ``Had`` before Sigma-Delta
-quantization and by ``Had^T`` afterwards, so ``Had`` must be orthogonal: this
-oracle uses the normalised Sylvester matrix Had = H_B / sqrt(B).
+quantization and by ``Had^T`` afterwards, so ``Had`` must be orthogonal.
+Three choices of ``Had`` (one B x B matrix shared by every block, as
+Algorithm 1's input list has it):
+
+* HAD_SYLVESTER: the normalised Sylvester matrix Had = H_B / sqrt(B);
+* HAD_SIGNED: Algorithm 1 calls its input a *random* Hadamard matrix without
+  saying how it is randomised; read here as Had = diag(s) H_B / sqrt(B) with
+  a vector s of B signs (+-1) drawn by the caller, which keeps Had orthogonal
+  and makes w Had the transform of the sign-flipped block w * s;
+* HAD_NONE: Had = I, the "without Hadamard" rows of the ablation (Table 2).
 """
 from __future__ import annotations
 
 import numpy as np
+
+HAD_NONE, HAD_SYLVESTER, HAD_SIGNED = 0, 1, 2
+
+
+def check_mode(mode: int, signs, block: int) -> np.ndarray | None:
+    """Validate (mode, signs) for blocks of length ``block``; returns the signs as int8."""
+    if mode not in (HAD_NONE, HAD_SYLVESTER, HAD_SIGNED):
+        raise ValueError("hadamard mode must be 0 (none), 1 (Sylvester) or 2 (signed)")
+    if mode != HAD_SIGNED:
+        return None
+    s = np.asarray(signs)
+    if s.shape != (block,) or not np.all((s == 1) | (s == -1)):
+        raise ValueError("signed Hadamard needs `block` signs in {-1, +1}")
+    return s.astype(np.int8)
 
 
 def sylvester(n: int) -> np.ndarray:
@@ -49,16 +71,31 @@ def inv_sqrt_f32(n: int) -> np.float32:
     return np.float32(1.0 / np.sqrt(np.float64(n)))
 
 
-def rotate_blocks_f32(w_blocks: np.ndarray) -> np.ndarray:
-    """w * Had for each length-B row block, in fp32: FWHT then one rounded scaling.
+def rotate_blocks_f32(w_blocks: np.ndarray, mode: int = HAD_SYLVESTER, signs=None) -> np.ndarray:
+    """w * Had for each length-B row block, in fp32.
 
-    Had = H_B / sqrt(B) is symmetric, so the row vector w Had equals (H_B w)/sqrt(B).
+    Sylvester: Had = H_B / sqrt(B) is symmetric, so the row vector w Had equals
+    (H_B w) / sqrt(B): FWHT then one rounded scaling.  Signed: w diag(s) is
+    w with the signs of its entries flipped where s = -1 (exact), then as
+    Sylvester.  None: w unchanged.
     """
     n = w_blocks.shape[-1]
-    y = fwht_f32(w_blocks)
+    s = check_mode(mode, signs, n)
+    if mode == HAD_NONE:
+        return np.array(w_blocks, dtype=np.float32, copy=True)
+    x = np.asarray(w_blocks, dtype=np.float32)
+    if mode == HAD_SIGNED:
+        x = np.where(s < 0, -x, x).astype(np.float32)
+    y = fwht_f32(x)
     return (y * inv_sqrt_f32(n)).astype(np.float32)
 
 
-def had_fp64(n: int) -> np.ndarray:
-    """Normalised Had = H_n / sqrt(n) in fp64 (orthogonal and symmetric)."""
-    return sylvester(n).astype(np.float64) / np.sqrt(np.float64(n))
+def had_fp64(n: int, mode: int = HAD_SYLVESTER, signs=None) -> np.ndarray:
+    """Had in fp64 (orthogonal): H_n / sqrt(n), diag(s) H_n / sqrt(n) or I."""
+    s = check_mode(mode, signs, n)
+    if mode == HAD_NONE:
+        return np.eye(n)
+    h = sylvester(n).astype(np.float64) / np.sqrt(np.float64(n))
+    if mode == HAD_SIGNED:
+        h = s.astype(np.float64)[:, None] * h
+    return h

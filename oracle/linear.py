@@ -23,42 +23,45 @@ from __future__ import annotations
 
 import numpy as np
 
-from .hadamard import had_fp64
+from .hadamard import HAD_SYLVESTER, had_fp64
 from .resample import resample_fft, down_matrix_fp64
 
 
-def reconstruct_fp64(codes: np.ndarray, scales: np.ndarray, block: int, m_up: int) -> np.ndarray:
+def reconstruct_fp64(codes: np.ndarray, scales: np.ndarray, block: int, m_up: int,
+                     hadamard: int = HAD_SYLVESTER, signs=None) -> np.ndarray:
     """W_hat (N x K) in fp64 from int8 codes (N x nb*M) and fp32 row scales."""
     codes = np.asarray(codes)
     n = codes.shape[0]
     nb = codes.shape[1] // m_up
     y = codes.astype(np.float64).reshape(n, nb, m_up) * np.asarray(scales, np.float64)[:, None, None]
     z = resample_fft(y, block)                       # Resample(Y, d_col), (n, nb, B)
-    q = z @ had_fp64(block).T                        # * Had^T
+    q = z @ had_fp64(block, hadamard, signs).T       # * Had^T
     return q.reshape(n, nb * block)
 
 
 def linear_fp64(x: np.ndarray, codes: np.ndarray, scales: np.ndarray, block: int,
-                m_up: int) -> np.ndarray:
+                m_up: int, hadamard: int = HAD_SYLVESTER, signs=None) -> np.ndarray:
     """y = x W_hat^T in fp64; x (m x K) in any float type (converted exactly)."""
-    w_hat = reconstruct_fp64(codes, scales, block, m_up)
+    w_hat = reconstruct_fp64(codes, scales, block, m_up, hadamard, signs)
     return np.asarray(x, dtype=np.float64) @ w_hat.T
 
 
-def expand_activations_fp64(x: np.ndarray, block: int, m_up: int) -> np.ndarray:
+def expand_activations_fp64(x: np.ndarray, block: int, m_up: int,
+                            hadamard: int = HAD_SYLVESTER, signs=None) -> np.ndarray:
     """x_tilde (m x nb*M): per block, (x_b Had) D^T, fp64."""
     x = np.asarray(x, dtype=np.float64)
     m, k = x.shape
     nb = k // block
-    h = x.reshape(m, nb, block) @ had_fp64(block)    # x_b Had
+    h = x.reshape(m, nb, block) @ had_fp64(block, hadamard, signs)   # x_b Had
     d = down_matrix_fp64(block, m_up)                # (M, B)
     return (h @ d.T).reshape(m, nb * m_up)
 
 
 def linear_via_expansion_fp64(x: np.ndarray, codes: np.ndarray, scales: np.ndarray,
-                              block: int, m_up: int) -> np.ndarray:
+                              block: int, m_up: int, hadamard: int = HAD_SYLVESTER,
+                              signs=None) -> np.ndarray:
     """y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j], fp64."""
-    xt = expand_activations_fp64(x, block, m_up)
+    xt = expand_activations_fp64(x, block, m_up, hadamard, signs)
     return (xt @ np.asarray(codes, np.float64).T) * np.asarray(scales, np.float64)[None, :]
 
 

@@ -132,6 +132,13 @@ def activations_f32(seed: int, stream: int, m: int, k: int) -> np.ndarray:
     return normal_f32(base, cnt, 1.0).reshape(m, k)
 
 
+def hadamard_signs(seed: int, block: int) -> np.ndarray:
+    """``block`` random signs (int8, +-1) for the sign-randomised Hadamard: sign
+    t is -1 when the top bit of hash t of stream (seed, 2**31) is set."""
+    h = hashes(stream_base(seed, 1 << 31), np.arange(block, dtype=np.uint64))
+    return np.where((h >> np.uint64(63)) == np.uint64(1), -1, 1).astype(np.int8)
+
+
 def to_f16(x32: np.ndarray) -> np.ndarray:
     return x32.astype(np.float16)
 

@@ -107,3 +107,34 @@ def test_synthetic_weights_deterministic_and_row_addressable():
     b = synth.weight_rows(7, 3, 20, 512, 0.02, True, rows=np.array([4, 19]))
     assert np.array_equal(a[[4, 19]], b)
     assert abs(float(np.std(synth.weight_rows(1, 0, 64, 1024, 0.02, False))) - 0.02) < 0.001
+
+
+@pytest.mark.parametrize("levels", [2, 3])
+def test_signed_hadamard_is_sylvester_on_sign_flipped_columns(levels):
+    # w diag(s) H / sqrt(B) = (w * s) H / sqrt(B): encoding W with the signed
+    # Had equals encoding W with its columns' signs flipped by s (tiled over
+    # the blocks) with the plain Sylvester Had, bit for bit.
+    import synth
+    from oracle import hadamard as Hd
+    rng = np.random.default_rng(11)
+    w = (rng.standard_normal((9, 512)) * 0.02).astype(np.float32)
+    s = synth.hadamard_signs(4, 256)
+    a = E.encode(w, 2.0, levels, 256, Hd.HAD_SIGNED, s)
+    b = E.encode((w * np.tile(s, 2)).astype(np.float32), 2.0, levels, 256)
+    assert np.array_equal(a.codes, b.codes)
+    assert np.array_equal(a.scales.view(np.uint32), b.scales.view(np.uint32))
+
+
+@pytest.mark.parametrize("levels", [2, 3])
+def test_no_hadamard_at_osr_one_is_plain_sigma_delta_of_the_weights(levels):
+    # Had = I and M = B: the resampling is the identity, so the codes are the
+    # Sigma-Delta scan of the raw weight blocks with the row absmax scale.
+    from oracle import hadamard as Hd
+    from oracle import sigma_delta as SD
+    rng = np.random.default_rng(12)
+    w = (rng.standard_normal((7, 512)) * 0.02).astype(np.float32)
+    r = E.encode(w, 1.0, levels, 256, Hd.HAD_NONE)
+    s = np.max(np.abs(w), axis=1).astype(np.float32)
+    want = SD.scan_f32(w.reshape(7, 2, 256), s[:, None], levels).reshape(7, 512)
+    assert np.array_equal(r.codes, want)
+    assert np.array_equal(r.scales, s)

@@ -65,3 +65,54 @@ def test_outlier_smoothing():
     y = H.rotate_blocks_f32(x)
     crest = lambda a: np.max(np.abs(a), axis=1) / np.sqrt(np.mean(a.astype(np.float64) ** 2, axis=1))
     assert np.all(crest(y) < 0.5 * crest(x))
+
+
+# --- choices of Had: Sylvester, sign-randomised diag(s) H / sqrt(B), none ---
+
+def test_signed_had_worked_example_n4():
+    # diag(s) H_4 / 2 with s = (+1, -1, +1, +1), written out by hand.
+    want = np.array([[1, 1, 1, 1],
+                     [-1, 1, -1, 1],
+                     [1, 1, -1, -1],
+                     [1, -1, -1, 1]], dtype=np.float64) / 2.0
+    got = H.had_fp64(4, H.HAD_SIGNED, np.array([1, -1, 1, 1]))
+    assert np.array_equal(got, want)
+
+
+@pytest.mark.parametrize("mode", [H.HAD_NONE, H.HAD_SYLVESTER, H.HAD_SIGNED])
+@pytest.mark.parametrize("n", [4, 64, 256])
+def test_every_had_is_orthogonal(mode, n):
+    s = np.where(np.random.default_rng(n).random(n) < 0.5, -1, 1)
+    h = H.had_fp64(n, mode, s if mode == H.HAD_SIGNED else None)
+    assert np.max(np.abs(h @ h.T - np.eye(n))) < 1e-13
+
+
+@pytest.mark.parametrize("n", [64, 256])
+def test_signed_rotation_matches_library_hadamard(n):
+    # w Had for Had = diag(s) H / sqrt(n), against scipy's Hadamard in fp64.
+    rng = np.random.default_rng(n + 1)
+    s = np.where(rng.random(n) < 0.5, -1, 1).astype(np.int8)
+    w = rng.standard_normal((6, n)).astype(np.float32)
+    want = (w.astype(np.float64) * s) @ scipy.linalg.hadamard(n) / np.sqrt(n)
+    got = H.rotate_blocks_f32(w, H.HAD_SIGNED, s)
+    assert np.max(np.abs(got - want)) < 1e-5 * np.max(np.abs(want))
+    # and the flip really is on the input side: the plain rotation of w differs
+    assert not np.allclose(H.rotate_blocks_f32(w), got)
+
+
+def test_signed_with_all_plus_signs_is_sylvester_bit_for_bit():
+    w = np.random.default_rng(5).standard_normal((4, 256)).astype(np.float32)
+    a = H.rotate_blocks_f32(w, H.HAD_SIGNED, np.ones(256, np.int8))
+    assert np.array_equal(a.view(np.uint32), H.rotate_blocks_f32(w).view(np.uint32))
+
+
+def test_no_hadamard_is_the_identity():
+    w = np.random.default_rng(6).standard_normal((3, 64)).astype(np.float32)
+    assert np.array_equal(H.rotate_blocks_f32(w, H.HAD_NONE).view(np.uint32), w.view(np.uint32))
+
+
+@pytest.mark.parametrize("mode,signs", [(3, None), (-1, None), (H.HAD_SIGNED, None),
+                                        (H.HAD_SIGNED, np.ones(63)), (H.HAD_SIGNED, np.zeros(64))])
+def test_bad_had_choices_are_rejected(mode, signs):
+    with pytest.raises(ValueError):
+        H.rotate_blocks_f32(np.zeros((1, 64), np.float32), mode, signs)
