@@ -4,7 +4,8 @@
  *
  * The library encodes fp32 weight matrices into binary or ternary
  * Sigma-Delta codes (Algorithm 1 without block compensation: block Hadamard
- * smoothing, Resample up to OSR x the block length, per-row scale,
+ * smoothing (Sylvester, sign-randomised or none), Resample up to OSR x the
+ * block length, per-row scale,
  * first-order Sigma-Delta scan) and evaluates y = x W_hat^T directly on the
  * codes (Fig. 5: the activations are expanded to the oversampled length and
  * contracted against the codes, additions only in the decode kernel).
@@ -13,8 +14,8 @@
  *  - Pointers named *_dev are device (HBM) pointers, *_host are host pointers.
  *    All memory is owned by the caller; the library never frees or retains a
  *    caller pointer.  The library owns only its cached coefficient tables
- *    (one set per device and (block, M) pair, allocated on first use, released
- *    by sdq_release_tables).
+ *    (one set per device and (block, M, Had) choice, allocated on first use,
+ *    released by sdq_release_tables).
  *  - `stream` is a hipStream_t passed as void* (NULL = the null stream).  GPU
  *    work is enqueued asynchronously on it; host-side argument errors are
  *    returned before anything is enqueued.
@@ -48,6 +49,20 @@ typedef enum {
 typedef enum { SDQ_F16 = 0, SDQ_BF16 = 1, SDQ_F32 = 2 } sdq_dtype;
 
 /*
+ * The smoothing matrix Had of Algorithm 1 (one B x B orthogonal matrix shared
+ * by every block; the weights are encoded as w_b Had and reconstructed with
+ * Had^T, Section 3.3):
+ *   SDQ_HAD_SYLVESTER  Had = H_B / sqrt(B), the Sylvester matrix of Eq. 13
+ *                      (the default of sdq_layout_init);
+ *   SDQ_HAD_SIGNED     Had = diag(s) H_B / sqrt(B) for B caller-drawn signs
+ *                      s_t in {-1, +1}: Algorithm 1 asks for a random
+ *                      Hadamard matrix without fixing how it is drawn; this
+ *                      sign flip keeps Had orthogonal;
+ *   SDQ_HAD_NONE       Had = I (the ablation without Hadamard, Table 2).
+ */
+typedef enum { SDQ_HAD_NONE = 0, SDQ_HAD_SYLVESTER = 1, SDQ_HAD_SIGNED = 2 } sdq_hadamard;
+
+/*
  * Geometry of one encoded linear layer (filled by sdq_layout_init; treat as
  * read-only).  Notation of the paper: the weight W has d_row = n rows and
  * d_col = k columns; Algorithm 1 splits the columns into blocks of B and
@@ -65,7 +80,9 @@ typedef struct sdq_layout {
   int64_t n_pad;           /* n rounded up to a multiple of 64                   */
   int64_t n_chunks;        /* 16-byte chunks per row = ceil(k_up / codes_per_chunk) */
   int32_t codes_per_chunk; /* 128 (binary) or 64 (ternary)                       */
-  int32_t reserved;
+  int32_t hadamard;        /* sdq_hadamard: the smoothing matrix Had             */
+  uint32_t had_signs[8];   /* SDQ_HAD_SIGNED: bit t (word t/32, bit t%32) set    */
+                           /* <=> s_t = -1, t < block; all zero otherwise        */
 } sdq_layout;
 
 /*
@@ -90,6 +107,15 @@ typedef struct sdq_layout {
  * 64/128/256 or k % block != 0), SDQ_ERR_OSR, SDQ_ERR_LEVELS. */
 sdq_status sdq_layout_init(sdq_layout* out, int64_t n, int64_t k, double osr,
                            int32_t levels, int32_t block);
+
+/* Select the smoothing matrix Had of a layout (Algorithm 1; sdq_hadamard).
+ *   mode         SDQ_HAD_NONE, SDQ_HAD_SYLVESTER or SDQ_HAD_SIGNED.
+ *   signs_host   SDQ_HAD_SIGNED: `block` int8 values, each -1 or +1 (host
+ *                memory, read during the call only); otherwise ignored (may
+ *                be NULL).
+ * Codes encoded under one choice must be evaluated with the same layout.
+ * Errors: SDQ_ERR_ARG (layout NULL, bad mode, signs missing or not +-1). */
+sdq_status sdq_layout_set_hadamard(sdq_layout* layout, int32_t mode, const int8_t* signs_host);
 
 /* Bytes of the packed code buffer: n_pad * n_chunks * 16 (0 for a NULL layout). */
 size_t sdq_codes_bytes(const sdq_layout* layout);
@@ -129,9 +155,13 @@ sdq_status sdq_quantize(const float* w_dev, const sdq_layout* layout, void* code
 sdq_status sdq_quantize_check(const void* workspace_dev, void* stream);
 
 /* Device workspace (bytes) sdq_linear needs for m activation rows: the
- * expanded activations at offset 0 (m x k_up rounded up to whole chunks;
- * fp32 for m <= 16, fp16 otherwise), then for m <= 16 a fixed block of
- * split-K counters and the split-K partial sums of this layout. */
+ * expanded activations, at offset 0 --
+ *   m = 1:        fp32 x_tilde, k_up rounded up to whole chunks;
+ *   2 <= m <= 16: x_tilde as 24-bit fixed point (three signed-byte planes,
+ *                 rows in groups of four, per block in chunk slots), then the
+ *                 fp32 plane scale of every (row, block);
+ *   m > 16:       fp16 x_tilde, m x k_up rounded up to whole chunks (twice,
+ *                 an fp16 pair hi + lo, for layouts with SDQ_HAD_NONE). */
 size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
 
 /*
@@ -222,10 +252,14 @@ sdq_status sdq_unpack_codes(const sdq_layout* layout, const void* codes_host, in
  * SDQ_ERR_SHAPE, SDQ_ERR_OSR. */
 sdq_status sdq_upsample_table(int32_t block, int32_t m_up, float* out_host);
 
-/* Upload the coefficient tables for (block, m_up) on the current device ahead
- * of time, so that later calls allocate nothing.  Errors: SDQ_ERR_SHAPE,
- * SDQ_ERR_OSR, SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
+/* Upload the coefficient tables for (block, m_up) with the Sylvester Had on
+ * the current device ahead of time, so that later calls allocate nothing.
+ * Errors: SDQ_ERR_SHAPE, SDQ_ERR_OSR, SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
 sdq_status sdq_prepare(int32_t block, int32_t m_up);
+
+/* As sdq_prepare, for the (block, M, Had) choice of a layout.
+ * Errors: SDQ_ERR_ARG (layout not from sdq_layout_init), SDQ_ERR_NOMEM, SDQ_ERR_HIP. */
+sdq_status sdq_prepare_layout(const sdq_layout* layout);
 
 /* Free every cached coefficient table (all devices).  No call may be in flight. */
 void sdq_release_tables(void);

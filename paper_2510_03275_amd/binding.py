@@ -19,6 +19,7 @@ LIB_PATH = os.path.join(_HERE, "libsdq.so")
 
 SDQ_OK = 0
 SDQ_F16, SDQ_BF16, SDQ_F32 = 0, 1, 2
+SDQ_HAD_NONE, SDQ_HAD_SYLVESTER, SDQ_HAD_SIGNED = 0, 1, 2
 
 STATUS_NAMES = {
     0: "SDQ_OK", -1: "SDQ_ERR_ARG", -2: "SDQ_ERR_SHAPE", -3: "SDQ_ERR_OSR", -4: "SDQ_ERR_LEVELS",
@@ -40,12 +41,14 @@ class sdq_layout(ctypes.Structure):
         ("levels", ctypes.c_int32), ("bits", ctypes.c_int32),
         ("nb", ctypes.c_int64), ("k_up", ctypes.c_int64),
         ("n_pad", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
-        ("codes_per_chunk", ctypes.c_int32), ("reserved", ctypes.c_int32),
+        ("codes_per_chunk", ctypes.c_int32), ("hadamard", ctypes.c_int32),
+        ("had_signs", ctypes.c_uint32 * 8),
     ]
 
     def __repr__(self):
         return (f"sdq_layout(n={self.n}, k={self.k}, block={self.block}, m_up={self.m_up}, "
-                f"levels={self.levels}, k_up={self.k_up}, n_pad={self.n_pad}, n_chunks={self.n_chunks})")
+                f"levels={self.levels}, k_up={self.k_up}, n_pad={self.n_pad}, n_chunks={self.n_chunks}, "
+                f"hadamard={self.hadamard})")
 
 
 def hip_runtimes_loaded() -> list:
@@ -70,6 +73,7 @@ def _load() -> ctypes.CDLL:
     sig = {
         "sdq_layout_init": (ctypes.c_int, [L, ctypes.c_int64, ctypes.c_int64, ctypes.c_double,
                                            ctypes.c_int32, ctypes.c_int32]),
+        "sdq_layout_set_hadamard": (ctypes.c_int, [L, ctypes.c_int32, P]),
         "sdq_codes_bytes": (ctypes.c_size_t, [L]),
         "sdq_compression_ratio": (ctypes.c_double, [L]),
         "sdq_quantize_workspace_bytes": (ctypes.c_size_t, [L]),
@@ -89,6 +93,7 @@ def _load() -> ctypes.CDLL:
         "sdq_unpack_codes": (ctypes.c_int, [L, P, P]),
         "sdq_upsample_table": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32, P]),
         "sdq_prepare": (ctypes.c_int, [ctypes.c_int32, ctypes.c_int32]),
+        "sdq_prepare_layout": (ctypes.c_int, [L]),
         "sdq_release_tables": (None, []),
         "sdq_status_string": (ctypes.c_char_p, [ctypes.c_int]),
         "sdq_last_error": (ctypes.c_char_p, []),
@@ -137,6 +142,17 @@ def sdq_layout_init(n: int, k: int, osr: float, levels: int, block: int = 256) -
     out = sdq_layout()
     _check(_lib.sdq_layout_init(ctypes.byref(out), n, k, float(osr), levels, block))
     return out
+
+
+def sdq_layout_set_hadamard(layout: sdq_layout, mode: int, signs=None) -> sdq_layout:
+    """Select Had for the layout (in place; also returned).  ``signs``: `block`
+    values of +-1 for SDQ_HAD_SIGNED."""
+    buf = None
+    if signs is not None:
+        buf = np.ascontiguousarray(signs, dtype=np.int8)
+    _check(_lib.sdq_layout_set_hadamard(ctypes.byref(layout), int(mode),
+                                        None if buf is None else buf.ctypes.data))
+    return layout
 
 
 def sdq_codes_bytes(layout: sdq_layout) -> int:
@@ -227,6 +243,10 @@ def sdq_prepare(block: int, m_up: int) -> None:
     _check(_lib.sdq_prepare(block, m_up))
 
 
+def sdq_prepare_layout(layout: sdq_layout) -> None:
+    _check(_lib.sdq_prepare_layout(ctypes.byref(layout)))
+
+
 def sdq_release_tables() -> None:
     _lib.sdq_release_tables()
 
@@ -247,12 +267,16 @@ class Encoded:
 
 
 def quantize(w, osr: float, levels: int, block: int = 256, workspace=None, check: bool = True,
-             stream=None) -> Encoded:
-    """Encode a device fp32 weight [n, k]; returns codes, scales and layout."""
+             stream=None, hadamard: int = SDQ_HAD_SYLVESTER, signs=None) -> Encoded:
+    """Encode a device fp32 weight [n, k]; returns codes, scales and layout.
+
+    ``hadamard`` / ``signs`` choose Had (see sdq_layout_set_hadamard)."""
     import torch
     if w.dtype != torch.float32 or not w.is_cuda or not w.is_contiguous():
         raise ValueError("w must be a contiguous fp32 device tensor")
     layout = sdq_layout_init(w.shape[0], w.shape[1], osr, levels, block)
+    if hadamard != SDQ_HAD_SYLVESTER:
+        sdq_layout_set_hadamard(layout, hadamard, signs)
     codes = torch.empty(sdq_codes_bytes(layout), dtype=torch.uint8, device=w.device)
     scales = torch.empty(layout.n, dtype=torch.float32, device=w.device)
     need = sdq_quantize_workspace_bytes(layout)

@@ -42,18 +42,24 @@ __global__ void clear_kernel(uint32_t* __restrict__ flag, uint32_t* __restrict__
   if (i < n) rmax[i] = 0u;
 }
 
+// Sign words of the signed Had (bit t set <=> s_t = -1), passed by value.
+struct SignMask {
+  uint32_t w[8];
+};
+
 // One workgroup: 64 rows x one block of B columns, four lanes per row.  Lane
 // (row, q) holds the B/4 elements t = 16 j + 4 q + e (j < B/16, e < 4) of its
 // row, loaded as float4 (a wave reads 64 contiguous bytes of each of its 16
-// rows per load).  The transform runs in registers in the stage order
+// rows per load).  For the signed Had the signs flip first (exact); the
+// transform (skipped for Had = I) runs in registers in the stage order
 // h = 1, 2 (bits of e), 4, 8 (bits of q: partner lanes xor 1, 2), 16, ...,
 // B/2 (bits of j); every stage pairs the same elements and rounds the same
 // sums and differences as the textbook loop, so the result is bit-identical.
 template <int B>
 __global__ __launch_bounds__(kRotThreads) void rotate_kernel(
     const float* __restrict__ w, int64_t n, int64_t k, int64_t n_ws, int64_t k_up, int m_up,
-    int g0, int phases, float inv_sqrt_b, float* __restrict__ v, float* __restrict__ xup,
-    uint32_t* __restrict__ rmax, uint32_t* __restrict__ flag) {
+    int g0, int phases, int had, SignMask sm, float inv_sqrt_b, float* __restrict__ v,
+    float* __restrict__ xup, uint32_t* __restrict__ rmax, uint32_t* __restrict__ flag) {
   constexpr int J = B / 16;
   const int tid = threadIdx.x;
   const int q = tid & 3;
@@ -81,6 +87,20 @@ __global__ __launch_bounds__(kRotThreads) void rotate_kernel(
       for (int e = 0; e < 4; ++e) x[j][e] = 0.0f;   // padding rows: zeros
   }
   if (bad) atomicOr(flag, 1u);
+  // Signed Had = diag(s) H / sqrt(B): flip the sign of w_t where s_t = -1
+  // (exact); element (j, e) of this lane is t = 16 j + 4 q + e, in sign word
+  // j / 2 at bit 16 (j % 2) + 4 q + e.
+  if (had == SDQ_HAD_SIGNED) {
+#pragma unroll
+    for (int j = 0; j < J; ++j)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const uint32_t bit = (sm.w[j / 2] >> (16 * (j % 2) + 4 * q + e)) & 1u;
+        x[j][e] = __uint_as_float(__float_as_uint(x[j][e]) ^ (bit << 31));
+      }
+  }
+  // Had = I: no transform (the launch passes a scale of 1).
+  if (had != SDQ_HAD_NONE) {
   // h = 1, 2: inside the float4.
 #pragma unroll
   for (int j = 0; j < J; ++j) {
@@ -123,6 +143,7 @@ __global__ __launch_bounds__(kRotThreads) void rotate_kernel(
           x[j][e] = a + c;
           x[j + hj][e] = a - c;
         }
+  }
   // Scale; store rows-contiguous per t; copy the unit-impulse samples
   // (t = i * B / g0 feeds sample m = i * P); fold their |v| into the row max.
   const int stride_mask = B / g0 - 1;          // B / g0 is a power of two
@@ -306,24 +327,27 @@ sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T,
   const int64_t n_panels = L->n_pad / kPanel;
   const int64_t n_ws = quant_ws_rows(L);     // rows covered by the upsample tiles
   const int B = L->block;
-  const float inv_sqrt_b = static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
+  const float inv_sqrt_b =
+      L->hadamard == SDQ_HAD_NONE ? 1.0f : static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
+  SignMask sm;
+  for (int i = 0; i < 8; ++i) sm.w[i] = L->hadamard == SDQ_HAD_SIGNED ? L->had_signs[i] : 0u;
   clear_kernel<<<dim3(static_cast<unsigned>((L->n_pad + 255) / 256)), dim3(256), 0, stream>>>(
       ws.flag, ws.rmax, L->n_pad);
   const dim3 rgrid(static_cast<unsigned>(n_ws / kPanel), static_cast<unsigned>(L->nb));
   switch (B) {
     case 64:
       rotate_kernel<64><<<rgrid, dim3(kRotThreads), 0, stream>>>(
-          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, inv_sqrt_b, ws.v, ws.xup,
+          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, L->hadamard, sm, inv_sqrt_b, ws.v, ws.xup,
           ws.rmax, ws.flag);
       break;
     case 128:
       rotate_kernel<128><<<rgrid, dim3(kRotThreads), 0, stream>>>(
-          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, inv_sqrt_b, ws.v, ws.xup,
+          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, L->hadamard, sm, inv_sqrt_b, ws.v, ws.xup,
           ws.rmax, ws.flag);
       break;
     default:
       rotate_kernel<256><<<rgrid, dim3(kRotThreads), 0, stream>>>(
-          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, inv_sqrt_b, ws.v, ws.xup,
+          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, L->hadamard, sm, inv_sqrt_b, ws.v, ws.xup,
           ws.rmax, ws.flag);
       break;
   }

@@ -5,7 +5,8 @@
 //            batched GEMM.  E is held as an fp16 pair hi + lo, so x E_hi + x E_lo
 //            reproduces the fp64 product to ~2^-22 relative for fp16 / bf16
 //            inputs (both exact in fp16 at these magnitudes); fp32 inputs add
-//            x_lo E_hi.  The result is rounded once to fp16.
+//            x_lo E_hi.  The result is rounded once to fp16 (without Had also
+//            kept as an fp16 pair, the GEMM then running over both halves).
 //   gemm     y[i, r] = s_r * sum_j x_tilde[i, j] C[r, j]: the codes are expanded
 //            in registers to fp16 +1 / 0 / -1 and fed to the same MFMA.  This
 //            is the contraction of Fig. 5 at prefill batch sizes, where it is a
@@ -31,7 +32,6 @@ namespace {
 typedef _Float16 half8 __attribute__((ext_vector_type(8)));
 typedef float floatx16 __attribute__((ext_vector_type(16)));
 
-constexpr int kExpWaves = 4;          // expand: 32 rows x (4 x 128) samples per workgroup
 
 __device__ inline floatx16 mfma32(const half8& a, const half8& b, const floatx16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
@@ -48,129 +48,6 @@ __device__ inline int64_t xcd_tile(int64_t id, int64_t n) {
   return xcd * per + (xcd < rem ? xcd : rem) + j;
 }
 
-// Loads 8 consecutive activations as fp16 hi (and lo for fp32 inputs).
-__device__ inline void load_x8(const void* x, sdq_dtype xt, int64_t idx, bool ok, half8& hi, half8& lo) {
-  if (!ok) {
-    for (int q = 0; q < 8; ++q) { hi[q] = 0; lo[q] = 0; }
-    return;
-  }
-  if (xt == SDQ_F16) {
-    hi = *reinterpret_cast<const half8*>(static_cast<const _Float16*>(x) + idx);
-    for (int q = 0; q < 8; ++q) lo[q] = 0;
-  } else if (xt == SDQ_BF16) {
-    const uint4 raw = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + idx);
-    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-    for (int q = 0; q < 8; ++q) {
-      const uint32_t bits = ((w[q / 2] >> (16 * (q % 2))) & 0xFFFFu) << 16;
-      const float f = __uint_as_float(bits);
-      hi[q] = static_cast<_Float16>(f);
-      lo[q] = static_cast<_Float16>(f - static_cast<float>(hi[q]));
-    }
-  } else {
-    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(x) + idx);
-    const float4 c = *reinterpret_cast<const float4*>(static_cast<const float*>(x) + idx + 4);
-    const float f[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
-    for (int q = 0; q < 8; ++q) {
-      hi[q] = static_cast<_Float16>(f[q]);
-      lo[q] = static_cast<_Float16>(f[q] - static_cast<float>(hi[q]));
-    }
-  }
-}
-
-// load_x8 with the input type fixed at compile time (hi only unless XT is fp32).
-template <sdq_dtype XT>
-__device__ inline void load_x8_t(const void* x, int64_t idx, bool ok, half8& hi, half8& lo) {
-  if (!ok) {
-    for (int q = 0; q < 8; ++q) { hi[q] = 0; lo[q] = 0; }
-    return;
-  }
-  if (XT == SDQ_F16) {
-    hi = *reinterpret_cast<const half8*>(static_cast<const _Float16*>(x) + idx);
-  } else if (XT == SDQ_BF16) {
-    const uint4 raw = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + idx);
-    const uint32_t w[4] = {raw.x, raw.y, raw.z, raw.w};
-    for (int q = 0; q < 8; ++q)
-      hi[q] = static_cast<_Float16>(__uint_as_float(((w[q / 2] >> (16 * (q % 2))) & 0xFFFFu) << 16));
-  } else {
-    const float4 a = *reinterpret_cast<const float4*>(static_cast<const float*>(x) + idx);
-    const float4 c = *reinterpret_cast<const float4*>(static_cast<const float*>(x) + idx + 4);
-    const float f[8] = {a.x, a.y, a.z, a.w, c.x, c.y, c.z, c.w};
-    for (int q = 0; q < 8; ++q) {
-      hi[q] = static_cast<_Float16>(f[q]);
-      lo[q] = static_cast<_Float16>(f[q] - static_cast<float>(hi[q]));
-    }
-  }
-}
-
-// One wave: 32 activation rows x 128 samples (4 accumulator tiles) of one
-// block; a workgroup: 4 waves side by side along the samples.  Per k step of
-// 16 the wave loads one x fragment (8 values per lane) and four E^T hi / lo
-// fragments, next step prefetched.
-__global__ __launch_bounds__(64 * kExpWaves) void expand_prefill_kernel(
-    const void* __restrict__ x, sdq_dtype xt, int64_t m, int64_t k, int B, int m_up,
-    int64_t k_up, int64_t k_up_pad, const uint16_t* __restrict__ et_hi,
-    const uint16_t* __restrict__ et_lo, _Float16* __restrict__ xt_out) {
-  const int lane = threadIdx.x % 64;
-  const int wave = threadIdx.x / 64;
-  const int64_t b = blockIdx.x;
-  const int c0 = (blockIdx.y * kExpWaves + wave) * 128;
-  const int64_t i0 = static_cast<int64_t>(blockIdx.z) * 32;
-  if (b == 0 && blockIdx.y == 0) {
-    // Zero the padding columns of these 32 rows.
-    const int64_t pad = k_up_pad - k_up;
-    for (int64_t idx = threadIdx.x; idx < 32 * pad; idx += 64 * kExpWaves) {
-      const int64_t i = i0 + idx / pad;
-      if (i < m) xt_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
-    }
-  }
-  if (c0 >= m_up) return;
-  const int64_t row = i0 + lane % 32;
-  const int kg = (lane / 32) * 8;
-  const bool row_ok = row < m;
-  // fp16 and bf16 activations are exact in fp16 here (bf16 has the shorter
-  // mantissa); only fp32 inputs need their low part.
-  const bool need_lo = xt == SDQ_F32;
-  int cols[4];
-  bool col_ok[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    cols[j] = c0 + 32 * j + lane % 32;
-    col_ok[j] = c0 + 32 * j < m_up;           // M is a multiple of 32
-    if (!col_ok[j]) cols[j] = c0 + lane % 32;
-  }
-  floatx16 acc[4];
-#pragma unroll
-  for (int j = 0; j < 4; ++j)
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[j][v] = 0.0f;
-  for (int t0 = 0; t0 < B; t0 += 16) {
-    half8 ahi, alo;
-    load_x8(x, xt, row * k + b * B + t0 + kg, row_ok, ahi, alo);
-    half8 bh[4], bl[4];
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const int64_t off = static_cast<int64_t>(cols[j]) * B + t0 + kg;
-      bh[j] = *reinterpret_cast<const half8*>(et_hi + off);
-      bl[j] = *reinterpret_cast<const half8*>(et_lo + off);
-    }
-#pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      acc[j] = mfma32(ahi, bh[j], acc[j]);
-      acc[j] = mfma32(ahi, bl[j], acc[j]);
-      if (need_lo) acc[j] = mfma32(alo, bh[j], acc[j]);
-    }
-  }
-#pragma unroll
-  for (int j = 0; j < 4; ++j) {
-    if (!col_ok[j]) continue;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) {
-      const int64_t i = i0 + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
-      if (i < m) xt_out[i * k_up_pad + b * m_up + cols[j]] = static_cast<_Float16>(acc[j][v]);
-    }
-  }
-}
-
 // Tiled expansion: workgroup tile kXTM activation rows x 128 samples of one
 // block, t in steps of 64 through LDS (x as fp16 hi (+ lo for fp32 inputs),
 // E^T as fp16 hi and lo), so each operand element fetched from memory feeds
@@ -185,7 +62,8 @@ template <sdq_dtype XT, int kXTM>
 __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
     const void* __restrict__ x, int64_t m, int64_t k, int B, int m_up,
     int64_t k_up, int64_t k_up_pad, const uint16_t* __restrict__ et_hi,
-    const uint16_t* __restrict__ et_lo, _Float16* __restrict__ xt_out) {
+    const uint16_t* __restrict__ et_lo, _Float16* __restrict__ xt_out,
+    _Float16* __restrict__ xt_lo_out) {
   constexpr bool NEED_LO = XT == SDQ_F32;
   __shared__ __attribute__((aligned(16))) _Float16 xs[NEED_LO ? 2 : 1][kXTM * kXLd];
   __shared__ __attribute__((aligned(16))) _Float16 es[2][kXTN * kXLd];
@@ -205,7 +83,10 @@ __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
     const int64_t pad = k_up_pad - k_up;            // zero the padding columns of these rows
     for (int64_t idx = tid; idx < kXTM * pad; idx += 256) {
       const int64_t i = i0 + idx / pad;
-      if (i < m) xt_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
+      if (i < m) {
+        xt_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
+        if (xt_lo_out) xt_lo_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
+      }
     }
   }
   constexpr int RT = kXTM / 64;                    // 32-row tiles per wave
@@ -327,7 +208,13 @@ __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
         const int64_t i = i0 + 32 * RT * wr + 32 * rt + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
-        if (i < m) xt_out[i * k_up_pad + b * m_up + col] = static_cast<_Float16>(acc[rt][ct][v]);
+        if (i < m) {
+          const _Float16 hi = static_cast<_Float16>(acc[rt][ct][v]);
+          xt_out[i * k_up_pad + b * m_up + col] = hi;
+          if (xt_lo_out)
+            xt_lo_out[i * k_up_pad + b * m_up + col] =
+                static_cast<_Float16>(acc[rt][ct][v] - static_cast<float>(hi));
+        }
       }
   }
 }
@@ -504,38 +391,36 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
 
 }  // namespace
 
+// Without Had the row scales follow the weights' outliers and the layer
+// output can be small next to s_r |x_tilde|: one fp16 rounding of x_tilde
+// then exceeds the 1e-3 budget.  Those layouts keep x_tilde as an fp16 pair
+// hi + lo and run the GEMM on both.
+bool prefill_split(const sdq_layout* L) { return L->hadamard == SDQ_HAD_NONE; }
+
 size_t prefill_ws_bytes(const sdq_layout* L, int64_t m) {
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
-  return align_up(static_cast<size_t>(m) * k_up_pad * 2, 256);
+  return align_up(static_cast<size_t>(m) * k_up_pad * 2, 256) * (prefill_split(L) ? 2 : 1);
 }
 
 sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
                                  const Tables* T, void* ws, hipStream_t stream) {
   _Float16* xbuf = static_cast<_Float16*>(ws);
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
-  if (L->block % kXTK == 0) {
-    // Sample tiles fastest: neighbouring workgroups share the x tile.
-    static const char* env = std::getenv("SDQ_XTM");   // tuning aid: 128 or 256 rows per tile
-    const int tm = env && std::atoi(env) == 256 ? 256 : 128;
-    const dim3 tgrid(static_cast<unsigned>(((L->m_up + kXTN - 1) / kXTN) * L->nb * ((m + tm - 1) / tm)));
-#define SDQ_XT(XT, TM)                                                                          \
-  expand_prefill_tiled_kernel<XT, TM><<<tgrid, dim3(256), 0, stream>>>(                         \
-      x, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf)
-    if (xt == SDQ_F32) {
-      if (tm == 256) SDQ_XT(SDQ_F32, 256); else SDQ_XT(SDQ_F32, 128);
-    } else if (xt == SDQ_BF16) {
-      if (tm == 256) SDQ_XT(SDQ_BF16, 256); else SDQ_XT(SDQ_BF16, 128);
-    } else {
-      if (tm == 256) SDQ_XT(SDQ_F16, 256); else SDQ_XT(SDQ_F16, 128);
-    }
+  _Float16* xlo = prefill_split(L)
+                      ? reinterpret_cast<_Float16*>(static_cast<char*>(ws) +
+                                                    align_up(static_cast<size_t>(m) * k_up_pad * 2, 256))
+                      : nullptr;
+  // Sample tiles fastest: neighbouring workgroups share the x tile.  B is a
+  // multiple of the 64-wide t step for every supported block.
+  constexpr int tm = 128;
+  const dim3 tgrid(static_cast<unsigned>(((L->m_up + kXTN - 1) / kXTN) * L->nb * ((m + tm - 1) / tm)));
+#define SDQ_XT(XT)                                                                              \
+  expand_prefill_tiled_kernel<XT, tm><<<tgrid, dim3(256), 0, stream>>>(                         \
+      x, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf, xlo)
+  if (xt == SDQ_F32) SDQ_XT(SDQ_F32);
+  else if (xt == SDQ_BF16) SDQ_XT(SDQ_BF16);
+  else SDQ_XT(SDQ_F16);
 #undef SDQ_XT
-  } else {
-    const dim3 egrid(static_cast<unsigned>(L->nb),
-                     static_cast<unsigned>((L->m_up / 128 + (L->m_up % 128 ? 1 : 0) + kExpWaves - 1) / kExpWaves),
-                     static_cast<unsigned>((m + 31) / 32));
-    expand_prefill_kernel<<<egrid, dim3(64 * kExpWaves), 0, stream>>>(
-        x, xt, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf);
-  }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "prefill expansion launch");
   return SDQ_OK;
@@ -544,24 +429,27 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
 sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
                                    const sdq_layout* L, float* y, bool accumulate, void* ws,
                                    hipStream_t stream) {
-  const _Float16* xbuf = static_cast<const _Float16*>(ws);
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
+  const size_t plane = align_up(static_cast<size_t>(m) * k_up_pad * 2, 256);
   // The kernel addresses x_tilde with 32-bit element offsets: launch row
   // chunks of at most 2^31 elements.
   const int64_t rows_max = std::max<int64_t>(kBM, ((int64_t{1} << 31) / k_up_pad) / kBM * kBM);
-  for (int64_t r0 = 0; r0 < m; r0 += rows_max) {
-    const int64_t mm = std::min(rows_max, m - r0);
-    const dim3 ggrid(static_cast<unsigned>((L->n + kBN - 1) / kBN), static_cast<unsigned>((mm + kBM - 1) / kBM));
-    const _Float16* xc = xbuf + r0 * k_up_pad;
-    float* yc = y + r0 * L->n;
-    if (L->levels == 2)
-      gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(
-          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc,
-          accumulate ? 1 : 0);
-    else
-      gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(
-          xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc,
-          accumulate ? 1 : 0);
+  const int passes = prefill_split(L) ? 2 : 1;   // x_tilde hi, then lo added on
+  for (int pass = 0; pass < passes; ++pass) {
+    const _Float16* xbuf = reinterpret_cast<const _Float16*>(static_cast<const char*>(ws) + pass * plane);
+    const int acc = accumulate || pass > 0 ? 1 : 0;
+    for (int64_t r0 = 0; r0 < m; r0 += rows_max) {
+      const int64_t mm = std::min(rows_max, m - r0);
+      const dim3 ggrid(static_cast<unsigned>((L->n + kBN - 1) / kBN), static_cast<unsigned>((mm + kBM - 1) / kBM));
+      const _Float16* xc = xbuf + r0 * k_up_pad;
+      float* yc = y + r0 * L->n;
+      if (L->levels == 2)
+        gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(
+            xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc, acc);
+      else
+        gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(
+            xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc, acc);
+    }
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "prefill GEMM launch");

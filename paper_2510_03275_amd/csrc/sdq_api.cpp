@@ -7,6 +7,7 @@
 #include <cstdarg>
 #include <cstdio>
 #include <cstring>
+#include <array>
 #include <map>
 #include <mutex>
 #include <numeric>
@@ -73,15 +74,17 @@ static int64_t gcd64(int64_t a, int64_t b) {
 
 constexpr int kUpsampleTileN = 64;   // column tile of the upsampling kernel
 
+using SignWords = std::array<uint32_t, 8>;
 static std::mutex g_tables_mutex;
-static std::map<std::tuple<int, int, int>, Tables> g_tables;
+static std::map<std::tuple<int, int, int, int, SignWords>, Tables> g_tables;
 
-sdq_status get_tables(int block, int m_up, const Tables** out) {
+static sdq_status get_tables_for(int block, int m_up, int had, const SignWords& signs,
+                                 const Tables** out) {
   int dev = 0;
   hipError_t e = hipGetDevice(&dev);
   if (e != hipSuccess) return hip_error(e, "hipGetDevice");
   std::lock_guard<std::mutex> lock(g_tables_mutex);
-  auto key = std::make_tuple(dev, block, m_up);
+  auto key = std::make_tuple(dev, block, m_up, had, signs);
   auto it = g_tables.find(key);
   if (it != g_tables.end()) {
     *out = &it->second;
@@ -90,6 +93,8 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
   Tables T;
   T.block = block;
   T.m_up = m_up;
+  T.hadamard = had;
+  std::copy(signs.begin(), signs.end(), T.signs);
   T.g0 = static_cast<int>(gcd64(block, m_up));
   T.phases = m_up / T.g0;
   T.m_nz = m_up - T.g0;
@@ -113,7 +118,8 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
     if (e != hipSuccess) return hip_error(e, "table upload");
   }
   // E^T[m][t] = sum_u Had[t][u] D[m][u]: a Walsh-Hadamard transform of each row
-  // of D (fp64), scaled by 1/sqrt(B); kept in fp32 and as two fp16 terms.
+  // of D (fp64), scaled by 1/sqrt(B), its entry t negated where s_t = -1 for
+  // the signed Had, or D itself without Had; kept in fp32 and as two fp16 terms.
   const size_t em = static_cast<size_t>(m_up) * block;
   T.m_pad = (m_up + 63) / 64 * 64;
   std::vector<float> edec(static_cast<size_t>(T.m_pad) * block, 0.0f);
@@ -123,16 +129,22 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
   double e1max = 0.0;   // max over samples m of sum_t |fp32(E[t][m])|
   for (int m = 0; m < m_up; ++m) {
     for (int t = 0; t < block; ++t) row[t] = downsample_entry(m, t, block, m_up);
-    for (int h = 1; h < block; h <<= 1)
-      for (int i = 0; i < block; i += 2 * h)
-        for (int j = i; j < i + h; ++j) {
-          const double a = row[j], c = row[j + h];
-          row[j] = a + c;
-          row[j + h] = a - c;
-        }
+    if (had != SDQ_HAD_NONE) {
+      for (int h = 1; h < block; h <<= 1)
+        for (int i = 0; i < block; i += 2 * h)
+          for (int j = i; j < i + h; ++j) {
+            const double a = row[j], c = row[j + h];
+            row[j] = a + c;
+            row[j + h] = a - c;
+          }
+      for (int t = 0; t < block; ++t) {
+        row[t] *= inv_sqrt_b;
+        if (had == SDQ_HAD_SIGNED && (signs[t / 32] >> (t % 32) & 1u)) row[t] = -row[t];
+      }
+    }
     double col1 = 0.0;
     for (int t = 0; t < block; ++t) {
-      const double val = row[t] * inv_sqrt_b;
+      const double val = row[t];
       const size_t at = static_cast<size_t>(m) * block + t;
       edec[(static_cast<size_t>(t / 4) * T.m_pad + m) * 4 + t % 4] = static_cast<float>(val);
       col1 += std::fabs(static_cast<double>(static_cast<float>(val)));
@@ -161,7 +173,26 @@ sdq_status get_tables(int block, int m_up, const Tables** out) {
   return SDQ_OK;
 }
 
+sdq_status get_tables(const sdq_layout* L, const Tables** out) {
+  SignWords w{};
+  if (L->hadamard == SDQ_HAD_SIGNED) std::copy(L->had_signs, L->had_signs + 8, w.begin());
+  return get_tables_for(L->block, L->m_up, L->hadamard, w, out);
+}
+
 static bool valid_block(int b) { return b == 64 || b == 128 || b == 256; }
+
+// The Had choice: a known mode, sign bits only below the block for the
+// signed Had and none otherwise.
+static bool valid_hadamard(const sdq_layout* L) {
+  if (L->hadamard != SDQ_HAD_NONE && L->hadamard != SDQ_HAD_SYLVESTER && L->hadamard != SDQ_HAD_SIGNED)
+    return false;
+  for (int i = 0; i < 8; ++i) {
+    const uint32_t allowed = L->hadamard != SDQ_HAD_SIGNED || 32 * i >= L->block ? 0u
+                             : (32 * (i + 1) <= L->block ? ~0u : (1u << (L->block - 32 * i)) - 1u);
+    if (L->had_signs[i] & ~allowed) return false;
+  }
+  return true;
+}
 
 static sdq_status check_layout(const sdq_layout* L) {
   if (!L) return set_error(SDQ_ERR_ARG, "layout is NULL");
@@ -171,7 +202,7 @@ static sdq_status check_layout(const sdq_layout* L) {
       L->bits != (L->levels == 2 ? 1 : 2) ||
       L->codes_per_chunk != kChunkBytes * 8 / L->bits ||
       L->n_chunks != (L->k_up + L->codes_per_chunk - 1) / L->codes_per_chunk ||
-      L->n_pad != (L->n + kPanel - 1) / kPanel * kPanel)
+      L->n_pad != (L->n + kPanel - 1) / kPanel * kPanel || !valid_hadamard(L))
     return set_error(SDQ_ERR_ARG, "layout is not one produced by sdq_layout_init");
   return SDQ_OK;
 }
@@ -249,7 +280,26 @@ sdq_status sdq_layout_init(sdq_layout* out, int64_t n, int64_t k, double osr, in
   L.n_pad = (n + kPanel - 1) / kPanel * kPanel;
   L.codes_per_chunk = kChunkBytes * 8 / L.bits;
   L.n_chunks = (L.k_up + L.codes_per_chunk - 1) / L.codes_per_chunk;
+  L.hadamard = SDQ_HAD_SYLVESTER;
   *out = L;
+  return SDQ_OK;
+}
+
+sdq_status sdq_layout_set_hadamard(sdq_layout* L, int32_t mode, const int8_t* signs) {
+  if (!L) return set_error(SDQ_ERR_ARG, "layout is NULL");
+  if (mode != SDQ_HAD_NONE && mode != SDQ_HAD_SYLVESTER && mode != SDQ_HAD_SIGNED)
+    return set_error(SDQ_ERR_ARG, "hadamard mode %d is not SDQ_HAD_NONE, _SYLVESTER or _SIGNED", mode);
+  if (!valid_block(L->block)) return set_error(SDQ_ERR_ARG, "layout is not one produced by sdq_layout_init");
+  uint32_t words[8] = {0, 0, 0, 0, 0, 0, 0, 0};
+  if (mode == SDQ_HAD_SIGNED) {
+    if (!signs) return set_error(SDQ_ERR_ARG, "the signed Hadamard needs %d signs", L->block);
+    for (int t = 0; t < L->block; ++t) {
+      if (signs[t] != 1 && signs[t] != -1) return set_error(SDQ_ERR_ARG, "sign %d is %d, not +-1", t, signs[t]);
+      if (signs[t] < 0) words[t / 32] |= 1u << (t % 32);
+    }
+  }
+  L->hadamard = mode;
+  std::copy(words, words + 8, L->had_signs);
   return SDQ_OK;
 }
 
@@ -279,7 +329,7 @@ sdq_status sdq_quantize(const float* w, const sdq_layout* L, void* codes, float*
     return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   if (L->n == 0) return SDQ_OK;
   const Tables* T = nullptr;
-  st = get_tables(L->block, L->m_up, &T);
+  st = get_tables(L, &T);
   if (st != SDQ_OK) return st;
   QuantWs qw;
   quant_ws_layout(L, &qw, ws);
@@ -323,7 +373,7 @@ static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_
   if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
   if (!x) return set_error(SDQ_ERR_ARG, "x is NULL");
   const Tables* T = nullptr;
-  sdq_status st = get_tables(L->block, L->m_up, &T);
+  sdq_status st = get_tables(L, &T);
   if (st != SDQ_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   return m <= 16 ? launch_decode_expand(x, xt, m, L, T, ws, y_zero, s)
@@ -518,7 +568,14 @@ sdq_status sdq_prepare(int32_t block, int32_t m_up) {
   if (!valid_block(block)) return set_error(SDQ_ERR_SHAPE, "block must be 64, 128 or 256");
   if (m_up < block || m_up % 32 || m_up > 8 * block) return set_error(SDQ_ERR_OSR, "bad M=%d", m_up);
   const Tables* T = nullptr;
-  return get_tables(block, m_up, &T);
+  return get_tables_for(block, m_up, SDQ_HAD_SYLVESTER, SignWords{}, &T);
+}
+
+sdq_status sdq_prepare_layout(const sdq_layout* L) {
+  sdq_status st = check_layout(L);
+  if (st != SDQ_OK) return st;
+  const Tables* T = nullptr;
+  return get_tables(L, &T);
 }
 
 void sdq_release_tables(void) {

@@ -13,17 +13,19 @@ namespace sdq {
 constexpr int kPanel = 64;        // rows per panel of the packed format
 constexpr int kChunkBytes = 16;   // bytes per chunk of the packed format
 
-// Device coefficient tables for one (block, M) pair on one device.
+// Device coefficient tables for one (block, M, Had) choice on one device.
 struct Tables {
   int block = 0;
   int m_up = 0;
+  int hadamard = SDQ_HAD_SYLVESTER;   // Had (sdq_hadamard) folded into E
+  uint32_t signs[8] = {};              // SDQ_HAD_SIGNED: bit t set <=> s_t = -1
   int g0 = 0;          // gcd(B, M): number of samples whose kernel is a unit impulse
   int phases = 0;      // P = M / g0: samples m with m % P == 0 copy v[(m / P) * (B / g0)]
   int m_nz = 0;        // M - g0 samples per block computed as dense sums
   int m_nz_pad = 0;    // m_nz rounded up to the upsample tile width
   float* unz = nullptr;   // [B][m_nz_pad] fp32 coefficients g(p(t, m_j)), zero padded
   // E = Had D^T (B x M) with D the decimation (Resample back to B), so that
-  // x_tilde_b = x_b E.  Two copies:
+  // x_tilde_b = x_b E (Had = H_B / sqrt(B), diag(s) H_B / sqrt(B) or I).  Two copies:
   //   edec   fp32, groups of four t: edec[((t / 4) * m_pad + m) * 4 + t % 4] =
   //          E[t][m], columns m_up .. m_pad-1 zero (m_pad = M rounded up to 64);
   //   et_hi, et_lo  transposed [M][B] as an fp16 pair hi + lo with
@@ -35,8 +37,9 @@ struct Tables {
   uint16_t* et_lo = nullptr;
 };
 
-// Returns the cached tables for the current device (creating them on first use).
-sdq_status get_tables(int block, int m_up, const Tables** out);
+// Returns the cached tables of the layout's (block, M, Had) for the current
+// device (creating them on first use).
+sdq_status get_tables(const sdq_layout* L, const Tables** out);
 
 // Host fp64 coefficient helpers (also back the parity entry points).
 double upsample_kernel(int64_t p, int block, int m_up);          // g(p)

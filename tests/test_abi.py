@@ -34,7 +34,46 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_layout_struct_size_matches_header():
-    assert ctypes.sizeof(Bd.sdq_layout) == 72
+    assert ctypes.sizeof(Bd.sdq_layout) == 104
+    assert Bd.sdq_layout.hadamard.offset == 68 and Bd.sdq_layout.had_signs.offset == 72
+
+
+def test_layout_hadamard_choice():
+    import synth
+    L = P.sdq_layout_init(8, 512, 2.0, 3, 256)
+    assert L.hadamard == P.SDQ_HAD_SYLVESTER and list(L.had_signs) == [0] * 8
+    s = synth.hadamard_signs(1, 256)
+    P.sdq_layout_set_hadamard(L, P.SDQ_HAD_SIGNED, s)
+    bits = np.array([(L.had_signs[t // 32] >> (t % 32)) & 1 for t in range(256)])
+    assert np.array_equal(bits == 1, s < 0)
+    P.sdq_layout_set_hadamard(L, P.SDQ_HAD_NONE)
+    assert L.hadamard == P.SDQ_HAD_NONE and list(L.had_signs) == [0] * 8
+    Ls = P.sdq_layout_init(8, 128, 2.0, 3, 64)
+    P.sdq_layout_set_hadamard(Ls, P.SDQ_HAD_SIGNED, -np.ones(64, np.int8))
+    assert list(Ls.had_signs) == [0xFFFFFFFF, 0xFFFFFFFF] + [0] * 6
+
+
+@pytest.mark.parametrize("mode,signs", [(3, None), (-1, None), (2, None),
+                                        (2, np.zeros(256, np.int8)), (2, np.full(256, 2, np.int8))])
+def test_layout_hadamard_rejects(mode, signs):
+    L = P.sdq_layout_init(8, 512, 2.0, 3, 256)
+    with pytest.raises(P.SdqError) as ei:
+        P.sdq_layout_set_hadamard(L, mode, signs)
+    assert ei.value.status == -1
+    assert L.hadamard == P.SDQ_HAD_SYLVESTER
+
+
+def test_tampered_hadamard_fields_are_rejected_before_gpu_work():
+    L = P.sdq_layout_init(8, 128, 2.0, 3, 64)
+    L.had_signs[0] = 1                       # sign bits without the signed Had
+    assert P.lib().sdq_quantize_workspace_bytes(ctypes.byref(L)) == 0
+    L2 = P.sdq_layout_init(8, 128, 2.0, 3, 64)
+    P.sdq_layout_set_hadamard(L2, P.SDQ_HAD_SIGNED, np.ones(64, np.int8))
+    L2.had_signs[2] = 1                      # a sign beyond the block of 64
+    assert P.lib().sdq_quantize_workspace_bytes(ctypes.byref(L2)) == 0
+    L3 = P.sdq_layout_init(8, 128, 2.0, 3, 64)
+    L3.hadamard = 5
+    assert P.lib().sdq_linear_workspace_bytes(ctypes.byref(L3), 1) == 0
 
 
 @pytest.mark.parametrize("n,k,osr,levels,block,m_up,cpc", [
