@@ -17,8 +17,11 @@ streams its codes from HBM.  The line also carries:
 * phases    -- the encoder on the same weight (rows/s, fp32 VALU roofline), the
                prefill path on the LLaMA-70B 8192x8192 linear at m = 2048 with
                bf16 activations (TFLOP/s, fp16 MFMA roofline), MultiOSR on
-               the LLaMA-7B layer's seven linears, and the 80-layer LLaMA-70B
-               stack (560 linears quantised, one token through all of them);
+               the LLaMA-7B layer's seven linears, the 80-layer LLaMA-70B
+               stack (560 linears quantised, one token through all of them),
+               and the continuous-precision sweep (output error and weight SNR
+               against OSR 1..4 for each Hadamard choice, and MultiOSR against
+               a uniform OSR);
 * cpu_baseline -- the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -317,6 +320,98 @@ def bench_stack(torch, P, synth, SG, replays: int = 3):
     return res
 
 
+SWEEP_OSRS = tuple(1.0 + 0.25 * i for i in range(13))      # 1.0 .. 4.0
+
+
+def precision_sweep(torch, P, synth, SG, n: int = 4096, k: int = 4096, m: int = 64,
+                    osrs=SWEEP_OSRS, hads=(1, 2, 0), levels_list=(3, 2), seed: int = 2516):
+    """Continuous precision and the Hadamard ablation on one synthetic layer
+    (LLaMA-7B q_proj shape, N(0, 0.02^2) weights with x10 outliers): for every
+    (levels, Had, OSR) the codes' bits per weight, the layer-output error
+    ||y - x W^T|| / ||x W^T|| on m fp16 activation rows (y from sdq_linear,
+    x W^T in fp64 on the host), and the weight reconstruction SNR
+    10 log10(||W||^2 / ||W - W_hat||^2) with W_hat^T = sdq_linear of the
+    identity.  Hads: 1 Sylvester, 2 sign-randomised, 0 none."""
+    import numpy as np
+    w = SG.weight_rows_gpu(seed, 0, n, k, 0.02, True)
+    x = SG.activations_gpu(seed, 7, m, k).to(torch.float16)
+    y_ref = x.double().cpu().numpy() @ w.double().cpu().numpy().T
+    ref_norm = float(np.linalg.norm(y_ref))
+    w_sq = float(torch.sum(w.double() ** 2).item())
+    eye = torch.eye(k, dtype=torch.float16, device="cuda")
+    signs = synth.hadamard_signs(seed, 256)
+    rows = []
+    for levels in levels_list:
+        for had in hads:
+            for osr in osrs:
+                enc = P.quantize(w, osr, levels, hadamard=had, signs=signs if had == 2 else None)
+                y = P.linear(x, enc).double().cpu().numpy()
+                w_hat_t = P.linear(eye, enc)                     # (k, n) = W_hat^T
+                err_sq = float(torch.sum((w_hat_t.t().double() - w.double()) ** 2).item())
+                rows.append({"levels": levels, "had": had, "osr": osr,
+                             "bits_per_weight": (1 if levels == 2 else 2) * enc.layout.m_up / enc.layout.block,
+                             "out_rel_err": float(np.linalg.norm(y - y_ref)) / ref_norm,
+                             "weight_snr_db": 10.0 * math.log10(w_sq / err_sq)})
+                del enc, w_hat_t
+    del w, x, eye
+    torch.cuda.empty_cache()
+    return rows
+
+
+def multiosr_ablation(torch, P, synth, SG, targets=(1.5, 2.0, 2.5, 3.0), lo: float = 1.0,
+                      hi: float = 4.0, m: int = 16):
+    """MultiOSR against one uniform OSR at the same parameter-weighted mean, on
+    the seven LLaMA-7B linears of one layer (per-linear variances log-uniform in
+    [1e-4, 1e-3], ternary): the parameter-weighted mean and the largest
+    per-linear output error ||y - x W^T|| / ||x W^T||."""
+    import numpy as np
+    wl = synth.workload(3)
+    out = torch.zeros(2, dtype=torch.float64, device="cuda")
+    var, refs = [], []
+    for lin in wl.linears:
+        w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+        ws = torch.empty(P.sdq_moments_workspace_bytes(w.numel()), dtype=torch.uint8, device="cuda")
+        P.sdq_weight_moments(w, out, ws)
+        var.append(float(out[1].item()))
+        x = SG.activations_gpu(wl.seed, 40 + lin.linear_id, m, lin.k).to(torch.float16)
+        refs.append((x, x.double().cpu().numpy() @ w.double().cpu().numpy().T))
+        del w, ws
+    nparams = np.array([lin.n * lin.k for lin in wl.linears], dtype=np.float64)
+    res = []
+    for target in targets:
+        alloc = {"uniform": [target] * len(wl.linears),
+                 "multiosr": [float(o) for o in P.sdq_multiosr(var, nparams.astype(np.int64),
+                                                               [lin.layer for lin in wl.linears],
+                                                               target, lo, hi)]}
+        entry = {"target_mean_osr": target}
+        for name, osrs in alloc.items():
+            errs = []
+            for lin, o, (x, y_ref) in zip(wl.linears, osrs, refs):
+                w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+                enc = P.quantize(w, o, wl.levels)
+                y = P.linear(x, enc).double().cpu().numpy()
+                errs.append(float(np.linalg.norm(y - y_ref) / np.linalg.norm(y_ref)))
+                del w, enc
+            entry[name] = {"osr": osrs, "mean_osr": float(np.dot(osrs, nparams) / nparams.sum()),
+                           "weighted_mean_out_rel_err": float(np.dot(errs, nparams) / nparams.sum()),
+                           "max_out_rel_err": max(errs)}
+        res.append(entry)
+    del refs
+    torch.cuda.empty_cache()
+    return {"workload": "llama7b_layer_7_linears_ternary", "lo": lo, "hi": hi, "m": m, "rows": res}
+
+
+def bench_sweep(torch, P, synth, SG):
+    t0 = time.perf_counter()
+    rows = precision_sweep(torch, P, synth, SG)
+    t1 = time.perf_counter()
+    abl = multiosr_ablation(torch, P, synth, SG)
+    t2 = time.perf_counter()
+    return {"workload": "llama7b_q_proj_4096x4096_outliers_sweep_osr1to4", "rows": rows,
+            "configs_per_s": len(rows) / (t1 - t0), "sweep_s": t1 - t0,
+            "multiosr_ablation": abl, "ablation_s": t2 - t1}
+
+
 def cpu_baseline(synth, dec, budget_s: float = 12.0):
     """The oracle on host cores: encode a sample of rows, then its fp64 linear."""
     import numpy as np
@@ -464,6 +559,10 @@ def main() -> int:
             line["phases"]["stack_70b"] = bench_stack(torch, P, synth, SG)
         except Exception as exc:  # noqa: BLE001 -- report, keep the headline line
             line["phases"]["stack_70b"] = {"error": repr(exc)}
+        try:
+            line["phases"]["precision_sweep"] = bench_sweep(torch, P, synth, SG)
+        except Exception as exc:  # noqa: BLE001
+            line["phases"]["precision_sweep"] = {"error": repr(exc)}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(synth, dec)
     line["wall_s"] = time.perf_counter() - t_start
