@@ -24,13 +24,15 @@ Contents (each function cites the passage it follows):
                      re-implemented independently, and Eq. 14's ratio;
 * ``multiosr``    -- the per-linear OSR allocation of Section 3.4 (reading
                      documented in the module; parity of its exact rule is
-                     unpinned by the paper).
+                     unpinned by the paper);
+* ``compensation``-- the block compensation of Algorithm 1 (Hessian, the
+                     Cholesky factor of its inverse, the block loop).
 
 Precision: the encoder runs in fp32 with every multiply and add rounded
 separately (no fused multiply-add), so its codes are a bit-exact target; the
 linear and everything else run in fp64.
 """
-from . import hadamard, resample, sigma_delta, encoder, linear, layout, multiosr  # noqa: F401
+from . import hadamard, resample, sigma_delta, encoder, linear, layout, multiosr, compensation  # noqa: F401
 from .encoder import encode, EncodeResult  # noqa: F401
 from .linear import linear_fp64, reconstruct_fp64, expand_activations_fp64  # noqa: F401
 from .multiosr import variance_fp64  # noqa: F401
