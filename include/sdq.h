@@ -43,7 +43,8 @@ typedef enum {
   SDQ_ERR_WORKSPACE = -6,  /* workspace pointer missing or too small             */
   SDQ_ERR_HIP = -7,        /* a HIP runtime call failed                          */
   SDQ_ERR_NOMEM = -8,      /* the coefficient-table cache could not allocate     */
-  SDQ_ERR_UNSUPPORTED = -9 /* a valid request this build does not implement      */
+  SDQ_ERR_UNSUPPORTED = -9, /* a valid request this build does not implement     */
+  SDQ_ERR_NOT_SPD = -10    /* a Hessian (plus damping) is not positive definite  */
 } sdq_status;
 
 typedef enum { SDQ_F16 = 0, SDQ_BF16 = 1, SDQ_F32 = 2 } sdq_dtype;
@@ -153,6 +154,47 @@ sdq_status sdq_quantize(const float* w_dev, const sdq_layout* layout, void* code
  * that used this workspace: SDQ_OK, or SDQ_ERR_NONFINITE when a weight or an
  * upsampled sample was NaN / Inf (the codes of such rows are meaningless). */
 sdq_status sdq_quantize_check(const void* workspace_dev, void* stream);
+
+/*
+ * Block compensation of Algorithm 1 (lines 3-8; GPTQ-style).  All in fp64.
+ *
+ * sdq_hessian_accumulate: H += 2 X^T X (the Hessian of Algorithm 1's caption
+ * without its damping), for calibration activations x_dev (fp32 [m x k],
+ * row-major) and h_dev (fp64 [k x k], row-major, both triangles written;
+ * zero it before the first call).  Errors: SDQ_ERR_ARG.
+ *
+ * sdq_hessian_factor: Algorithm 1 line 4, u_dev = Cholesky((H + lambda I)^-1)^T,
+ * the upper factor U with U^T U = (H + lambda I)^-1 (fp64 [k x k], lower part
+ * zero), computed without forming the inverse (a blocked Cholesky of the
+ * index-reversed matrix and a blocked triangular inverse).  h_dev: symmetric
+ * fp64 [k x k]; k a multiple of 64; lambda >= 0 absolute (GPTQ takes 1 % of the
+ * mean diagonal).  workspace: sdq_hessian_factor_workspace_bytes(k) bytes
+ * (about 16 k^2).  A non-positive pivot does not fail the call; it is reported
+ * by sdq_hessian_check(workspace) as SDQ_ERR_NOT_SPD.
+ * Errors: SDQ_ERR_SHAPE, SDQ_ERR_ARG, SDQ_ERR_WORKSPACE.
+ *
+ * sdq_quantize_compensated: as sdq_quantize, with the block compensation:
+ * the row scales are those of the plain encoding of W; W is then walked in
+ * blocks of B columns in fp64, each block rounded to fp32 and encoded with
+ * those scales, and the columns after it corrected by
+ * W_F -= E U_QQ^-1 U_QF, where E = W_Q - Q_hat is the block's error against
+ * its reconstruction (Resample back to B, Had^T) and U_QQ, U_QF are blocks of
+ * u_dev (the printed W_F -= E U_QF of Algorithm 1 omits the U_QQ^-1 that
+ * GPTQ's block mechanism carries).  u_dev: fp64 [k x k] upper factor as from
+ * sdq_hessian_factor.  workspace: sdq_quantize_compensated_workspace_bytes
+ * (the plain encoder's plus about 8 n (k + 2B + M) + 24 nb B^2 bytes).
+ * Codes and scales as sdq_quantize; the non-finite flag is reported by
+ * sdq_quantize_check on the same workspace.  Errors as sdq_quantize.
+ */
+sdq_status sdq_hessian_accumulate(const float* x_dev, int64_t m, int64_t k, double* h_dev, void* stream);
+size_t sdq_hessian_factor_workspace_bytes(int64_t k);
+sdq_status sdq_hessian_factor(const double* h_dev, int64_t k, double lambda, double* u_dev,
+                              void* workspace_dev, size_t workspace_bytes, void* stream);
+sdq_status sdq_hessian_check(const void* workspace_dev, void* stream);
+size_t sdq_quantize_compensated_workspace_bytes(const sdq_layout* layout);
+sdq_status sdq_quantize_compensated(const float* w_dev, const sdq_layout* layout, const double* u_dev,
+                                    void* codes_dev, float* scales_dev, void* workspace_dev,
+                                    size_t workspace_bytes, void* stream);
 
 /* Device workspace (bytes) sdq_linear needs for m activation rows: the
  * expanded activations, at offset 0 --

@@ -55,7 +55,7 @@ def inverse_cholesky_upper(h: np.ndarray, lam: float) -> np.ndarray:
     h = np.asarray(h, dtype=np.float64)
     hinv = np.linalg.inv(h + lam * np.eye(h.shape[0]))
     hinv = 0.5 * (hinv + hinv.T)
-    return np.linalg.cholesky(hinv).T
+    return np.ascontiguousarray(np.linalg.cholesky(hinv).T)
 
 
 def encode_block_with_scale(wb: np.ndarray, osr: float, levels: int, block: int, s: np.ndarray,

@@ -24,7 +24,7 @@ SDQ_HAD_NONE, SDQ_HAD_SYLVESTER, SDQ_HAD_SIGNED = 0, 1, 2
 STATUS_NAMES = {
     0: "SDQ_OK", -1: "SDQ_ERR_ARG", -2: "SDQ_ERR_SHAPE", -3: "SDQ_ERR_OSR", -4: "SDQ_ERR_LEVELS",
     -5: "SDQ_ERR_NONFINITE", -6: "SDQ_ERR_WORKSPACE", -7: "SDQ_ERR_HIP", -8: "SDQ_ERR_NOMEM",
-    -9: "SDQ_ERR_UNSUPPORTED",
+    -9: "SDQ_ERR_UNSUPPORTED", -10: "SDQ_ERR_NOT_SPD",
 }
 
 
@@ -86,6 +86,12 @@ def _load() -> ctypes.CDLL:
                                                   ctypes.c_size_t, P]),
         "sdq_linear_expanded": (ctypes.c_int, [ctypes.c_int64, P, P, L, P, ctypes.c_int32, P,
                                                ctypes.c_size_t, P]),
+        "sdq_hessian_accumulate": (ctypes.c_int, [P, ctypes.c_int64, ctypes.c_int64, P, P]),
+        "sdq_hessian_factor_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
+        "sdq_hessian_factor": (ctypes.c_int, [P, ctypes.c_int64, ctypes.c_double, P, P, ctypes.c_size_t, P]),
+        "sdq_hessian_check": (ctypes.c_int, [P, P]),
+        "sdq_quantize_compensated_workspace_bytes": (ctypes.c_size_t, [L]),
+        "sdq_quantize_compensated": (ctypes.c_int, [P, L, P, P, P, P, ctypes.c_size_t, P]),
         "sdq_multiosr": (ctypes.c_int, [P, P, P, ctypes.c_int64, ctypes.c_double, ctypes.c_double,
                                         ctypes.c_double, ctypes.c_double, P]),
         "sdq_moments_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
@@ -204,6 +210,37 @@ def sdq_linear_expanded(m: int, codes, scales, layout: sdq_layout, y, workspace,
                                     _stream(stream)))
 
 
+def _nbytes(t) -> int:
+    return 0 if t is None else t.numel() * t.element_size()
+
+
+def sdq_hessian_accumulate(x, h, stream=None) -> None:
+    """h += 2 x^T x (x fp32 [m, k] device, h fp64 [k, k] device)."""
+    _check(_lib.sdq_hessian_accumulate(_ptr(x), x.shape[0], x.shape[1], _ptr(h), _stream(stream)))
+
+
+def sdq_hessian_factor_workspace_bytes(k: int) -> int:
+    return int(_lib.sdq_hessian_factor_workspace_bytes(k))
+
+
+def sdq_hessian_factor(h, lam: float, u, workspace, stream=None) -> None:
+    _check(_lib.sdq_hessian_factor(_ptr(h), h.shape[0], float(lam), _ptr(u), _ptr(workspace),
+                                   _nbytes(workspace), _stream(stream)))
+
+
+def sdq_hessian_check(workspace, stream=None) -> None:
+    _check(_lib.sdq_hessian_check(_ptr(workspace), _stream(stream)))
+
+
+def sdq_quantize_compensated_workspace_bytes(layout: sdq_layout) -> int:
+    return int(_lib.sdq_quantize_compensated_workspace_bytes(ctypes.byref(layout)))
+
+
+def sdq_quantize_compensated(w, layout: sdq_layout, u, codes, scales, workspace, stream=None) -> None:
+    _check(_lib.sdq_quantize_compensated(_ptr(w), ctypes.byref(layout), _ptr(u), _ptr(codes), _ptr(scales),
+                                         _ptr(workspace), _nbytes(workspace), _stream(stream)))
+
+
 def sdq_multiosr(var: Sequence[float], nparams: Sequence[int], layer_id: Sequence[int],
                  target: float, lo: float, hi: float, grid: float = 0.125) -> np.ndarray:
     var_a = np.ascontiguousarray(var, dtype=np.float64)
@@ -285,6 +322,37 @@ def quantize(w, osr: float, levels: int, block: int = 256, workspace=None, check
     sdq_quantize(w, layout, codes, scales, workspace, stream)
     if check:
         sdq_quantize_check(workspace, stream)
+    return Encoded(layout, codes, scales)
+
+
+def hessian_factor(h, lam: float, check: bool = True, stream=None):
+    """U = Cholesky((H + lam I)^-1)^T for a device fp64 [k, k] H; returns U (fp64, device)."""
+    import torch
+    u = torch.empty_like(h)
+    ws = torch.empty(sdq_hessian_factor_workspace_bytes(h.shape[0]), dtype=torch.uint8, device=h.device)
+    sdq_hessian_factor(h, lam, u, ws, stream)
+    if check:
+        sdq_hessian_check(ws, stream)
+    return u
+
+
+def quantize_compensated(w, osr: float, levels: int, u, block: int = 256, check: bool = True,
+                         stream=None, hadamard: int = SDQ_HAD_SYLVESTER, signs=None) -> Encoded:
+    """Encode a device fp32 weight [n, k] with Algorithm 1's block compensation (u: fp64 [k, k])."""
+    import torch
+    if w.dtype != torch.float32 or not w.is_cuda or not w.is_contiguous():
+        raise ValueError("w must be a contiguous fp32 device tensor")
+    if u.dtype != torch.float64 or tuple(u.shape) != (w.shape[1], w.shape[1]) or not u.is_contiguous():
+        raise ValueError("u must be a contiguous fp64 device tensor [k, k]")
+    layout = sdq_layout_init(w.shape[0], w.shape[1], osr, levels, block)
+    if hadamard != SDQ_HAD_SYLVESTER:
+        sdq_layout_set_hadamard(layout, hadamard, signs)
+    codes = torch.empty(sdq_codes_bytes(layout), dtype=torch.uint8, device=w.device)
+    scales = torch.empty(layout.n, dtype=torch.float32, device=w.device)
+    ws = torch.empty(sdq_quantize_compensated_workspace_bytes(layout), dtype=torch.uint8, device=w.device)
+    sdq_quantize_compensated(w, layout, u, codes, scales, ws, stream)
+    if check:
+        sdq_quantize_check(ws, stream)
     return Encoded(layout, codes, scales)
 
 

@@ -20,7 +20,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdq.so")
 ARCH = os.environ.get("SDQ_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["sdq_api.cpp", "encoder.hip", "linear_decode.hip", "linear_prefill.hip", "moments.hip"]
+SOURCES = ["sdq_api.cpp", "encoder.hip", "linear_decode.hip", "linear_prefill.hip", "moments.hip",
+           "compensation.hip"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

@@ -1,0 +1,401 @@
+// Block compensation of Algorithm 1 (lines 3-8), fp64 on the device.
+//
+//   hessian  H += 2 X^T X for calibration activations X (m x K).
+//   factor   U = Cholesky((H + lambda I)^-1)^T (line 4), upper, U^T U = (H + lambda I)^-1.
+//            Computed without forming the inverse: with J the index reversal,
+//            J (H + lambda I) J = L L^T (blocked Cholesky, 64-column panels)
+//            and U = J L^-1 J (blocked triangular inverse), because
+//            (J L^-1 J)^T (J L^-1 J) = J (L L^T)^-1 J = (H + lambda I)^-1.
+//   encode   the weight's row scales come from the uncompensated W (the plain
+//            encoder); W is then carried in fp64 and walked in blocks of B
+//            columns: block b is rounded to fp32 and encoded with those
+//            scales (the same rotate / upsample / scan kernels), its
+//            reconstruction Q_b = (s * C_b) E^T (E = Had D^T, the table of the
+//            activation expansion, in fp64) gives the error E_b = W_b - Q_b, and
+//            the later columns take the optimal-brain-surgeon correction of the
+//            jointly quantized block, W_F -= E_b U_QQ^-1 U_QF.
+//
+// All of it is dense fp64 linear algebra: one register-tiled VALU GEMM with
+// general strides (64 x 64 tile per workgroup, 4 x 4 outputs per thread,
+// 16-deep k steps through LDS) serves the Hessian, the panel solves, the
+// trailing updates, the triangular inverses and the block corrections; a
+// 64 x 64 Cholesky-and-inverse kernel works on diagonal blocks in LDS.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+
+#include "sdq_internal.h"
+
+namespace sdq {
+namespace {
+
+constexpr int kT = 64;     // factorisation panel / GEMM tile
+constexpr int kTK = 16;    // GEMM k step
+
+// C = beta C + alpha A B; element (i, p) of A at A[i * rsa + p * csa], likewise
+// B and C; blockIdx.z selects a batch (strides bsa, bsb, bsc).  lower_only skips
+// tiles strictly above the diagonal of C.  beta == 0 never reads C.  A and B
+// may overlap C only where every output tile depends on the same rows of A
+// alone (an in-place panel solve with N <= 64).
+template <typename TA, typename TB>
+__global__ __launch_bounds__(256) void gemm64_kernel(
+    int64_t M, int64_t N, int64_t K, double alpha, const TA* A, int64_t rsa, int64_t csa,
+    int64_t bsa, const TB* B, int64_t rsb, int64_t csb, int64_t bsb, double beta, double* C,
+    int64_t rsc, int64_t csc, int64_t bsc, int lower_only) {
+  __shared__ double As[kTK][kT + 2];
+  __shared__ double Bs[kTK][kT + 2];
+  const int tid = threadIdx.x;
+  const int tx = tid % 16, ty = tid / 16;
+  const int64_t i0 = static_cast<int64_t>(blockIdx.y) * kT;
+  const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kT;
+  if (lower_only && i0 + kT - 1 < j0) return;
+  A += static_cast<int64_t>(blockIdx.z) * bsa;
+  B += static_cast<int64_t>(blockIdx.z) * bsb;
+  C += static_cast<int64_t>(blockIdx.z) * bsc;
+  double acc[4][4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
+  const bool a_pfast = csa == 1;     // consecutive threads along the contiguous index
+  const bool b_jfast = csb == 1;
+  for (int64_t p0 = 0; p0 < K; p0 += kTK) {
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + 256 * q;
+      const int ii = a_pfast ? e / kTK : e % kT;
+      const int pp = a_pfast ? e % kTK : e / kT;
+      const int64_t gi = i0 + ii, gp = p0 + pp;
+      As[pp][ii] = gi < M && gp < K ? static_cast<double>(A[gi * rsa + gp * csa]) : 0.0;
+    }
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      const int e = tid + 256 * q;
+      const int jj = b_jfast ? e % kT : e / kTK;
+      const int pp = b_jfast ? e / kT : e % kTK;
+      const int64_t gj = j0 + jj, gp = p0 + pp;
+      Bs[pp][jj] = gj < N && gp < K ? static_cast<double>(B[gp * rsb + gj * csb]) : 0.0;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int pp = 0; pp < kTK; ++pp) {
+      double a[4], b[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        a[u] = As[pp][ty * 4 + u];
+        b[u] = Bs[pp][tx * 4 + u];
+      }
+#pragma unroll
+      for (int u = 0; u < 4; ++u)
+#pragma unroll
+        for (int v = 0; v < 4; ++v) acc[u][v] = __builtin_fma(a[u], b[v], acc[u][v]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int u = 0; u < 4; ++u)
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int64_t gi = i0 + ty * 4 + u, gj = j0 + tx * 4 + v;
+      if (gi < M && gj < N) {
+        double* c = C + gi * rsc + gj * csc;
+        double val = alpha * acc[u][v];
+        if (beta != 0.0) val += beta * *c;
+        *c = val;
+      }
+    }
+}
+
+// One 64 x 64 diagonal block per workgroup (grid x: blocks along a diagonal,
+// stride sa1 / sx1; grid y: batches, stride sa2 / sx2).  factor = 1: Cholesky
+// of the block's lower part in place (A = L L^T, the upper part zeroed); a
+// pivot that is not positive sets *info and is replaced by 1.  Then X = L^-1
+// (lower) by forward substitution, one column per thread.
+__global__ __launch_bounds__(256) void potrf64_kernel(double* A, int64_t lda, int64_t sa1,
+                                                      int64_t sa2, double* X, int64_t ldx,
+                                                      int64_t sx1, int64_t sx2, int factor,
+                                                      int* info) {
+  __shared__ double a[kT][kT + 1];
+  __shared__ double x[kT][kT + 1];
+  A += blockIdx.x * sa1 + blockIdx.y * sa2;
+  X += blockIdx.x * sx1 + blockIdx.y * sx2;
+  const int tid = threadIdx.x;
+  for (int e = tid; e < kT * kT; e += 256) {
+    const int i = e / kT, k = e % kT;
+    a[i][k] = k <= i ? A[i * lda + k] : 0.0;
+  }
+  __syncthreads();
+  if (factor) {
+    for (int j = 0; j < kT; ++j) {
+      if (tid == 0) {
+        double d = a[j][j];
+        if (!(d > 0.0)) {
+          info[0] = 1;
+          d = 1.0;
+        }
+        a[j][j] = sqrt(d);
+      }
+      __syncthreads();
+      if (tid > j && tid < kT) a[tid][j] /= a[j][j];
+      __syncthreads();
+      for (int e = tid; e < kT * kT; e += 256) {
+        const int i = e / kT, k = e % kT;
+        if (k > j && i >= k) a[i][k] -= a[i][j] * a[k][j];
+      }
+      __syncthreads();
+    }
+    for (int e = tid; e < kT * kT; e += 256) {
+      const int i = e / kT, k = e % kT;
+      A[i * lda + k] = k <= i ? a[i][k] : 0.0;
+    }
+  }
+  if (tid < kT) {
+    const int c = tid;
+    for (int i = 0; i < kT; ++i) {
+      double s = i == c ? 1.0 : 0.0;
+      for (int k = c; k < i; ++k) s -= a[i][k] * x[k][c];
+      x[i][c] = i < c ? 0.0 : s / a[i][i];
+    }
+  }
+  __syncthreads();
+  for (int e = tid; e < kT * kT; e += 256) {
+    const int i = e / kT, k = e % kT;
+    X[i * ldx + k] = x[i][k];
+  }
+}
+
+// dst[i][j] = src[n-1-i][n-1-j] (+ lam on the diagonal) where kept (i >= j
+// for keep_lower, else j >= i), 0 elsewhere; grid y selects a batch.
+__global__ void reverse_tri_kernel(const double* __restrict__ src, int64_t lds, int64_t ss,
+                                   int64_t n, double* __restrict__ dst, int64_t ldd, int64_t sd,
+                                   int keep_lower, double lam) {
+  src += blockIdx.y * ss;
+  dst += blockIdx.y * sd;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < n * n;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t i = e / n, j = e % n;
+    const bool keep = keep_lower ? i >= j : j >= i;
+    dst[i * ldd + j] = keep ? src[(n - 1 - i) * lds + (n - 1 - j)] + (i == j ? lam : 0.0) : 0.0;
+  }
+}
+
+__global__ void fill_f64_kernel(double* __restrict__ p, int64_t count, double v) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    p[i] = v;
+}
+
+__global__ void clear_info_kernel(int* info) { if (threadIdx.x == 0) info[0] = 0; }
+
+__global__ void widen_kernel(const float* __restrict__ w, int64_t count, double* __restrict__ w64) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < count;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x)
+    w64[i] = static_cast<double>(w[i]);
+}
+
+// Block column col0 .. col0 + B - 1 of W64 (n x k): rounded to fp32 into wblk
+// (n x B, the encoder's input) and copied into ebuf (n x B, fp64).
+__global__ void extract_block_kernel(const double* __restrict__ w64, int64_t n, int64_t k, int B,
+                                     int64_t col0, float* __restrict__ wblk, double* __restrict__ ebuf) {
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < n * B;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t r = e / B, t = e % B;
+    const double v = w64[r * k + col0 + t];
+    wblk[e] = static_cast<float>(v);
+    ebuf[e] = v;
+  }
+}
+
+// cb[r][m] = s_r * code(r, j0 + m) (n x M, fp64) from the packed format.
+__global__ void unpack_scaled_kernel(const uint32_t* __restrict__ codes, const float* __restrict__ scales,
+                                     int64_t n, int64_t n_chunks, int cpc, int bits, int64_t j0,
+                                     int m_up, double* __restrict__ cb) {
+  const int per_word = 32 / bits;
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < n * m_up;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t r = e / m_up;
+    const int64_t j = j0 + e % m_up;
+    const int64_t c = j / cpc;
+    const int q = static_cast<int>(j % cpc);
+    const uint32_t word = codes[(((r / kPanel) * n_chunks + c) * kPanel + r % kPanel) * 4 + q / per_word];
+    const uint32_t f = (word >> (bits * (q % per_word))) & ((1u << bits) - 1u);
+    const double code = bits == 1 ? (f ? 1.0 : -1.0) : (f == 1u ? 1.0 : (f == 3u ? -1.0 : 0.0));
+    cb[e] = static_cast<double>(scales[r]) * code;
+  }
+}
+
+unsigned grid1(int64_t count) {
+  return static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 8192));
+}
+
+template <typename TA, typename TB>
+void gemm64(int64_t M, int64_t N, int64_t K, double alpha, const TA* A, int64_t rsa, int64_t csa,
+            const TB* B, int64_t rsb, int64_t csb, double beta, double* C, int64_t rsc, int64_t csc,
+            hipStream_t stream, int lower_only = 0, int batch = 1, int64_t bsa = 0, int64_t bsb = 0,
+            int64_t bsc = 0) {
+  if (M <= 0 || N <= 0) return;
+  const dim3 grid(static_cast<unsigned>((N + kT - 1) / kT), static_cast<unsigned>((M + kT - 1) / kT),
+                  static_cast<unsigned>(batch));
+  gemm64_kernel<TA, TB><<<grid, dim3(256), 0, stream>>>(M, N, K, alpha, A, rsa, csa, bsa, B, rsb, csb,
+                                                        bsb, beta, C, rsc, csc, bsc, lower_only);
+}
+
+// Lower-triangular inverse X = L^-1 of a batch of n x n matrices (n a multiple
+// of 64; batch stride s): the diagonal 64-blocks of X must already hold the
+// inverses of L's; X's strictly upper part zero; tmp holds 64 x n per batch.
+// Row block i: X[i, :i] = -X_ii (L[i, :i] X[:i, :i]).
+void trtri_lower(const double* L, double* X, int64_t n, int64_t ld, int64_t s, int batch, double* tmp,
+                 hipStream_t stream) {
+  const int64_t t = n / kT;
+  for (int64_t i = 1; i < t; ++i) {
+    const int64_t w = i * kT;
+    gemm64(int64_t{kT}, w, w, 1.0, L + i * kT * ld, ld, int64_t{1}, X, ld, int64_t{1}, 0.0, tmp, n,
+           int64_t{1}, stream, 0, batch, s, s, kT * n);
+    gemm64(int64_t{kT}, w, int64_t{kT}, -1.0, X + i * kT * ld + i * kT, ld, int64_t{1}, tmp, n,
+           int64_t{1}, 0.0, X + i * kT * ld, ld, int64_t{1}, stream, 0, batch, s, kT * n, s);
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+
+sdq_status launch_hessian_accumulate(const float* x, int64_t m, int64_t k, double* h, hipStream_t stream) {
+  // H[i][j] += 2 sum_p X[p][i] X[p][j]
+  gemm64(k, k, m, 2.0, x, int64_t{1}, k, x, k, int64_t{1}, 1.0, h, k, int64_t{1}, stream);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "hessian launch");
+  return SDQ_OK;
+}
+
+size_t hessian_factor_ws_bytes(int64_t k) {
+  return 256 + align_up(static_cast<size_t>(k) * k * 8, 256) * 2 + align_up(static_cast<size_t>(kT) * k * 8, 256);
+}
+
+sdq_status launch_hessian_factor(const double* h, int64_t k, double lam, double* u, void* ws,
+                                 hipStream_t stream) {
+  char* p = static_cast<char*>(ws);
+  int* info = reinterpret_cast<int*>(p);
+  double* A = reinterpret_cast<double*>(p + 256);
+  double* X = reinterpret_cast<double*>(p + 256 + align_up(static_cast<size_t>(k) * k * 8, 256));
+  double* tmp = reinterpret_cast<double*>(p + 256 + 2 * align_up(static_cast<size_t>(k) * k * 8, 256));
+  const int64_t kk = k * k;
+  clear_info_kernel<<<1, 64, 0, stream>>>(info);
+  fill_f64_kernel<<<grid1(kk), 256, 0, stream>>>(X, kk, 0.0);
+  reverse_tri_kernel<<<dim3(grid1(kk), 1), 256, 0, stream>>>(h, k, 0, k, A, k, 0, 1, lam);
+  const int64_t t = k / kT;
+  for (int64_t j = 0; j < t; ++j) {
+    const int64_t d = j * kT;
+    potrf64_kernel<<<dim3(1, 1), 256, 0, stream>>>(A + d * k + d, k, 0, 0, X + d * k + d, k, 0, 0, 1, info);
+    const int64_t r0 = d + kT, rows = k - r0;
+    if (rows <= 0) break;
+    // panel: L[r0:, d] = A[r0:, d] L_dd^-T (in place; one 64-wide column of tiles)
+    gemm64(rows, int64_t{kT}, int64_t{kT}, 1.0, A + r0 * k + d, k, int64_t{1}, X + d * k + d, int64_t{1}, k,
+           0.0, A + r0 * k + d, k, int64_t{1}, stream);
+    // trailing lower part: A[r0:, r0:] -= L[r0:, d] L[r0:, d]^T
+    gemm64(rows, rows, int64_t{kT}, -1.0, A + r0 * k + d, k, int64_t{1}, A + r0 * k + d, int64_t{1}, k, 1.0,
+           A + r0 * k + r0, k, int64_t{1}, stream, 1);
+  }
+  trtri_lower(A, X, k, k, 0, 1, tmp, stream);
+  reverse_tri_kernel<<<dim3(grid1(kk), 1), 256, 0, stream>>>(X, k, 0, k, u, k, 0, 0, 0.0);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "hessian factor launch");
+  return SDQ_OK;
+}
+
+// Workspace of the compensated encoder: the plain encoder's, then (256-byte
+// aligned) scratch row maxima, W64 (n x k), the fp32 block (n x B), E and G
+// (n x B each), the scaled codes (n x M), and per block the reversed diagonal
+// block of U, its inverse, the inverse reversed back (nb x B x B each) and
+// the triangular-inverse scratch (nb x 64 x B).
+struct CompWs {
+  QuantWs q;
+  uint32_t* rmax_scratch;
+  double* w64;
+  float* wblk;
+  double* ebuf;
+  double* gbuf;
+  double* cb;
+  double* lb;
+  double* xb;
+  double* vb;
+  double* tmp;
+};
+
+size_t comp_ws_layout(const sdq_layout* L, CompWs* out, void* base) {
+  char* p = static_cast<char*>(base);
+  size_t off = align_up(quant_ws_layout(L, nullptr, nullptr), 256);
+  auto take = [&](size_t bytes) {
+    const size_t at = off;
+    off = align_up(off + bytes, 256);
+    return p ? p + at : nullptr;
+  };
+  CompWs w;
+  if (p) quant_ws_layout(L, &w.q, base);
+  const size_t n = static_cast<size_t>(L->n), B = static_cast<size_t>(L->block), nb = static_cast<size_t>(L->nb);
+  w.rmax_scratch = reinterpret_cast<uint32_t*>(take(static_cast<size_t>(L->n_pad) * 4));
+  w.w64 = reinterpret_cast<double*>(take(n * L->k * 8));
+  w.wblk = reinterpret_cast<float*>(take(n * B * 4));
+  w.ebuf = reinterpret_cast<double*>(take(n * B * 8));
+  w.gbuf = reinterpret_cast<double*>(take(n * B * 8));
+  w.cb = reinterpret_cast<double*>(take(n * L->m_up * 8));
+  w.lb = reinterpret_cast<double*>(take(nb * B * B * 8));
+  w.xb = reinterpret_cast<double*>(take(nb * B * B * 8));
+  w.vb = reinterpret_cast<double*>(take(nb * B * B * 8));
+  w.tmp = reinterpret_cast<double*>(take(nb * kT * B * 8));
+  if (out) *out = w;
+  return off;
+}
+
+sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, const Tables* T,
+                                       const double* u, void* codes, float* scales, void* ws,
+                                       hipStream_t stream) {
+  CompWs cw;
+  comp_ws_layout(L, &cw, ws);
+  const int64_t n = L->n, k = L->k, B = L->block, nb = L->nb, M = L->m_up;
+  // 1. The plain encoding: row scales of the raw W, and block 0's final codes.
+  sdq_status st = launch_quantize(w, L, T, codes, scales, cw.q, stream);
+  if (st != SDQ_OK) return st;
+  // 2. V_b = U_bb^-1 for every block: U_bb reversed is lower triangular;
+  //    invert it (64-blocks, then the off-diagonal blocks) and reverse back.
+  const int64_t bb = B * B;
+  fill_f64_kernel<<<grid1(nb * bb), 256, 0, stream>>>(cw.xb, nb * bb, 0.0);
+  reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
+      u, k, B * k + B, B, cw.lb, B, bb, 1, 0.0);
+  potrf64_kernel<<<dim3(static_cast<unsigned>(B / kT), static_cast<unsigned>(nb)), 256, 0, stream>>>(
+      cw.lb, B, kT * B + kT, bb, cw.xb, B, kT * B + kT, bb, 0, reinterpret_cast<int*>(cw.q.flag) + 1);
+  trtri_lower(cw.lb, cw.xb, B, B, bb, static_cast<int>(nb), cw.tmp, stream);
+  reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
+      cw.xb, B, bb, B, cw.vb, B, bb, 0, 0.0);
+  // 3. The walk over the blocks, W in fp64.
+  widen_kernel<<<grid1(n * k), 256, 0, stream>>>(w, n * k, cw.w64);
+  for (int64_t b = 0; b < nb; ++b) {
+    extract_block_kernel<<<grid1(n * B), 256, 0, stream>>>(cw.w64, n, k, static_cast<int>(B), b * B,
+                                                           cw.wblk, cw.ebuf);
+    if (b > 0) {
+      st = launch_encode_blocks(cw.wblk, B, b, 1, L, T, codes, scales, cw.q, cw.rmax_scratch,
+                                cw.q.rmax, stream);
+      if (st != SDQ_OK) return st;
+    }
+    if (b == nb - 1) break;
+    unpack_scaled_kernel<<<grid1(n * M), 256, 0, stream>>>(static_cast<const uint32_t*>(codes), scales, n,
+                                                           L->n_chunks, L->codes_per_chunk, L->bits,
+                                                           b * M, static_cast<int>(M), cw.cb);
+    // E_b = W_b - (s C_b) E^T
+    gemm64(n, B, M, -1.0, cw.cb, M, int64_t{1}, T->e64, int64_t{1}, M, 1.0, cw.ebuf, B, int64_t{1}, stream);
+    // G = E_b V_b
+    gemm64(n, B, B, 1.0, cw.ebuf, B, int64_t{1}, cw.vb + b * bb, B, int64_t{1}, 0.0, cw.gbuf, B, int64_t{1},
+           stream);
+    // W_F -= G U[Q, F]
+    const int64_t f0 = (b + 1) * B;
+    gemm64(n, k - f0, B, -1.0, cw.gbuf, B, int64_t{1}, u + b * B * k + f0, k, int64_t{1}, 1.0, cw.w64 + f0, k,
+           int64_t{1}, stream);
+  }
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "compensated encoder launch");
+  return SDQ_OK;
+}
+
+size_t comp_ws_bytes(const sdq_layout* L) { return comp_ws_layout(L, nullptr, nullptr); }
+
+}  // namespace sdq

@@ -264,12 +264,15 @@ __global__ __launch_bounds__(kUpThreads) void upsample_kernel(
 }
 
 // One wave per (panel, block) chain set: lane = row.  Words of 32 / bits codes
-// never straddle blocks because M is a multiple of 32.
+// never straddle blocks because M is a multiple of 32.  The samples hold
+// blocks b0 .. b0 + nb - 1 of the layer (k_up = nb * M per row); codes land at
+// their place in the layer's nb_total blocks, the scales are written with
+// block 0 and the row's padding words with its last block.
 template <int LEVELS>
 __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
     const float* __restrict__ xup, const uint32_t* __restrict__ rmax, int64_t n, int64_t nb,
-    int64_t k_up, int m_up, int64_t n_chunks, uint32_t* __restrict__ codes,
-    float* __restrict__ scales, uint32_t* __restrict__ flag) {
+    int64_t b0, int64_t nb_total, int64_t k_up, int m_up, int64_t n_chunks,
+    uint32_t* __restrict__ codes, float* __restrict__ scales, uint32_t* __restrict__ flag) {
   constexpr int BITS = LEVELS == 2 ? 1 : 2;
   constexpr int PER_WORD = 32 / BITS;
   constexpr int WORDS_PER_CHUNK = 4;
@@ -277,10 +280,11 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
   const int64_t b = static_cast<int64_t>(blockIdx.y) * kScanWaves + threadIdx.x / 64;
   const int64_t panel = blockIdx.x;
   if (b >= nb) return;
+  const int64_t gb = b0 + b;            // block index in the layer
   const int64_t r = panel * kPanel + lane;
   const bool live = r < n;
   const float s = live ? __uint_as_float(rmax[r]) : 0.0f;
-  if (live && b == 0) {
+  if (live && gb == 0) {
     scales[r] = s;
     if (!isfinite(s)) atomicOr(flag, 1u);
   }
@@ -288,7 +292,7 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
   const float* src = xup + (panel * k_up + b * m_up) * kPanel + lane;
   uint32_t* dst_row = codes + (panel * n_chunks * kPanel + lane) * WORDS_PER_CHUNK;
   float u = 0.0f;
-  int64_t wj = (b * m_up) / PER_WORD;   // first word of this block in the row
+  int64_t wj = (gb * m_up) / PER_WORD;  // first word of this block in the row
   for (int m0 = 0; m0 < m_up; m0 += PER_WORD, ++wj) {
     uint32_t word = 0u;
     if (live) {
@@ -310,7 +314,7 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
     const int64_t c = wj / WORDS_PER_CHUNK;
     dst_row[c * kPanel * WORDS_PER_CHUNK + (wj % WORDS_PER_CHUNK)] = word;
   }
-  if (b == nb - 1) {
+  if (gb == nb_total - 1) {
     // Zero the padding words after the last code of the row.
     const int64_t total_words = n_chunks * WORDS_PER_CHUNK;
     for (; wj < total_words; ++wj) {
@@ -322,54 +326,55 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
 
 }  // namespace
 
-sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
-                           float* scales, const QuantWs& ws, hipStream_t stream) {
+sdq_status launch_encode_blocks(const float* w, int64_t ldw, int64_t b0, int64_t nbl,
+                                const sdq_layout* L, const Tables* T, void* codes, float* scales,
+                                const QuantWs& ws, uint32_t* rmax_acc, const uint32_t* rmax_scale,
+                                hipStream_t stream) {
   const int64_t n_panels = L->n_pad / kPanel;
   const int64_t n_ws = quant_ws_rows(L);     // rows covered by the upsample tiles
   const int B = L->block;
+  const int64_t k_up = nbl * L->m_up;        // samples per row held in the workspace
   const float inv_sqrt_b =
       L->hadamard == SDQ_HAD_NONE ? 1.0f : static_cast<float>(1.0 / std::sqrt(static_cast<double>(B)));
   SignMask sm;
   for (int i = 0; i < 8; ++i) sm.w[i] = L->hadamard == SDQ_HAD_SIGNED ? L->had_signs[i] : 0u;
-  clear_kernel<<<dim3(static_cast<unsigned>((L->n_pad + 255) / 256)), dim3(256), 0, stream>>>(
-      ws.flag, ws.rmax, L->n_pad);
-  const dim3 rgrid(static_cast<unsigned>(n_ws / kPanel), static_cast<unsigned>(L->nb));
+  const dim3 rgrid(static_cast<unsigned>(n_ws / kPanel), static_cast<unsigned>(nbl));
+#define SDQ_ROT(BB)                                                                                 \
+  rotate_kernel<BB><<<rgrid, dim3(kRotThreads), 0, stream>>>(                                       \
+      w, L->n, ldw, n_ws, k_up, L->m_up, T->g0, T->phases, L->hadamard, sm, inv_sqrt_b, ws.v, ws.xup, \
+      rmax_acc, ws.flag)
   switch (B) {
-    case 64:
-      rotate_kernel<64><<<rgrid, dim3(kRotThreads), 0, stream>>>(
-          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, L->hadamard, sm, inv_sqrt_b, ws.v, ws.xup,
-          ws.rmax, ws.flag);
-      break;
-    case 128:
-      rotate_kernel<128><<<rgrid, dim3(kRotThreads), 0, stream>>>(
-          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, L->hadamard, sm, inv_sqrt_b, ws.v, ws.xup,
-          ws.rmax, ws.flag);
-      break;
-    default:
-      rotate_kernel<256><<<rgrid, dim3(kRotThreads), 0, stream>>>(
-          w, L->n, L->k, n_ws, L->k_up, L->m_up, T->g0, T->phases, L->hadamard, sm, inv_sqrt_b, ws.v, ws.xup,
-          ws.rmax, ws.flag);
-      break;
+    case 64: SDQ_ROT(64); break;
+    case 128: SDQ_ROT(128); break;
+    default: SDQ_ROT(256); break;
   }
+#undef SDQ_ROT
   if (T->m_nz > 0) {
     const dim3 ugrid(static_cast<unsigned>(n_ws / kUpBM),
-                     static_cast<unsigned>(T->m_nz_pad / kUpBN), static_cast<unsigned>(L->nb));
+                     static_cast<unsigned>(T->m_nz_pad / kUpBN), static_cast<unsigned>(nbl));
     upsample_kernel<<<ugrid, dim3(kUpThreads), 0, stream>>>(
-        ws.v, T->unz, L->n, n_ws, L->k_up, B, L->m_up, T->phases, T->m_nz, T->m_nz_pad, ws.xup,
-        ws.rmax);
+        ws.v, T->unz, L->n, n_ws, k_up, B, L->m_up, T->phases, T->m_nz, T->m_nz_pad, ws.xup,
+        rmax_acc);
   }
-  const dim3 sgrid(static_cast<unsigned>(n_panels), static_cast<unsigned>((L->nb + kScanWaves - 1) / kScanWaves));
+  const dim3 sgrid(static_cast<unsigned>(n_panels), static_cast<unsigned>((nbl + kScanWaves - 1) / kScanWaves));
   if (L->levels == 3)
     scan_kernel<3><<<sgrid, dim3(64 * kScanWaves), 0, stream>>>(
-        ws.xup, ws.rmax, L->n, L->nb, L->k_up, L->m_up, L->n_chunks, static_cast<uint32_t*>(codes),
-        scales, ws.flag);
+        ws.xup, rmax_scale, L->n, nbl, b0, L->nb, k_up, L->m_up, L->n_chunks,
+        static_cast<uint32_t*>(codes), scales, ws.flag);
   else
     scan_kernel<2><<<sgrid, dim3(64 * kScanWaves), 0, stream>>>(
-        ws.xup, ws.rmax, L->n, L->nb, L->k_up, L->m_up, L->n_chunks, static_cast<uint32_t*>(codes),
-        scales, ws.flag);
+        ws.xup, rmax_scale, L->n, nbl, b0, L->nb, k_up, L->m_up, L->n_chunks,
+        static_cast<uint32_t*>(codes), scales, ws.flag);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "encoder launch");
   return SDQ_OK;
+}
+
+sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
+                           float* scales, const QuantWs& ws, hipStream_t stream) {
+  clear_kernel<<<dim3(static_cast<unsigned>((L->n_pad + 255) / 256)), dim3(256), 0, stream>>>(
+      ws.flag, ws.rmax, L->n_pad);
+  return launch_encode_blocks(w, L->k, 0, L->nb, L, T, codes, scales, ws, ws.rmax, ws.rmax, stream);
 }
 
 }  // namespace sdq

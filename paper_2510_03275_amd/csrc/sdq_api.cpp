@@ -124,6 +124,7 @@ static sdq_status get_tables_for(int block, int m_up, int had, const SignWords& 
   T.m_pad = (m_up + 63) / 64 * 64;
   std::vector<float> edec(static_cast<size_t>(T.m_pad) * block, 0.0f);
   std::vector<uint16_t> eh(em), el(em);
+  std::vector<double> e64(em);          // E[t][m] in fp64, row-major B x M
   std::vector<double> row(block);
   const double inv_sqrt_b = 1.0 / std::sqrt(static_cast<double>(block));
   double e1max = 0.0;   // max over samples m of sum_t |fp32(E[t][m])|
@@ -146,6 +147,7 @@ static sdq_status get_tables_for(int block, int m_up, int had, const SignWords& 
     for (int t = 0; t < block; ++t) {
       const double val = row[t];
       const size_t at = static_cast<size_t>(m) * block + t;
+      e64[static_cast<size_t>(t) * m_up + m] = val;
       edec[(static_cast<size_t>(t / 4) * T.m_pad + m) * 4 + t % 4] = static_cast<float>(val);
       col1 += std::fabs(static_cast<double>(static_cast<float>(val)));
       const _Float16 hi = static_cast<_Float16>(val);
@@ -164,9 +166,12 @@ static sdq_status get_tables_for(int block, int m_up, int had, const SignWords& 
     e = hipMalloc(dst, em * 2);
     if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
   }
+  e = hipMalloc(&T.e64, em * 8);
+  if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
   e = hipMemcpy(T.edec, edec.data(), edec.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(T.et_hi, eh.data(), em * 2, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(T.et_lo, el.data(), em * 2, hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(T.e64, e64.data(), em * 8, hipMemcpyHostToDevice);
   if (e != hipSuccess) return hip_error(e, "table upload");
   auto res = g_tables.emplace(key, T);
   *out = &res.first->second;
@@ -245,6 +250,7 @@ const char* sdq_status_string(sdq_status s) {
     case SDQ_ERR_HIP: return "HIP runtime error";
     case SDQ_ERR_NOMEM: return "out of device memory";
     case SDQ_ERR_UNSUPPORTED: return "unsupported request";
+    case SDQ_ERR_NOT_SPD: return "matrix not positive definite";
   }
   return "unknown status";
 }
@@ -345,6 +351,61 @@ sdq_status sdq_quantize_check(const void* ws, void* stream) {
   if (e != hipSuccess) return hip_error(e, "reading the status flag");
   if (flag) return set_error(SDQ_ERR_NONFINITE, "a weight or an upsampled sample is not finite");
   return SDQ_OK;
+}
+
+sdq_status sdq_hessian_accumulate(const float* x, int64_t m, int64_t k, double* h, void* stream) {
+  if (m < 0 || k <= 0) return set_error(SDQ_ERR_ARG, "need m >= 0 and k > 0");
+  if (m == 0) return SDQ_OK;
+  if (!x || !h) return set_error(SDQ_ERR_ARG, "x and h must be non-NULL");
+  return launch_hessian_accumulate(x, m, k, h, static_cast<hipStream_t>(stream));
+}
+
+size_t sdq_hessian_factor_workspace_bytes(int64_t k) {
+  if (k <= 0 || k % 64) return 0;
+  return hessian_factor_ws_bytes(k);
+}
+
+sdq_status sdq_hessian_factor(const double* h, int64_t k, double lambda, double* u, void* ws,
+                              size_t ws_bytes, void* stream) {
+  if (k <= 0 || k % 64) return set_error(SDQ_ERR_SHAPE, "k=%lld must be a positive multiple of 64", (long long)k);
+  if (!h || !u) return set_error(SDQ_ERR_ARG, "h and u must be non-NULL");
+  if (!(lambda >= 0.0) || !std::isfinite(lambda)) return set_error(SDQ_ERR_ARG, "lambda must be finite and >= 0");
+  const size_t need = hessian_factor_ws_bytes(k);
+  if (!ws || ws_bytes < need)
+    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  return launch_hessian_factor(h, k, lambda, u, ws, static_cast<hipStream_t>(stream));
+}
+
+sdq_status sdq_hessian_check(const void* ws, void* stream) {
+  if (!ws) return set_error(SDQ_ERR_ARG, "workspace is NULL");
+  hipError_t e = hipStreamSynchronize(static_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return hip_error(e, "hipStreamSynchronize");
+  int info = 0;
+  e = hipMemcpy(&info, ws, sizeof(info), hipMemcpyDeviceToHost);
+  if (e != hipSuccess) return hip_error(e, "reading the factorisation status");
+  if (info) return set_error(SDQ_ERR_NOT_SPD, "H + lambda I is not positive definite in fp64");
+  return SDQ_OK;
+}
+
+size_t sdq_quantize_compensated_workspace_bytes(const sdq_layout* L) {
+  if (check_layout(L) != SDQ_OK) return 0;
+  return comp_ws_bytes(L);
+}
+
+sdq_status sdq_quantize_compensated(const float* w, const sdq_layout* L, const double* u, void* codes,
+                                    float* scales, void* ws, size_t ws_bytes, void* stream) {
+  sdq_status st = check_layout(L);
+  if (st != SDQ_OK) return st;
+  if (L->n > 0 && (!w || !u || !codes || !scales))
+    return set_error(SDQ_ERR_ARG, "w, u, codes and scales must be non-NULL");
+  const size_t need = comp_ws_bytes(L);
+  if (!ws || ws_bytes < need)
+    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (L->n == 0) return SDQ_OK;
+  const Tables* T = nullptr;
+  st = get_tables(L, &T);
+  if (st != SDQ_OK) return st;
+  return launch_quantize_compensated(w, L, T, u, codes, scales, ws, static_cast<hipStream_t>(stream));
 }
 
 size_t sdq_linear_workspace_bytes(const sdq_layout* L, int64_t m) {
@@ -588,6 +649,7 @@ void sdq_release_tables(void) {
     if (kv.second.edec) (void)hipFree(kv.second.edec);
     if (kv.second.et_hi) (void)hipFree(kv.second.et_hi);
     if (kv.second.et_lo) (void)hipFree(kv.second.et_lo);
+    if (kv.second.e64) (void)hipFree(kv.second.e64);
     (void)hipSetDevice(cur);
   }
   g_tables.clear();

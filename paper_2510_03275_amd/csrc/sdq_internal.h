@@ -35,6 +35,7 @@ struct Tables {
   float* edec = nullptr;
   uint16_t* et_hi = nullptr;
   uint16_t* et_lo = nullptr;
+  double* e64 = nullptr;   // E[t][m], fp64, row-major B x M (block reconstruction)
 };
 
 // Returns the cached tables of the layout's (block, M, Had) for the current
@@ -62,6 +63,14 @@ size_t quant_ws_layout(const sdq_layout* L, QuantWs* ws, void* base);
 
 sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
                            float* scales, const QuantWs& ws, hipStream_t stream);
+// Encode blocks b0 .. b0 + nbl - 1 from w (row stride ldw; column 0 of w is the
+// first column of block b0): rotate and upsample fold their row maxima into
+// rmax_acc, the scan uses the row scales in rmax_scale (one buffer for a plain
+// encode; a scratch buffer and the fixed scales for a re-encoded block).
+sdq_status launch_encode_blocks(const float* w, int64_t ldw, int64_t b0, int64_t nbl,
+                                const sdq_layout* L, const Tables* T, void* codes, float* scales,
+                                const QuantWs& ws, uint32_t* rmax_acc, const uint32_t* rmax_scale,
+                                hipStream_t stream);
 
 // Decode path (m <= 16): expansion (fp32 x_tilde) then LUT GEMV.
 size_t decode_ws_bytes(const sdq_layout* L, int64_t m);
@@ -84,6 +93,16 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
 sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
                                    const sdq_layout* L, float* y, bool accumulate, void* ws,
                                    hipStream_t stream);
+
+// Block compensation (Algorithm 1 lines 3-8), fp64.
+sdq_status launch_hessian_accumulate(const float* x, int64_t m, int64_t k, double* h, hipStream_t stream);
+size_t hessian_factor_ws_bytes(int64_t k);
+sdq_status launch_hessian_factor(const double* h, int64_t k, double lam, double* u, void* ws,
+                                 hipStream_t stream);
+size_t comp_ws_bytes(const sdq_layout* L);
+sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, const Tables* T,
+                                       const double* u, void* codes, float* scales, void* ws,
+                                       hipStream_t stream);
 
 // Moments (mean, variance) of a device array.
 size_t moments_ws_bytes(int64_t count);

@@ -206,3 +206,23 @@ def test_single_hip_runtime_in_process():
     import torch  # noqa: F401
     from synth import gpu  # noqa: F401
     assert len(Bd.hip_runtimes_loaded()) == 1
+
+
+def test_compensation_entry_points_validate_before_gpu_work():
+    lib = P.lib()
+    assert lib.sdq_hessian_factor_workspace_bytes(100) == 0
+    assert lib.sdq_hessian_factor_workspace_bytes(128) >= 2 * 128 * 128 * 8
+    fake = ctypes.c_void_p(0x1000)
+    assert lib.sdq_hessian_factor(fake, 100, 0.1, fake, fake, 1 << 30, None) == -2
+    assert lib.sdq_hessian_factor(None, 128, 0.1, fake, fake, 1 << 30, None) == -1
+    assert lib.sdq_hessian_factor(fake, 128, -1.0, fake, fake, 1 << 30, None) == -1
+    assert lib.sdq_hessian_factor(fake, 128, float("nan"), fake, fake, 1 << 30, None) == -1
+    assert lib.sdq_hessian_factor(fake, 128, 0.1, fake, fake, 16, None) == -6
+    assert lib.sdq_hessian_accumulate(fake, -1, 64, fake, None) == -1
+    assert lib.sdq_hessian_accumulate(None, 0, 64, fake, None) == 0          # m = 0: nothing to do
+    L = P.sdq_layout_init(64, 512, 2.0, 3)
+    need = lib.sdq_quantize_compensated_workspace_bytes(ctypes.byref(L))
+    assert need > lib.sdq_quantize_workspace_bytes(ctypes.byref(L)) + 64 * 512 * 8
+    assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), None, fake, fake, fake, need, None) == -1
+    assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), fake, fake, fake, fake, need - 1, None) == -6
+    assert lib.sdq_status_string(-10) == b"matrix not positive definite"
