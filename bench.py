@@ -19,9 +19,10 @@ streams its codes from HBM.  The line also carries:
                bf16 activations (TFLOP/s, fp16 MFMA roofline), MultiOSR on
                the LLaMA-7B layer's seven linears, the 80-layer LLaMA-70B
                stack (560 linears quantised, one token through all of them),
-               and the continuous-precision sweep (output error and weight SNR
+               the continuous-precision sweep (output error and weight SNR
                against OSR 1..4 for each Hadamard choice, and MultiOSR against
-               a uniform OSR);
+               a uniform OSR), and Algorithm 1's block compensation (Hessian,
+               factor, compensated encoding: times and held-out error);
 * cpu_baseline -- the CPU oracle on a bounded sample of the same workload.
 """
 from __future__ import annotations
@@ -401,6 +402,79 @@ def multiosr_ablation(torch, P, synth, SG, targets=(1.5, 2.0, 2.5, 3.0), lo: flo
     return {"workload": "llama7b_layer_7_linears_ternary", "lo": lo, "hi": hi, "m": m, "rows": res}
 
 
+F64_PEAK_TFLOPS = 78.6   # MI355X fp64 vector (and matrix) peak, FMA = 2 flops
+
+
+def bench_compensation(torch, P, synth, SG, n: int = 4096, k: int = 4096, m_cal: int = 16384,
+                       m_test: int = 256, rank: int = 32, osr: float = 2.0, levels: int = 3,
+                       seed: int = 2517):
+    """Algorithm 1's block compensation on a LLaMA-7B q_proj-sized layer: the
+    Hessian of m_cal calibration rows, its damped inverse's Cholesky factor and
+    the compensated encoding, each timed (fp64 throughput against the fp64
+    peak), and the layer-output error on m_test held-out rows of the same
+    input distribution with and without compensation.  Inputs: a shared
+    low-rank part plus noise with uneven channel scales (the seeded
+    generator's normals combined on the device)."""
+    import numpy as np
+    w = SG.weight_rows_gpu(seed, 0, n, k, 0.02, True)
+    mix = SG.activations_gpu(seed, 11, k, rank)
+    ch = torch.exp(0.5 * SG.activations_gpu(seed, 12, 1, k))
+
+    def draw(stream, m):
+        z = SG.activations_gpu(seed, stream, m, rank)
+        e = SG.activations_gpu(seed, stream + 1, m, k)
+        return ((z @ mix.t()) * 0.9 + e) * ch
+
+    x_cal = draw(13, m_cal).contiguous()
+    x_test = draw(15, m_test).contiguous()
+
+    def timed(fn):
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        out = fn()
+        b.record()
+        torch.cuda.synchronize()
+        return out, a.elapsed_time(b)
+
+    h = torch.zeros((k, k), dtype=torch.float64, device="cuda")
+    P.sdq_hessian_accumulate(x_cal[:64].contiguous(), h)          # warm-up (and discarded)
+    h.zero_()
+    _, ms_h = timed(lambda: P.sdq_hessian_accumulate(x_cal, h))
+    lam = 0.01 * float(torch.mean(torch.diagonal(h)).item())
+    u = P.hessian_factor(h, lam)                                   # warm-up
+    u, ms_f = timed(lambda: P.hessian_factor(h, lam, check=False))
+    ws = torch.empty(P.sdq_hessian_factor_workspace_bytes(k), dtype=torch.uint8, device="cuda")
+    P.sdq_hessian_factor(h, lam, u, ws)
+    P.sdq_hessian_check(ws)
+    P.quantize_compensated(w, osr, levels, u)                      # warm-up
+    enc_c, ms_c = timed(lambda: P.quantize_compensated(w, osr, levels, u, check=False))
+    enc_p, ms_p = timed(lambda: P.quantize(w, osr, levels, check=False))
+    y_ref = x_test.double().cpu().numpy() @ w.double().cpu().numpy().T
+    errs = {}
+    for name, enc in (("plain", enc_p), ("compensated", enc_c)):
+        y = P.linear(x_test, enc).double().cpu().numpy()
+        errs[name] = float(np.linalg.norm(y - y_ref) / np.linalg.norm(y_ref))
+    flops_h = 2.0 * m_cal * k * k
+    flops_f = 2.0 * k ** 3 / 3.0          # Cholesky k^3/3 plus triangular inverse k^3/3
+    nb = k // 256
+    m_up = int(round(osr * 256))
+    flops_c = 2.0 * n * k * k / 2 + 2.0 * n * m_up * k + 2.0 * n * 256 * k
+    tf = lambda f, ms: f / (ms * 1e-3) / 1e12
+    del h, u, x_cal, enc_c, enc_p, w, ws
+    torch.cuda.empty_cache()
+    return {"workload": f"llama7b_q_proj_{n}x{k}_osr{osr:g}_ternary_compensated_{m_cal}_calibration_rows",
+            "hessian_ms": ms_h, "hessian_tflops": tf(flops_h, ms_h),
+            "factor_ms": ms_f, "factor_tflops": tf(flops_f, ms_f),
+            "compensated_quantize_ms": ms_c, "compensated_tflops": tf(flops_c, ms_c),
+            "plain_quantize_ms": ms_p, "blocks": nb,
+            "out_rel_err_plain": errs["plain"], "out_rel_err_compensated": errs["compensated"],
+            "roofline": {"bound": "alu", "achieved": tf(flops_h, ms_h), "peak": F64_PEAK_TFLOPS,
+                         "unit": "TFLOP/s", "frac": tf(flops_h, ms_h) / F64_PEAK_TFLOPS, "traffic": None,
+                         "kernel": "gemm64_kernel<float,float> (Hessian)",
+                         "note": "fp64 FMA GEMM; flops = 2 * m * k^2"}}
+
+
 def bench_sweep(torch, P, synth, SG):
     t0 = time.perf_counter()
     rows = precision_sweep(torch, P, synth, SG)
@@ -563,6 +637,10 @@ def main() -> int:
             line["phases"]["precision_sweep"] = bench_sweep(torch, P, synth, SG)
         except Exception as exc:  # noqa: BLE001
             line["phases"]["precision_sweep"] = {"error": repr(exc)}
+        try:
+            line["phases"]["compensation"] = bench_compensation(torch, P, synth, SG)
+        except Exception as exc:  # noqa: BLE001
+            line["phases"]["compensation"] = {"error": repr(exc)}
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(synth, dec)
     line["wall_s"] = time.perf_counter() - t_start
