@@ -61,7 +61,7 @@ TRAFFIC_SOURCES = {
 }
 TRAFFIC_KIB = {   # kernel -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB)
     "gemv_lut_kernel<1,2,2>": ("linear_decode.hip", 4420.88, 1040.0),
-    "gemv_lut_kernel<1,3,8>": ("linear_decode.hip", 57888.78, 3584.0),
+    "gemv_lut_kernel<1,3,4>": ("linear_decode.hip", 57888.78, 3584.0),
     "gemm_prefill_kernel<3>": ("linear_prefill.hip", 317410.33, 65536.0),
 }
 
@@ -184,8 +184,8 @@ def bench_decode_70b(torch, P, synth, SG, replays: int = 20):
             "code_bytes": nbytes, "rotating_code_buffers": rot,
             "roofline": {"bound": "hbm", "achieved": gemv_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": gemv_gbs / HBM_PEAK_GBS,
-                         "traffic": traffic_bytes("gemv_lut_kernel<1,3,8>"),
-                         "kernel": "gemv_lut_kernel<1,3,8>"}}
+                         "traffic": traffic_bytes("gemv_lut_kernel<1,3,4>"),
+                         "kernel": "gemv_lut_kernel<1,3,4>"}}
 
 
 def bench_encoder(torch, P, w, wl, reps: int = 5):

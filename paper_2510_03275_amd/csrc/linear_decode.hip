@@ -526,11 +526,14 @@ int round_mr(int64_t m) {
   return 16;
 }
 
-// Chunks per K segment of the table GEMV.  Larger segments amortise the table
-// build and cut the atomics per output, smaller ones give more workgroups; the
-// largest segment that still yields about four workgroups per CU wins
-// (measured on MI355X at m = 1: 4096 x 11008 picks 2, 28672 x 8192 picks 8).
-// Tables of MR rows x SEG chunks must fit 64 KB.
+// Chunks per K segment of the table GEMV.  Each segment adds one atomic per
+// output into y, and the atomics on one address serialise, so the segments
+// per output (n_chunks / SEG) set a floor; smaller segments give more
+// workgroups to stream the codes.  Measured on MI355X at m = 1 over nine layer
+// shapes (768 x 768 to 28672 x 8192 and 8192 x 28672): SEG = 4 is best unless
+// it leaves fewer than 800 workgroups and SEG = 2 keeps the segments per
+// output at 80 or below (small layers: 2), or it needs more than 128 segments
+// per output (long rows: 8).  Tables of MR rows x SEG chunks must fit 64 KB.
 int pick_seg(const sdq_layout* L, int mr) {
   static const char* env = std::getenv("SDQ_GEMV_SEG");   // tuning aid: 2, 4 or 8
   const int max_seg = mr >= 16 ? 2 : (mr >= 8 ? 4 : 8);
@@ -539,9 +542,12 @@ int pick_seg(const sdq_layout* L, int mr) {
     if ((v == 2 || v == 4 || v == 8) && v <= max_seg) return v;
   }
   const int64_t panel_groups = (L->n_pad / kPanel + kGemvWaves - 1) / kGemvWaves;
-  for (int seg = max_seg; seg > 2; seg /= 2)
-    if (panel_groups * ((L->n_chunks + seg - 1) / seg) >= 1024) return seg;
-  return 2;
+  const int64_t segs2 = (L->n_chunks + 1) / 2, segs4 = (L->n_chunks + 3) / 4;
+  int seg;
+  if (segs2 <= 80 && panel_groups * segs4 < 800) seg = 2;
+  else if (segs4 > 128) seg = 8;
+  else seg = 4;
+  return std::min(seg, max_seg);
 }
 
 int segs_for(const sdq_layout* L, int seg) {
