@@ -227,12 +227,15 @@ __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
 // (8 x 2 accumulator tiles of 32 x 32).  The x_tilde tile is double-buffered
 // in LDS and filled straight from global memory (global_load_lds_dwordx4, no
 // staging registers); its 16-byte groups are XOR-swizzled by row so that the
-// fragment reads of 16 consecutive rows fall on distinct banks.  The codes go
-// from global memory to registers one k step ahead and are expanded to fp16
-// with byte-permute lookups, each expanded fragment feeding eight MFMAs.
+// fragment reads of 16 consecutive rows fall on distinct banks.  A ring of
+// four buffers (128 KB): the copies for step k + 2 are issued while step k
+// computes, so a copy has two steps to land.  The codes go from global memory
+// to registers two steps ahead as well and are expanded to fp16 with
+// byte-permute lookups, each expanded fragment feeding eight MFMAs.
 // ---------------------------------------------------------------------------
 constexpr int kBM = 256, kBN = 256, kBK = 64;
-constexpr int kTileHalves = kBM * kBK;      // one LDS buffer (32 KB)
+constexpr int kTileHalves = kBM * kBK;      // one x_tilde tile (32 KB)
+constexpr int kABufs = 4;                    // a ring of tiles; steps k + 1 and k + 2 in flight during k
 
 typedef __attribute__((address_space(3))) void* lds_void_ptr;
 typedef __attribute__((address_space(1))) const void* gbl_void_ptr;
@@ -296,7 +299,7 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     const _Float16* __restrict__ xt, const uint4* __restrict__ codes,
     const float* __restrict__ scales, int64_t m, int64_t n, int64_t n_pad, int64_t n_chunks,
     int64_t k_up_pad, float* __restrict__ y, int accumulate) {
-  __shared__ __attribute__((aligned(1024))) _Float16 As[2][kTileHalves];
+  __shared__ __attribute__((aligned(1024))) _Float16 As[kABufs][kTileHalves];
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
@@ -334,22 +337,28 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
                                        (lds_void_ptr)(dst_ + j * 8 * kBK), 16, 0, 0);            \
   } while (0)
 
+  const int it1 = n_iter > 1 ? 1 : 0;
+  SDQ_FILL_A(0, 0);
+  SDQ_FILL_A(1, it1);
   uint4 c0 = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, 0);
   uint4 c1 = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, 0);
-  SDQ_FILL_A(0, 0);
+  uint4 d0 = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, it1);   // the next step's
+  uint4 d1 = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, it1);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
   // Fragment read offsets (halves) of row tile rt, k group g: row r = 32 rt + lane % 32.
   const int fr = lane % 32;
   for (int it = 0; it < n_iter; ++it) {
-    const int cur = it & 1;
-    // Prefetch the next k step into the other buffer (the last iteration
-    // refills the idle buffer with its own tile; it is never read again).
-    const int nx = it + 1 < n_iter ? it + 1 : it;
-    SDQ_FILL_A(cur ^ 1, nx);
-    const uint4 n0c = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, nx);
-    const uint4 n1c = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, nx);
+    // Step it reads buffer it % 4 and copies step it + 2 into buffer
+    // (it + 2) % 4 = cur ^ 2, an index the compiler can tell apart from cur,
+    // so it does not wait for the copies before reading (near the end the
+    // last step is copied again; that copy is never read).
+    const int cur = it & 3;
+    const int n2 = it + 2 < n_iter ? it + 2 : n_iter - 1;
+    SDQ_FILL_A(cur ^ 2, n2);
+    const uint4 e0 = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, n2);
+    const uint4 e1 = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, n2);
     const _Float16* abuf = As[cur];
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
@@ -364,10 +373,21 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
         acc[rt][1] = mfma32(afrag, b1, acc[rt][1]);
       }
     }
-    c0 = n0c;
-    c1 = n1c;
-    __builtin_amdgcn_s_waitcnt(0);          // this lane's tile copies have landed
-    __syncthreads();                          // ... and every other lane's
+    c0 = d0;
+    c1 = d1;
+    d0 = e0;
+    d1 = e1;
+    // The next step's tile (copied a step ago) has landed for this lane: at
+    // most this step's eight tile copies and two code loads are outstanding
+    // (vmcnt 10; expcnt and lgkmcnt not waited on), and for every lane after the
+    // barrier.  A plain s_barrier: __syncthreads() adds a release fence, which
+    // waits for every outstanding LDS copy.  The empty asm statements keep LDS
+    // accesses from moving across it; every fragment read of the buffer that
+    // is refilled next has returned before its MFMAs issued.
+    __builtin_amdgcn_s_waitcnt(0xF7A);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
   }
 #undef SDQ_FILL_A
 
