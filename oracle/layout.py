@@ -15,6 +15,16 @@ Format (the library's C header is the normative description):
 * binary field 1 means +1 and 0 means -1; ternary field 00 means 0, 01 means +1,
   11 means -1 (10 is never written);
 * padding codes and padding rows are all-zero bits.
+
+Base-3 packing of ternary codes (Eq. 14 counts a ternary code as log2(3) =
+1.58 bits; five codes per byte, 3^5 = 243 <= 256, store 1.6 bits each):
+
+* a 16-byte chunk holds 80 codes; the chunk and panel layout are as above;
+* code j of a row is in chunk j // 80 at position q = j % 80, which is digit
+  q % 5 of byte q // 5 of the chunk; a byte holds
+  d_0 + 3 d_1 + 9 d_2 + 27 d_3 + 81 d_4 with digit d = code + 1 in {0, 1, 2}
+  (bytes 243 .. 255 are never written);
+* padding codes are code 0 (digit 1) and padding rows all-zero bytes.
 """
 from __future__ import annotations
 
@@ -91,3 +101,41 @@ def unpack(buf: np.ndarray, n: int, k_up: int, levels: int) -> np.ndarray:
 def compression_ratio(bits_per_code: float, osr: float) -> float:
     """Eq. 14: eta = N * OSR / 16 (storage of the codes relative to fp16 weights)."""
     return bits_per_code * osr / 16.0
+
+
+B3_CODES_PER_CHUNK = 80
+
+
+def geometry_base3(n: int, k_up: int):
+    n_chunks = -(-k_up // B3_CODES_PER_CHUNK)
+    n_pad = -(-n // PANEL) * PANEL
+    return n_pad, n_chunks
+
+
+def pack_base3(codes: np.ndarray) -> np.ndarray:
+    """Ternary int8 codes (N x K_up) -> the base-3 packed buffer."""
+    codes = np.asarray(codes)
+    n, k_up = codes.shape
+    n_pad, n_chunks = geometry_base3(n, k_up)
+    digits = np.zeros((n_pad, n_chunks * B3_CODES_PER_CHUNK), dtype=np.uint32)
+    digits[:n] = 1                                   # padding codes of real rows: code 0
+    digits[:n, :k_up] = codes.astype(np.int64) + 1
+    digits[n:] = 0                                   # padding rows: zero bytes
+    d = digits.reshape(n_pad, n_chunks, 16, 5)
+    byte = d[..., 0] + 3 * d[..., 1] + 9 * d[..., 2] + 27 * d[..., 3] + 81 * d[..., 4]
+    byte = byte.astype(np.uint8).reshape(n_pad // PANEL, PANEL, n_chunks, 16).transpose(0, 2, 1, 3)
+    return np.ascontiguousarray(byte).reshape(-1)
+
+
+def unpack_base3(buf: np.ndarray, n: int, k_up: int) -> np.ndarray:
+    """Inverse of ``pack_base3``: buffer -> ternary int8 codes (N x K_up)."""
+    n_pad, n_chunks = geometry_base3(n, k_up)
+    b = np.asarray(buf, dtype=np.uint8).reshape(n_pad // PANEL, n_chunks, PANEL, 16)
+    b = b.transpose(0, 2, 1, 3).reshape(n_pad, n_chunks * 16).astype(np.int64)
+    digits = np.stack([(b // 3 ** i) % 3 for i in range(5)], axis=-1).reshape(n_pad, -1)
+    return (digits[:n, :k_up] - 1).astype(np.int8)
+
+
+def packed_bytes_base3(n: int, k_up: int) -> int:
+    n_pad, n_chunks = geometry_base3(n, k_up)
+    return n_pad * n_chunks * CHUNK_BYTES

@@ -56,3 +56,38 @@ def test_round_trip(levels, n, k_up):
     buf = LY.pack(codes, levels)
     assert buf.size == LY.packed_bytes(n, k_up, levels)
     assert np.array_equal(LY.unpack(buf, n, k_up, levels), codes)
+
+
+# --- base-3 packing of ternary codes (five codes per byte) ---
+
+def test_base3_worked_bytes():
+    # codes (+1, 0, -1, -1, +1) -> digits (2, 1, 0, 0, 2) -> 2 + 3 + 0 + 0 + 162 = 167;
+    # all zeros -> 1 + 3 + 9 + 27 + 81 = 121; all +1 -> 242; all -1 -> 0.
+    from oracle import layout as LY
+    codes = np.zeros((1, 80), np.int8)
+    codes[0, :5] = [1, 0, -1, -1, 1]
+    codes[0, 5:10] = 1
+    codes[0, 10:15] = -1
+    buf = LY.pack_base3(codes)
+    assert buf.size == 64 * 16
+    assert list(buf[:4]) == [167, 242, 0, 121]
+    assert np.all(buf[16:] == 0)                       # padding rows
+
+
+@pytest.mark.parametrize("n,k_up", [(1, 80), (5, 81), (70, 512), (130, 1088)])
+def test_base3_round_trip_and_size(n, k_up):
+    from oracle import layout as LY
+    rng = np.random.default_rng(n + k_up)
+    codes = rng.integers(-1, 2, size=(n, k_up)).astype(np.int8)
+    buf = LY.pack_base3(codes)
+    assert buf.size == LY.packed_bytes_base3(n, k_up) == -(-n // 64) * 64 * -(-k_up // 80) * 16
+    assert np.all(buf.reshape(-1) <= 242)
+    assert np.array_equal(LY.unpack_base3(buf, n, k_up), codes)
+
+
+def test_base3_is_smaller_than_two_bit_fields():
+    from oracle import layout as LY
+    # 1.6 bits per code against 2: 20 % fewer bytes for whole chunks; Eq. 14's
+    # eta for OSR 2 at 1.6 bits is 20 %.
+    assert LY.packed_bytes_base3(64, 16000) * 10 == LY.packed_bytes(64, 16000, 3) * 8
+    assert LY.compression_ratio(1.6, 2.0) == 0.2
