@@ -64,6 +64,13 @@ typedef enum { SDQ_F16 = 0, SDQ_BF16 = 1, SDQ_F32 = 2 } sdq_dtype;
 typedef enum { SDQ_HAD_NONE = 0, SDQ_HAD_SYLVESTER = 1, SDQ_HAD_SIGNED = 2 } sdq_hadamard;
 
 /*
+ * Storage of the codes: SDQ_PACK_FIELDS (1-bit binary or 2-bit ternary
+ * fields, the default) or, for ternary codes, SDQ_PACK_BASE3 -- five codes per
+ * byte, 1.6 bits each (Eq. 14 counts a ternary code as log2(3) = 1.58 bits).
+ */
+typedef enum { SDQ_PACK_FIELDS = 0, SDQ_PACK_BASE3 = 1 } sdq_packing;
+
+/*
  * Geometry of one encoded linear layer (filled by sdq_layout_init; treat as
  * read-only).  Notation of the paper: the weight W has d_row = n rows and
  * d_col = k columns; Algorithm 1 splits the columns into blocks of B and
@@ -84,6 +91,8 @@ typedef struct sdq_layout {
   int32_t hadamard;        /* sdq_hadamard: the smoothing matrix Had             */
   uint32_t had_signs[8];   /* SDQ_HAD_SIGNED: bit t (word t/32, bit t%32) set    */
                            /* <=> s_t = -1, t < block; all zero otherwise        */
+  int32_t packing;         /* sdq_packing                                        */
+  int32_t reserved;
 } sdq_layout;
 
 /*
@@ -99,6 +108,11 @@ typedef struct sdq_layout {
  *  - binary field: 1 = +1, 0 = -1.  Ternary field: 00 = 0, 01 = +1, 11 = -1
  *    (10 is never written and reads as 0);
  *  - padding codes (j >= k_up) and padding rows (r >= n) are zero bits.
+ * SDQ_PACK_BASE3 (ternary only): codes_per_chunk = 80, and position q of a
+ * chunk is digit q % 5 of byte q / 5, a byte holding
+ * d0 + 3 d1 + 9 d2 + 27 d3 + 81 d4 with digit d = code + 1 (bytes 243..255 are
+ * never written); padding codes of real rows are code 0, padding rows zero
+ * bytes.  The chunk and panel layout is the same.
  * Total size: sdq_codes_bytes() = n_pad * n_chunks * 16 bytes.
  */
 
@@ -118,11 +132,20 @@ sdq_status sdq_layout_init(sdq_layout* out, int64_t n, int64_t k, double osr,
  * Errors: SDQ_ERR_ARG (layout NULL, bad mode, signs missing or not +-1). */
 sdq_status sdq_layout_set_hadamard(sdq_layout* layout, int32_t mode, const int8_t* signs_host);
 
+/* Select the code storage of a ternary layout (sdq_packing); recomputes
+ * codes_per_chunk (80 for SDQ_PACK_BASE3, 64 otherwise) and n_chunks.
+ * Decode of one activation row reads base-3 codes directly; other row counts
+ * first unpack them to 2-bit fields in the workspace (one extra pass over the
+ * codes per call, see sdq_linear_workspace_bytes).
+ * Errors: SDQ_ERR_ARG (layout NULL or not from sdq_layout_init, bad value),
+ * SDQ_ERR_LEVELS (base-3 for binary codes). */
+sdq_status sdq_layout_set_packing(sdq_layout* layout, int32_t packing);
+
 /* Bytes of the packed code buffer: n_pad * n_chunks * 16 (0 for a NULL layout). */
 size_t sdq_codes_bytes(const sdq_layout* layout);
 
 /* Compression ratio of Eq. 14, eta = bits * OSR / 16, using the stored bits
- * per code (1 or 2) and OSR = M / B. */
+ * per code (1, 2, or 1.6 for base-3 packing) and OSR = M / B. */
 double sdq_compression_ratio(const sdq_layout* layout);
 
 /* Device workspace (bytes) sdq_quantize needs for this layout: the rotated
@@ -203,7 +226,9 @@ sdq_status sdq_quantize_compensated(const float* w_dev, const sdq_layout* layout
  *                 rows in groups of four, per block in chunk slots), then the
  *                 fp32 plane scale of every (row, block);
  *   m > 16:       fp16 x_tilde, m x k_up rounded up to whole chunks (twice,
- *                 an fp16 pair hi + lo, for layouts with SDQ_HAD_NONE). */
+ *                 an fp16 pair hi + lo, for layouts with SDQ_HAD_NONE);
+ * for a base-3 layout and m > 1 the chunks are those of 2-bit fields, and the
+ * 2-bit copy of the codes follows (n_pad x ceil(k_up / 64) x 16 bytes). */
 size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
 
 /*

@@ -20,6 +20,7 @@ LIB_PATH = os.path.join(_HERE, "libsdq.so")
 SDQ_OK = 0
 SDQ_F16, SDQ_BF16, SDQ_F32 = 0, 1, 2
 SDQ_HAD_NONE, SDQ_HAD_SYLVESTER, SDQ_HAD_SIGNED = 0, 1, 2
+SDQ_PACK_FIELDS, SDQ_PACK_BASE3 = 0, 1
 
 STATUS_NAMES = {
     0: "SDQ_OK", -1: "SDQ_ERR_ARG", -2: "SDQ_ERR_SHAPE", -3: "SDQ_ERR_OSR", -4: "SDQ_ERR_LEVELS",
@@ -43,12 +44,13 @@ class sdq_layout(ctypes.Structure):
         ("n_pad", ctypes.c_int64), ("n_chunks", ctypes.c_int64),
         ("codes_per_chunk", ctypes.c_int32), ("hadamard", ctypes.c_int32),
         ("had_signs", ctypes.c_uint32 * 8),
+        ("packing", ctypes.c_int32), ("reserved", ctypes.c_int32),
     ]
 
     def __repr__(self):
         return (f"sdq_layout(n={self.n}, k={self.k}, block={self.block}, m_up={self.m_up}, "
                 f"levels={self.levels}, k_up={self.k_up}, n_pad={self.n_pad}, n_chunks={self.n_chunks}, "
-                f"hadamard={self.hadamard})")
+                f"hadamard={self.hadamard}, packing={self.packing})")
 
 
 def hip_runtimes_loaded() -> list:
@@ -74,6 +76,7 @@ def _load() -> ctypes.CDLL:
         "sdq_layout_init": (ctypes.c_int, [L, ctypes.c_int64, ctypes.c_int64, ctypes.c_double,
                                            ctypes.c_int32, ctypes.c_int32]),
         "sdq_layout_set_hadamard": (ctypes.c_int, [L, ctypes.c_int32, P]),
+        "sdq_layout_set_packing": (ctypes.c_int, [L, ctypes.c_int32]),
         "sdq_codes_bytes": (ctypes.c_size_t, [L]),
         "sdq_compression_ratio": (ctypes.c_double, [L]),
         "sdq_quantize_workspace_bytes": (ctypes.c_size_t, [L]),
@@ -158,6 +161,12 @@ def sdq_layout_set_hadamard(layout: sdq_layout, mode: int, signs=None) -> sdq_la
         buf = np.ascontiguousarray(signs, dtype=np.int8)
     _check(_lib.sdq_layout_set_hadamard(ctypes.byref(layout), int(mode),
                                         None if buf is None else buf.ctypes.data))
+    return layout
+
+
+def sdq_layout_set_packing(layout: sdq_layout, packing: int) -> sdq_layout:
+    """Select the code storage of a ternary layout (in place; also returned)."""
+    _check(_lib.sdq_layout_set_packing(ctypes.byref(layout), int(packing)))
     return layout
 
 
@@ -304,16 +313,21 @@ class Encoded:
 
 
 def quantize(w, osr: float, levels: int, block: int = 256, workspace=None, check: bool = True,
-             stream=None, hadamard: int = SDQ_HAD_SYLVESTER, signs=None) -> Encoded:
+             stream=None, hadamard: int = SDQ_HAD_SYLVESTER, signs=None,
+             packing: int = SDQ_PACK_FIELDS) -> Encoded:
     """Encode a device fp32 weight [n, k]; returns codes, scales and layout.
 
-    ``hadamard`` / ``signs`` choose Had (see sdq_layout_set_hadamard)."""
+    ``hadamard`` / ``signs`` choose Had (see sdq_layout_set_hadamard);
+    ``packing`` the code storage of a ternary layout (SDQ_PACK_BASE3: five
+    codes per byte)."""
     import torch
     if w.dtype != torch.float32 or not w.is_cuda or not w.is_contiguous():
         raise ValueError("w must be a contiguous fp32 device tensor")
     layout = sdq_layout_init(w.shape[0], w.shape[1], osr, levels, block)
     if hadamard != SDQ_HAD_SYLVESTER:
         sdq_layout_set_hadamard(layout, hadamard, signs)
+    if packing != SDQ_PACK_FIELDS:
+        sdq_layout_set_packing(layout, packing)
     codes = torch.empty(sdq_codes_bytes(layout), dtype=torch.uint8, device=w.device)
     scales = torch.empty(layout.n, dtype=torch.float32, device=w.device)
     need = sdq_quantize_workspace_bytes(layout)
@@ -337,7 +351,8 @@ def hessian_factor(h, lam: float, check: bool = True, stream=None):
 
 
 def quantize_compensated(w, osr: float, levels: int, u, block: int = 256, check: bool = True,
-                         stream=None, hadamard: int = SDQ_HAD_SYLVESTER, signs=None) -> Encoded:
+                         stream=None, hadamard: int = SDQ_HAD_SYLVESTER, signs=None,
+                         packing: int = SDQ_PACK_FIELDS) -> Encoded:
     """Encode a device fp32 weight [n, k] with Algorithm 1's block compensation (u: fp64 [k, k])."""
     import torch
     if w.dtype != torch.float32 or not w.is_cuda or not w.is_contiguous():
@@ -347,6 +362,8 @@ def quantize_compensated(w, osr: float, levels: int, u, block: int = 256, check:
     layout = sdq_layout_init(w.shape[0], w.shape[1], osr, levels, block)
     if hadamard != SDQ_HAD_SYLVESTER:
         sdq_layout_set_hadamard(layout, hadamard, signs)
+    if packing != SDQ_PACK_FIELDS:
+        sdq_layout_set_packing(layout, packing)
     codes = torch.empty(sdq_codes_bytes(layout), dtype=torch.uint8, device=w.device)
     scales = torch.empty(layout.n, dtype=torch.float32, device=w.device)
     ws = torch.empty(sdq_quantize_compensated_workspace_bytes(layout), dtype=torch.uint8, device=w.device)

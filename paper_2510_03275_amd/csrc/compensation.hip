@@ -353,8 +353,15 @@ sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, cons
   CompWs cw;
   comp_ws_layout(L, &cw, ws);
   const int64_t n = L->n, k = L->k, B = L->block, nb = L->nb, M = L->m_up;
+  // Base-3 layouts: every pass works on 2-bit fields in the workspace, which
+  // are repacked at the end.
+  const bool base3 = L->packing == SDQ_PACK_BASE3;
+  const sdq_layout Fv = fields_view(L);
+  const sdq_layout* F = &Fv;
+  void* fcodes = base3 ? static_cast<void*>(cw.q.codes2) : codes;
   // 1. The plain encoding: row scales of the raw W, and block 0's final codes.
-  sdq_status st = launch_quantize(w, L, T, codes, scales, cw.q, stream);
+  clear_rmax(cw.q, L, stream);
+  sdq_status st = launch_encode_blocks(w, k, 0, nb, F, T, fcodes, scales, cw.q, cw.q.rmax, cw.q.rmax, stream);
   if (st != SDQ_OK) return st;
   // 2. V_b = U_bb^-1 for every block: U_bb reversed is lower triangular;
   //    invert it (64-blocks, then the off-diagonal blocks) and reverse back.
@@ -373,13 +380,13 @@ sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, cons
     extract_block_kernel<<<grid1(n * B), 256, 0, stream>>>(cw.w64, n, k, static_cast<int>(B), b * B,
                                                            cw.wblk, cw.ebuf);
     if (b > 0) {
-      st = launch_encode_blocks(cw.wblk, B, b, 1, L, T, codes, scales, cw.q, cw.rmax_scratch,
+      st = launch_encode_blocks(cw.wblk, B, b, 1, F, T, fcodes, scales, cw.q, cw.rmax_scratch,
                                 cw.q.rmax, stream);
       if (st != SDQ_OK) return st;
     }
     if (b == nb - 1) break;
-    unpack_scaled_kernel<<<grid1(n * M), 256, 0, stream>>>(static_cast<const uint32_t*>(codes), scales, n,
-                                                           L->n_chunks, L->codes_per_chunk, L->bits,
+    unpack_scaled_kernel<<<grid1(n * M), 256, 0, stream>>>(static_cast<const uint32_t*>(fcodes), scales, n,
+                                                           F->n_chunks, F->codes_per_chunk, F->bits,
                                                            b * M, static_cast<int>(M), cw.cb);
     // E_b = W_b - (s C_b) E^T
     gemm64(n, B, M, -1.0, cw.cb, M, int64_t{1}, T->e64, int64_t{1}, M, 1.0, cw.ebuf, B, int64_t{1}, stream);
@@ -390,6 +397,10 @@ sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, cons
     const int64_t f0 = (b + 1) * B;
     gemm64(n, k - f0, B, -1.0, cw.gbuf, B, int64_t{1}, u + b * B * k + f0, k, int64_t{1}, 1.0, cw.w64 + f0, k,
            int64_t{1}, stream);
+  }
+  if (base3) {
+    st = launch_repack_base3(cw.q.codes2, L, codes, stream);
+    if (st != SDQ_OK) return st;
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "compensated encoder launch");

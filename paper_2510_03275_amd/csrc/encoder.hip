@@ -22,6 +22,8 @@
 // multiply-add may merge a product into a sum.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
+
 #include "sdq_internal.h"
 
 #pragma clang fp contract(off)
@@ -324,7 +326,74 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
   }
 }
 
+// One thread per byte of the base-3 buffer (in buffer order: panel, chunk,
+// row of the panel, byte): five codes of the 2-bit fields -> d0 + 3 d1 + ...
+// + 81 d4 with d = code + 1; codes past k_up are code 0, rows past n zero bytes.
+__global__ void repack_base3_kernel(const uint32_t* __restrict__ fields, int64_t n, int64_t k_up,
+                                    int64_t nch2, int64_t nch3, int64_t total, uint8_t* __restrict__ out) {
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int byte = static_cast<int>(e % kChunkBytes);
+    const int64_t rr = (e / kChunkBytes) % kPanel;
+    const int64_t c = (e / (kChunkBytes * kPanel)) % nch3;
+    const int64_t r = (e / (kChunkBytes * kPanel * nch3)) * kPanel + rr;
+    uint32_t v = 0, pw = 1;
+    if (r < n) {
+      for (int i = 0; i < 5; ++i, pw *= 3) {
+        const int64_t j = c * kBase3PerChunk + 5 * byte + i;
+        int code = 0;
+        if (j < k_up) {
+          const int64_t c2 = j / 64;
+          const int q = static_cast<int>(j % 64);
+          const uint32_t word = fields[(((r / kPanel) * nch2 + c2) * kPanel + rr) * 4 + q / 16];
+          const uint32_t f = (word >> (2 * (q % 16))) & 3u;
+          code = f == 1u ? 1 : (f == 3u ? -1 : 0);
+        }
+        v += static_cast<uint32_t>(code + 1) * pw;
+      }
+    }
+    out[e] = static_cast<uint8_t>(v);
+  }
+}
+
+// One thread per 32-bit word of the 2-bit fields (16 codes): each code's
+// base-3 digit d gives the field of code d - 1 (00: 0, 01: +1, 11: -1).
+__global__ void unpack_base3_kernel(const uint8_t* __restrict__ b3, int64_t k_up, int64_t nch2,
+                                    int64_t nch3, int64_t total_words, uint32_t* __restrict__ fields) {
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total_words;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int wd = static_cast<int>(e % 4);
+    const int64_t rr = (e / 4) % kPanel;
+    const int64_t c2 = (e / (4 * kPanel)) % nch2;
+    const int64_t pn = e / (4 * kPanel * nch2);
+    const uint8_t* rowp = b3 + (pn * nch3 * kPanel + rr) * kChunkBytes;   // chunk 0 of this row
+    uint32_t word = 0;
+    for (int i = 0; i < 16; ++i) {
+      const int64_t j = c2 * 64 + wd * 16 + i;
+      if (j >= k_up) break;
+      const int64_t c3 = j / kBase3PerChunk;
+      const int q = static_cast<int>(j % kBase3PerChunk);
+      uint32_t v = rowp[c3 * kPanel * kChunkBytes + q / 5];
+      for (int t = 0; t < q % 5; ++t) v /= 3u;
+      const uint32_t d = v % 3u;
+      word |= (d == 2u ? 1u : (d == 0u ? 3u : 0u)) << (2 * i);
+    }
+    fields[e] = word;
+  }
+}
+
 }  // namespace
+
+sdq_status launch_unpack_base3(const void* codes, const sdq_layout* L, uint32_t* fields, hipStream_t stream) {
+  const sdq_layout F = fields_view(L);
+  const int64_t words = F.n_pad * F.n_chunks * (kChunkBytes / 4);
+  const unsigned grid = static_cast<unsigned>(std::min<int64_t>((words + 255) / 256, 16384));
+  unpack_base3_kernel<<<grid, 256, 0, stream>>>(static_cast<const uint8_t*>(codes), L->k_up, F.n_chunks,
+                                                L->n_chunks, words, fields);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "base-3 unpack launch");
+  return SDQ_OK;
+}
 
 sdq_status launch_encode_blocks(const float* w, int64_t ldw, int64_t b0, int64_t nbl,
                                 const sdq_layout* L, const Tables* T, void* codes, float* scales,
@@ -370,11 +439,32 @@ sdq_status launch_encode_blocks(const float* w, int64_t ldw, int64_t b0, int64_t
   return SDQ_OK;
 }
 
-sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
-                           float* scales, const QuantWs& ws, hipStream_t stream) {
+void clear_rmax(const QuantWs& ws, const sdq_layout* L, hipStream_t stream) {
   clear_kernel<<<dim3(static_cast<unsigned>((L->n_pad + 255) / 256)), dim3(256), 0, stream>>>(
       ws.flag, ws.rmax, L->n_pad);
-  return launch_encode_blocks(w, L->k, 0, L->nb, L, T, codes, scales, ws, ws.rmax, ws.rmax, stream);
+}
+
+sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
+                           float* scales, const QuantWs& ws, hipStream_t stream) {
+  clear_rmax(ws, L, stream);
+  if (L->packing != SDQ_PACK_BASE3)
+    return launch_encode_blocks(w, L->k, 0, L->nb, L, T, codes, scales, ws, ws.rmax, ws.rmax, stream);
+  // Base-3: scan into 2-bit fields in the workspace, then repack.
+  const sdq_layout F = fields_view(L);
+  sdq_status st = launch_encode_blocks(w, L->k, 0, L->nb, &F, T, ws.codes2, scales, ws, ws.rmax, ws.rmax, stream);
+  if (st != SDQ_OK) return st;
+  return launch_repack_base3(ws.codes2, L, codes, stream);
+}
+
+sdq_status launch_repack_base3(const uint32_t* fields, const sdq_layout* L, void* codes, hipStream_t stream) {
+  const sdq_layout F = fields_view(L);
+  const int64_t total = L->n_pad * L->n_chunks * kChunkBytes;
+  const unsigned grid = static_cast<unsigned>(std::min<int64_t>((total + 255) / 256, 16384));
+  repack_base3_kernel<<<grid, 256, 0, stream>>>(fields, L->n, L->k_up, F.n_chunks, L->n_chunks, total,
+                                                static_cast<uint8_t*>(codes));
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "base-3 repack launch");
+  return SDQ_OK;
 }
 
 }  // namespace sdq

@@ -518,6 +518,109 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
   }
 }
 
+// Base-3 codes (one activation row): byte p of a chunk holds codes 5p .. 5p+4
+// as b = sum_i (c_i + 1) 3^i.  Per byte two tables: 27 entries for its first
+// three codes and 9 for its last two; a lookup splits b = lo + 27 hi with
+// hi = (19 b) >> 9 (exact for b < 243).  Each table spans at most 27
+// consecutive words, so a wave's reads of one table hit distinct banks or
+// the same word.  Otherwise as the 2-bit table GEMV: loads first, tables of
+// the segment shared by four panels, one wave per panel.
+template <int SEG>
+__global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
+    const uint4* __restrict__ codes, const float* __restrict__ scales,
+    const float* __restrict__ xt, int64_t n, int64_t n_panels, int64_t n_chunks, int64_t k_up_pad,
+    int n_segs, int segs_fast, int accumulate, float* __restrict__ y) {
+  constexpr int kBytes = 16;                   // groups of five codes per chunk
+  constexpr int kGF = 36;                      // table floats per group: 27 + 9
+  constexpr int kGroups = SEG * kBytes;
+  constexpr int kThreads = 64 * kGemvWaves;
+  static_assert(2 * kGroups <= kThreads, "one table per thread at most");
+  static_assert(kGroups * kGF * 4 <= 65536, "table offsets fit the LDS immediate");
+  __shared__ __attribute__((aligned(16))) float lut[kGroups * kGF];
+
+  const int tid = threadIdx.x;
+  const int lane = tid % 64;
+  const int wave = tid / 64;
+  const int64_t panel = static_cast<int64_t>(segs_fast ? blockIdx.y : blockIdx.x) * kGemvWaves + wave;
+  const bool panel_ok = panel < n_panels;
+  const int seg = segs_fast ? blockIdx.x : blockIdx.y;
+  const int64_t c0 = static_cast<int64_t>(seg) * SEG;
+  const int nch = static_cast<int>(min<int64_t>(SEG, n_chunks - c0));
+  const int64_t code0 = c0 * kBase3PerChunk;
+
+  // 1. Loads.  Threads [0, kGroups) build the 27-entry tables, threads
+  //    [kGroups, 2 kGroups) the 9-entry ones.
+  const bool is_lo = tid < kGroups;
+  const int g = is_lo ? tid : tid - kGroups;
+  const bool gok = tid < 2 * kGroups && g < nch * kBytes;
+  float xs[3] = {0.f, 0.f, 0.f};
+  if (gok) {
+    const float* xp = xt + code0 + 5 * g + (is_lo ? 0 : 3);
+    xs[0] = xp[0];
+    xs[1] = xp[1];
+    if (is_lo) xs[2] = xp[2];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  uint4 q[SEG];
+  {
+    const uint4* src = codes + ((panel_ok ? panel : n_panels - 1) * n_chunks + c0) * kPanel + lane;
+#pragma unroll
+    for (int j = 0; j < SEG; ++j) q[j] = src[static_cast<int64_t>(min(j, nch - 1)) * kPanel];
+  }
+  __builtin_amdgcn_sched_barrier(0);
+
+  // 2. Tables: entry a + 3 b (+ 9 c) = (a - 1) x0 + (b - 1) x1 (+ (c - 1) x2).
+  if (tid < 2 * kGroups) {
+    float* dst = lut + g * kGF + (is_lo ? 0 : 27);
+    float t9[9];
+#pragma unroll
+    for (int b = 0; b < 3; ++b)
+#pragma unroll
+      for (int a = 0; a < 3; ++a) t9[a + 3 * b] = static_cast<float>(a - 1) * xs[0] + static_cast<float>(b - 1) * xs[1];
+    if (is_lo) {
+#pragma unroll
+      for (int c = 0; c < 3; ++c)
+#pragma unroll
+        for (int e = 0; e < 9; ++e) dst[9 * c + e] = t9[e] + static_cast<float>(c - 1) * xs[2];
+    } else {
+#pragma unroll
+      for (int e = 0; e < 9; ++e) dst[e] = t9[e];
+    }
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  __syncthreads();
+
+  // 3. Lookups: two per byte.
+  float acc = 0.0f;
+#pragma unroll
+  for (int c = 0; c < SEG; ++c) {
+    const uint32_t words[4] = {q[c].x, q[c].y, q[c].z, q[c].w};
+#pragma unroll
+    for (int wi = 0; wi < 4; ++wi) {
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const uint32_t b = (words[wi] >> (8 * k)) & 255u;
+        const uint32_t hi = (b * 19u) >> 9;
+        const uint32_t lo = b - 27u * hi;
+        const float* tg = lut + (c * kBytes + wi * 4 + k) * kGF;
+        acc += tg[lo];
+        acc += tg[27 + hi];
+      }
+      asm volatile("" : "+v"(acc));
+    }
+  }
+
+  // 4. Scale and write (as the 2-bit table GEMV).
+  const int64_t r = panel * kPanel + lane;
+#pragma unroll
+  for (int c = 0; c < SEG; ++c) asm volatile("" ::"v"(q[c].x));
+  if (!panel_ok || r >= n) return;
+  const float s = scales[r];
+  if (n_segs > 1) unsafeAtomicAdd(&y[r], acc * s);
+  else y[r] = accumulate ? y[r] + acc * s : acc * s;
+  (void)k_up_pad;
+}
+
 int round_mr(int64_t m) {
   if (m <= 1) return 1;
   if (m <= 2) return 2;
@@ -696,6 +799,20 @@ void launch_gemv_seg(const DecodeWs& w, const void* codes, const float* scales, 
       accumulate ? 1 : 0, y);
 }
 
+template <int SEG>
+void launch_gemv_base3_seg(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
+                           float* y, bool accumulate, hipStream_t stream) {
+  const int64_t n_panels = L->n_pad / kPanel;
+  const int n_segs = segs_for(L, SEG);
+  const unsigned pgroups = static_cast<unsigned>((n_panels + kGemvWaves - 1) / kGemvWaves);
+  const bool segs_fast = static_cast<int64_t>(pgroups) * n_segs > 2048;
+  const dim3 grid = segs_fast ? dim3(static_cast<unsigned>(n_segs), pgroups)
+                              : dim3(pgroups, static_cast<unsigned>(n_segs));
+  gemv_lut_base3_kernel<SEG><<<grid, dim3(64 * kGemvWaves), 0, stream>>>(
+      static_cast<const uint4*>(codes), scales, w.xt, L->n, n_panels, L->n_chunks,
+      L->n_chunks * L->codes_per_chunk, n_segs, segs_fast ? 1 : 0, accumulate ? 1 : 0, y);
+}
+
 template <int MR, int LEVELS>
 void launch_gemv_mr(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
                     int64_t m, float* y, bool acc, hipStream_t stream) {
@@ -728,6 +845,10 @@ size_t decode_ws_bytes(const sdq_layout* L, int64_t m) { return carve(L, m, null
 sdq_status decode_supported(const sdq_layout* L) {
   (void)L;
   return SDQ_OK;
+}
+
+bool decode_reads_base3(const sdq_layout* L, int64_t m) {
+  return L->packing == SDQ_PACK_BASE3 && m == 1 && !use_mfma(L, m);
 }
 
 bool decode_needs_zero_y(const sdq_layout* L, int64_t m) {
@@ -792,7 +913,14 @@ sdq_status launch_decode_contract(int64_t m, const void* codes, const float* sca
     const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 4096));
     fill_zero_kernel<<<dim3(blocks), dim3(256), 0, stream>>>(y, count);
   }
-  if (use_mfma(L, m)) {
+  if (L->packing == SDQ_PACK_BASE3) {
+    if (!decode_reads_base3(L, m)) return set_error(SDQ_ERR_ARG, "base-3 codes need unpacking on this path");
+    switch (pick_seg(L, 1)) {
+      case 8: launch_gemv_base3_seg<8>(w, codes, scales, L, y, accumulate, stream); break;
+      case 4: launch_gemv_base3_seg<4>(w, codes, scales, L, y, accumulate, stream); break;
+      default: launch_gemv_base3_seg<2>(w, codes, scales, L, y, accumulate, stream); break;
+    }
+  } else if (use_mfma(L, m)) {
     if (L->levels == 2) launch_mfma_levels<2>(w, codes, scales, L, m, y, accumulate, stream);
     else launch_mfma_levels<3>(w, codes, scales, L, m, y, accumulate, stream);
   } else if (L->levels == 2) {

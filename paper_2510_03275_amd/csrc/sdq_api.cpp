@@ -205,7 +205,9 @@ static sdq_status check_layout(const sdq_layout* L) {
       (L->levels != 2 && L->levels != 3) || L->m_up < L->block || L->m_up % 32 ||
       L->nb != L->k / L->block || L->k_up != L->nb * L->m_up ||
       L->bits != (L->levels == 2 ? 1 : 2) ||
-      L->codes_per_chunk != kChunkBytes * 8 / L->bits ||
+      (L->packing != SDQ_PACK_FIELDS && L->packing != SDQ_PACK_BASE3) ||
+      (L->packing == SDQ_PACK_BASE3 && L->levels != 3) ||
+      L->codes_per_chunk != (L->packing == SDQ_PACK_BASE3 ? kBase3PerChunk : kChunkBytes * 8 / L->bits) ||
       L->n_chunks != (L->k_up + L->codes_per_chunk - 1) / L->codes_per_chunk ||
       L->n_pad != (L->n + kPanel - 1) / kPanel * kPanel || !valid_hadamard(L))
     return set_error(SDQ_ERR_ARG, "layout is not one produced by sdq_layout_init");
@@ -226,6 +228,7 @@ size_t quant_ws_layout(const sdq_layout* L, QuantWs* ws, void* base) {
   const size_t rows = static_cast<size_t>(quant_ws_rows(L));
   w.v = reinterpret_cast<float*>(take(rows * L->k * 4));
   w.xup = reinterpret_cast<float*>(take(rows * L->k_up * 4));
+  w.codes2 = L->packing == SDQ_PACK_BASE3 ? reinterpret_cast<uint32_t*>(take(fields_codes_bytes(L))) : nullptr;
   if (ws) *ws = w;
   return off;
 }
@@ -291,6 +294,21 @@ sdq_status sdq_layout_init(sdq_layout* out, int64_t n, int64_t k, double osr, in
   return SDQ_OK;
 }
 
+sdq_status sdq_layout_set_packing(sdq_layout* L, int32_t packing) {
+  if (!L) return set_error(SDQ_ERR_ARG, "layout is NULL");
+  if (packing != SDQ_PACK_FIELDS && packing != SDQ_PACK_BASE3)
+    return set_error(SDQ_ERR_ARG, "packing %d is not SDQ_PACK_FIELDS or SDQ_PACK_BASE3", packing);
+  if (packing == SDQ_PACK_BASE3 && L->levels != 3)
+    return set_error(SDQ_ERR_LEVELS, "base-3 packing needs ternary codes");
+  sdq_layout T = *L;
+  T.packing = packing;
+  T.codes_per_chunk = packing == SDQ_PACK_BASE3 ? kBase3PerChunk : kChunkBytes * 8 / T.bits;
+  T.n_chunks = (T.k_up + T.codes_per_chunk - 1) / T.codes_per_chunk;
+  if (check_layout(&T) != SDQ_OK) return set_error(SDQ_ERR_ARG, "layout is not one produced by sdq_layout_init");
+  *L = T;
+  return SDQ_OK;
+}
+
 sdq_status sdq_layout_set_hadamard(sdq_layout* L, int32_t mode, const int8_t* signs) {
   if (!L) return set_error(SDQ_ERR_ARG, "layout is NULL");
   if (mode != SDQ_HAD_NONE && mode != SDQ_HAD_SYLVESTER && mode != SDQ_HAD_SIGNED)
@@ -316,7 +334,8 @@ size_t sdq_codes_bytes(const sdq_layout* L) {
 
 double sdq_compression_ratio(const sdq_layout* L) {
   if (!L || !L->block) return 0.0;
-  return L->bits * (static_cast<double>(L->m_up) / L->block) / 16.0;
+  const double bits = L->packing == SDQ_PACK_BASE3 ? 1.6 : static_cast<double>(L->bits);
+  return bits * (static_cast<double>(L->m_up) / L->block) / 16.0;
 }
 
 size_t sdq_quantize_workspace_bytes(const sdq_layout* L) {
@@ -408,10 +427,27 @@ sdq_status sdq_quantize_compensated(const float* w, const sdq_layout* L, const d
   return launch_quantize_compensated(w, L, T, u, codes, scales, ws, static_cast<hipStream_t>(stream));
 }
 
+// The layout a linear path reads: base-3 codes are read as stored by the
+// one-row table GEMV and unpacked to 2-bit fields (into the workspace, after
+// the path's own part) for every other path.
+static bool needs_unpack(const sdq_layout* L, int64_t m) {
+  return L->packing == SDQ_PACK_BASE3 && !(m <= 16 && decode_reads_base3(L, m));
+}
+
+static size_t path_ws_bytes(const sdq_layout* P, int64_t m) {
+  return m <= 16 ? decode_ws_bytes(P, m) : prefill_ws_bytes(P, m);
+}
+
+static size_t linear_ws_bytes(const sdq_layout* L, int64_t m) {
+  if (!needs_unpack(L, m)) return path_ws_bytes(L, m);
+  const sdq_layout F = fields_view(L);
+  return align_up(path_ws_bytes(&F, m), 256) + fields_codes_bytes(L);
+}
+
 size_t sdq_linear_workspace_bytes(const sdq_layout* L, int64_t m) {
   if (check_layout(L) != SDQ_OK || m < 0) return 0;
   if (m == 0) return 0;
-  return m <= 16 ? decode_ws_bytes(L, m) : prefill_ws_bytes(L, m);
+  return linear_ws_bytes(L, m);
 }
 
 static sdq_status linear_common(const sdq_layout* L, int64_t m, size_t ws_bytes, const void* ws) {
@@ -423,7 +459,7 @@ static sdq_status linear_common(const sdq_layout* L, int64_t m, size_t ws_bytes,
     st = decode_supported(L);
     if (st != SDQ_OK) return st;
   }
-  const size_t need = m <= 16 ? decode_ws_bytes(L, m) : prefill_ws_bytes(L, m);
+  const size_t need = linear_ws_bytes(L, m);
   if (!ws || ws_bytes < need)
     return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
   return SDQ_OK;
@@ -433,12 +469,14 @@ static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_
                               void* ws, float* y_zero, void* stream) {
   if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
   if (!x) return set_error(SDQ_ERR_ARG, "x is NULL");
+  const sdq_layout F = fields_view(L);
+  const sdq_layout* P = needs_unpack(L, m) ? &F : L;
   const Tables* T = nullptr;
-  sdq_status st = get_tables(L, &T);
+  sdq_status st = get_tables(P, &T);
   if (st != SDQ_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return m <= 16 ? launch_decode_expand(x, xt, m, L, T, ws, y_zero, s)
-                 : launch_prefill_expand(x, xt, m, L, T, ws, s);
+  return m <= 16 ? launch_decode_expand(x, xt, m, P, T, ws, y_zero, s)
+                 : launch_prefill_expand(x, xt, m, P, T, ws, s);
 }
 
 static sdq_status contract_impl(int64_t m, const void* codes, const float* scales,
@@ -446,8 +484,17 @@ static sdq_status contract_impl(int64_t m, const void* codes, const float* scale
                                 bool y_ready, void* stream) {
   if (!codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return m <= 16 ? launch_decode_contract(m, codes, scales, L, y, accumulate, ws, y_ready, s)
-                 : launch_prefill_contract(m, codes, scales, L, y, accumulate, ws, s);
+  const sdq_layout F = fields_view(L);
+  const sdq_layout* P = L;
+  if (needs_unpack(L, m)) {
+    P = &F;
+    uint32_t* fields = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + align_up(path_ws_bytes(P, m), 256));
+    sdq_status st = launch_unpack_base3(codes, L, fields, s);
+    if (st != SDQ_OK) return st;
+    codes = fields;
+  }
+  return m <= 16 ? launch_decode_contract(m, codes, scales, P, y, accumulate, ws, y_ready, s)
+                 : launch_prefill_contract(m, codes, scales, P, y, accumulate, ws, s);
 }
 
 sdq_status sdq_expand_activations(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
@@ -477,7 +524,9 @@ sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
   st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK) return st;
   // Decode: the expansion also zeroes y when the GEMV will add into it.
-  const bool zero_in_expand = !accumulate && m <= 16 && decode_needs_zero_y(L, m);
+  const sdq_layout F = fields_view(L);
+  const sdq_layout* P = needs_unpack(L, m) ? &F : L;
+  const bool zero_in_expand = !accumulate && m <= 16 && decode_needs_zero_y(P, m);
   st = expand_impl(x, xt, m, L, ws, zero_in_expand ? y : nullptr, stream);
   if (st != SDQ_OK) return st;
   return contract_impl(m, codes, scales, L, y, accumulate != 0, ws, true, stream);
@@ -596,6 +645,18 @@ sdq_status sdq_unpack_codes(const sdq_layout* L, const void* codes_host, int8_t*
   sdq_status st = check_layout(L);
   if (st != SDQ_OK) return st;
   if (L->n > 0 && (!codes_host || !out)) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+  if (L->packing == SDQ_PACK_BASE3) {
+    const uint8_t* bytes = static_cast<const uint8_t*>(codes_host);
+    for (int64_t r = 0; r < L->n; ++r)
+      for (int64_t j = 0; j < L->k_up; ++j) {
+        const int64_t c = j / kBase3PerChunk, q = j % kBase3PerChunk;
+        const int64_t chunk = ((r / kPanel) * L->n_chunks + c) * kPanel + (r % kPanel);
+        int v = bytes[chunk * kChunkBytes + q / 5];
+        for (int i = 0; i < q % 5; ++i) v /= 3;
+        out[r * L->k_up + j] = static_cast<int8_t>(v % 3 - 1);
+      }
+    return SDQ_OK;
+  }
   const uint32_t* words = static_cast<const uint32_t*>(codes_host);
   const int bits = L->bits;
   const int per_word = 32 / bits;

@@ -12,6 +12,23 @@ namespace sdq {
 
 constexpr int kPanel = 64;        // rows per panel of the packed format
 constexpr int kChunkBytes = 16;   // bytes per chunk of the packed format
+constexpr int kBase3PerChunk = 80; // ternary codes per chunk with base-3 packing
+
+// The same layout with 2-bit ternary fields (base-3 layouts are unpacked to
+// it for the paths that read 2-bit fields).
+inline sdq_layout fields_view(const sdq_layout* L) {
+  sdq_layout F = *L;
+  if (F.packing == SDQ_PACK_BASE3) {
+    F.packing = SDQ_PACK_FIELDS;
+    F.codes_per_chunk = kChunkBytes * 8 / F.bits;
+    F.n_chunks = (F.k_up + F.codes_per_chunk - 1) / F.codes_per_chunk;
+  }
+  return F;
+}
+inline size_t fields_codes_bytes(const sdq_layout* L) {
+  const sdq_layout F = fields_view(L);
+  return static_cast<size_t>(F.n_pad) * F.n_chunks * kChunkBytes;
+}
 
 // Device coefficient tables for one (block, M, Had) choice on one device.
 struct Tables {
@@ -57,12 +74,20 @@ struct QuantWs {
   uint32_t* rmax;    // [n_pad] row maxima as fp32 bit patterns
   float* v;          // [nb][B][n_ws] rotated weights, rows contiguous
   float* xup;        // [n_ws / 64][k_up][64] upsampled samples
+  uint32_t* codes2;  // base-3 layouts: the codes as 2-bit fields before repacking (else null)
 };
 inline int64_t quant_ws_rows(const sdq_layout* L) { return (L->n + 127) / 128 * 128; }
 size_t quant_ws_layout(const sdq_layout* L, QuantWs* ws, void* base);
 
+// Zeroes the non-finite flag and the row maxima of ws.
+void clear_rmax(const QuantWs& ws, const sdq_layout* L, hipStream_t stream);
 sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T, void* codes,
                            float* scales, const QuantWs& ws, hipStream_t stream);
+// Base-3 bytes of a ternary layout L from its codes as 2-bit fields (the
+// layout fields_view(L)).
+sdq_status launch_repack_base3(const uint32_t* fields, const sdq_layout* L, void* codes, hipStream_t stream);
+// The inverse: 2-bit fields (fields_view(L)) from base-3 codes.
+sdq_status launch_unpack_base3(const void* codes, const sdq_layout* L, uint32_t* fields, hipStream_t stream);
 // Encode blocks b0 .. b0 + nbl - 1 from w (row stride ldw; column 0 of w is the
 // first column of block b0): rotate and upsample fold their row maxima into
 // rmax_acc, the scan uses the row scales in rmax_scale (one buffer for a plain
@@ -79,6 +104,9 @@ sdq_status decode_supported(const sdq_layout* L);
 // at zero (or hold the values to accumulate onto): the expansion zeroes it if
 // handed y (y_zero), else the GEMV launch does unless y_ready is set.
 bool decode_needs_zero_y(const sdq_layout* L, int64_t m);
+// Whether the decode path reads base-3 codes as stored (one activation row,
+// table GEMV); every other path reads them unpacked to fields_view(L).
+bool decode_reads_base3(const sdq_layout* L, int64_t m);
 sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
                                 const Tables* T, void* ws, float* y_zero, hipStream_t stream);
 // accumulate: y += result instead of y = result.

@@ -34,8 +34,9 @@ def test_every_declared_symbol_is_exported():
 
 
 def test_layout_struct_size_matches_header():
-    assert ctypes.sizeof(Bd.sdq_layout) == 104
+    assert ctypes.sizeof(Bd.sdq_layout) == 112
     assert Bd.sdq_layout.hadamard.offset == 68 and Bd.sdq_layout.had_signs.offset == 72
+    assert Bd.sdq_layout.packing.offset == 104
 
 
 def test_layout_hadamard_choice():
@@ -158,6 +159,38 @@ def test_unpack_matches_oracle_packer(levels, n, k, osr):
     codes = rng.choice(vals, size=(n, L.k_up)).astype(np.int8)
     buf = LY.pack(codes, levels)
     assert np.array_equal(P.sdq_unpack_codes(L, buf), codes)
+
+
+@pytest.mark.parametrize("n,k,osr", [(1, 256, 2.0), (65, 512, 1.5), (130, 768, 2.5), (3, 512, 1.625),
+                                     (64, 1024, 2.0)])
+def test_unpack_base3_matches_oracle_packer(n, k, osr):
+    L = P.sdq_layout_set_packing(P.sdq_layout_init(n, k, osr, 3), P.SDQ_PACK_BASE3)
+    n_pad, n_chunks = LY.geometry_base3(n, L.k_up)
+    assert (L.packing, L.codes_per_chunk, L.n_chunks, L.n_pad) == (1, 80, n_chunks, n_pad)
+    assert P.sdq_codes_bytes(L) == LY.packed_bytes_base3(n, L.k_up)
+    rng = np.random.default_rng(n * 11 + k)
+    codes = rng.choice([-1, 0, 1], size=(n, L.k_up)).astype(np.int8)
+    assert np.array_equal(P.sdq_unpack_codes(L, LY.pack_base3(codes)), codes)
+
+
+def test_layout_packing_choice_and_rejects():
+    L = P.sdq_layout_init(8, 512, 2.0, 3)
+    assert (L.packing, L.codes_per_chunk, L.n_chunks) == (0, 64, 16)
+    P.sdq_layout_set_packing(L, P.SDQ_PACK_BASE3)
+    assert (L.packing, L.codes_per_chunk, L.n_chunks) == (1, 80, 13)
+    assert abs(P.sdq_compression_ratio(L) - 1.6 * 2.0 / 16) < 1e-15
+    P.sdq_layout_set_packing(L, P.SDQ_PACK_FIELDS)
+    assert (L.packing, L.codes_per_chunk, L.n_chunks) == (0, 64, 16)
+    Lb = P.sdq_layout_init(8, 512, 2.0, 2)
+    with pytest.raises(P.SdqError) as ei:
+        P.sdq_layout_set_packing(Lb, P.SDQ_PACK_BASE3)      # base-3 holds ternary codes only
+    assert ei.value.status == -4 and Lb.packing == 0
+    with pytest.raises(P.SdqError):
+        P.sdq_layout_set_packing(L, 7)
+    Lt = P.sdq_layout_init(8, 512, 2.0, 3)
+    Lt.packing = 1                                          # tampered: chunk geometry still 2-bit
+    assert P.lib().sdq_quantize_workspace_bytes(ctypes.byref(Lt)) == 0
+    assert P.lib().sdq_linear_workspace_bytes(ctypes.byref(Lt), 1) == 0
 
 
 @pytest.mark.parametrize("seed", range(8))
