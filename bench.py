@@ -156,12 +156,13 @@ def bench_decode(torch, P, synth, SG, steps: int, warmup: int):
                 ms_step=ms_step, ms_gemv=ms_gemv, ms_expand=ms_exp, wl=wl, lin=lin)
 
 
-def bench_decode_70b(torch, P, synth, SG, replays: int = 20):
-    """Decode at m = 1 on the LLaMA-70B up_proj shape (28672 x 8192, OSR 2, ternary)."""
+def bench_decode_70b(torch, P, synth, SG, replays: int = 20, base3: bool = False):
+    """Decode at m = 1 on the LLaMA-70B up_proj shape (28672 x 8192, OSR 2, ternary),
+    codes as 2-bit fields or base-3 bytes (1.6 bits per code)."""
     wl = synth.workload(4)
     lin = wl.linears[1]
     w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
-    enc = P.quantize(w, wl.osr, wl.levels)
+    enc = P.quantize(w, wl.osr, wl.levels, packing=P.SDQ_PACK_BASE3 if base3 else P.SDQ_PACK_FIELDS)
     del w
     L = enc.layout
     nbytes = P.sdq_codes_bytes(L)
@@ -179,13 +180,16 @@ def bench_decode_70b(torch, P, synth, SG, replays: int = 20):
     del codes
     torch.cuda.empty_cache()
     gemv_gbs = nbytes / (ms_gemv * 1e-3) / 1e9
-    return {"workload": "llama70b_up_proj_28672x8192_osr2_ternary_decode_m1_bf16",
+    kernel = "gemv_lut_base3_kernel<4>" if base3 else "gemv_lut_kernel<1,3,4>"
+    return {"workload": "llama70b_up_proj_28672x8192_osr2_ternary_decode_m1_bf16"
+                        + ("_base3" if base3 else ""),
             "gbs": nbytes / (ms_step * 1e-3) / 1e9, "ms": ms_step, "ms_gemv": ms_gemv,
-            "code_bytes": nbytes, "rotating_code_buffers": rot,
+            "gweights_per_s": lin.n * lin.k / (ms_step * 1e-3) / 1e9,
+            "code_bytes": nbytes, "bits_per_code": 8.0 * nbytes / (L.n_pad * L.k_up),
+            "rotating_code_buffers": rot,
             "roofline": {"bound": "hbm", "achieved": gemv_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": gemv_gbs / HBM_PEAK_GBS,
-                         "traffic": traffic_bytes("gemv_lut_kernel<1,3,4>"),
-                         "kernel": "gemv_lut_kernel<1,3,4>"}}
+                         "traffic": traffic_bytes(kernel), "kernel": kernel}}
 
 
 def bench_encoder(torch, P, w, wl, reps: int = 5):
@@ -526,7 +530,8 @@ def cpu_baseline(synth, dec, budget_s: float = 12.0):
 def traffic_probe(torch, P, synth, SG) -> None:
     """A short eager run for hardware-counter passes: one 256 MiB device copy of
     known size (to scale FETCH_SIZE / WRITE_SIZE), then four launches each of
-    the headline GEMV, the 70B up_proj GEMV and the prefill GEMM (their
+    the headline GEMV, the 70B up_proj GEMV (2-bit and base-3 codes) and the
+    prefill GEMM (their
     expansions run once before).  Prints what it ran; the counters come from
     rocprofv3 --pmc around this process."""
     nbytes = 256 << 20
@@ -537,13 +542,15 @@ def traffic_probe(torch, P, synth, SG) -> None:
     torch.cuda.synchronize()
     del a, b
     print(f"copy: {nbytes} bytes", flush=True)
-    for wl_i, lin_i, m, xdt, label in ((2, 0, 1, torch.float16, "headline down_proj m=1"),
-                                       (4, 1, 1, torch.bfloat16, "70B up_proj m=1"),
-                                       (4, 0, 2048, torch.bfloat16, "70B 8192x8192 m=2048")):
+    for wl_i, lin_i, m, xdt, b3, label in (
+            (2, 0, 1, torch.float16, False, "headline down_proj m=1"),
+            (4, 1, 1, torch.bfloat16, False, "70B up_proj m=1"),
+            (4, 1, 1, torch.bfloat16, True, "70B up_proj m=1 base-3"),
+            (4, 0, 2048, torch.bfloat16, False, "70B 8192x8192 m=2048")):
         wl = synth.workload(wl_i)
         lin = wl.linears[lin_i]
         w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
-        enc = P.quantize(w, wl.osr, wl.levels)
+        enc = P.quantize(w, wl.osr, wl.levels, packing=P.SDQ_PACK_BASE3 if b3 else P.SDQ_PACK_FIELDS)
         del w
         L = enc.layout
         x = SG.activations_gpu(wl.seed, 5, m, lin.k).to(xdt)
@@ -627,6 +634,7 @@ def main() -> int:
         torch.cuda.empty_cache()
         line["phases"] = {"encoder": enc_ph,
                           "decode_70b": bench_decode_70b(torch, P, synth, SG),
+                          "decode_70b_base3": bench_decode_70b(torch, P, synth, SG, base3=True),
                           "prefill": bench_prefill(torch, P, synth, SG),
                           "multiosr": bench_multiosr(torch, P, synth, SG)}
         try:

@@ -108,11 +108,14 @@ typedef struct sdq_layout {
  *  - binary field: 1 = +1, 0 = -1.  Ternary field: 00 = 0, 01 = +1, 11 = -1
  *    (10 is never written and reads as 0);
  *  - padding codes (j >= k_up) and padding rows (r >= n) are zero bits.
- * SDQ_PACK_BASE3 (ternary only): codes_per_chunk = 80, and position q of a
- * chunk is digit q % 5 of byte q / 5, a byte holding
- * d0 + 3 d1 + 9 d2 + 27 d3 + 81 d4 with digit d = code + 1 (bytes 243..255 are
- * never written); padding codes of real rows are code 0, padding rows zero
- * bytes.  The chunk and panel layout is the same.
+ * SDQ_PACK_BASE3 (ternary only): codes_per_chunk = 80; byte p of a chunk
+ * holds positions 5p .. 5p+4 with digits d_i = code + 1 as
+ * v = 81 d0 + 27 d1 + 9 d2 + 3 d3 + d4 (the first position most significant),
+ * stored as q = ceil(256 v / 243): v / 243 as an 8-bit fraction rounded up,
+ * so that v = floor(243 q / 256) and the digits come out most significant
+ * first as the integer parts of repeated multiplications by 3.  Padding codes
+ * of real rows are code 0, padding rows zero bytes.  The chunk and panel
+ * layout is the same.
  * Total size: sdq_codes_bytes() = n_pad * n_chunks * 16 bytes.
  */
 

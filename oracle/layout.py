@@ -113,7 +113,14 @@ def geometry_base3(n: int, k_up: int):
 
 
 def pack_base3(codes: np.ndarray) -> np.ndarray:
-    """Ternary int8 codes (N x K_up) -> the base-3 packed buffer."""
+    """Ternary int8 codes (N x K_up) -> the base-3 packed buffer.
+
+    Five codes per byte: with digits d_i = c_i + 1 of codes c_0 .. c_4 (the
+    first one most significant), v = 81 d_0 + 27 d_1 + 9 d_2 + 3 d_3 + d_4 in
+    [0, 243) is stored as the byte q = ceil(256 v / 243), i.e. v / 243 as an
+    8-bit binary fraction rounded up.  (The rounding makes the leading digits
+    readable by multiplying q by a power of 3 and keeping the high bits; the
+    oracle reads it back through v = floor(243 q / 256).)"""
     codes = np.asarray(codes)
     n, k_up = codes.shape
     n_pad, n_chunks = geometry_base3(n, k_up)
@@ -121,9 +128,10 @@ def pack_base3(codes: np.ndarray) -> np.ndarray:
     digits[:n] = 1                                   # padding codes of real rows: code 0
     digits[:n, :k_up] = codes.astype(np.int64) + 1
     digits[n:] = 0                                   # padding rows: zero bytes
-    d = digits.reshape(n_pad, n_chunks, 16, 5)
-    byte = d[..., 0] + 3 * d[..., 1] + 9 * d[..., 2] + 27 * d[..., 3] + 81 * d[..., 4]
-    byte = byte.astype(np.uint8).reshape(n_pad // PANEL, PANEL, n_chunks, 16).transpose(0, 2, 1, 3)
+    d = digits.reshape(n_pad, n_chunks, 16, 5).astype(np.int64)
+    v = 81 * d[..., 0] + 27 * d[..., 1] + 9 * d[..., 2] + 3 * d[..., 3] + d[..., 4]
+    q = -((-256 * v) // 243)                         # ceil(256 v / 243)
+    byte = q.astype(np.uint8).reshape(n_pad // PANEL, PANEL, n_chunks, 16).transpose(0, 2, 1, 3)
     return np.ascontiguousarray(byte).reshape(-1)
 
 
@@ -132,7 +140,8 @@ def unpack_base3(buf: np.ndarray, n: int, k_up: int) -> np.ndarray:
     n_pad, n_chunks = geometry_base3(n, k_up)
     b = np.asarray(buf, dtype=np.uint8).reshape(n_pad // PANEL, n_chunks, PANEL, 16)
     b = b.transpose(0, 2, 1, 3).reshape(n_pad, n_chunks * 16).astype(np.int64)
-    digits = np.stack([(b // 3 ** i) % 3 for i in range(5)], axis=-1).reshape(n_pad, -1)
+    v = (243 * b) // 256
+    digits = np.stack([(v // 3 ** (4 - i)) % 3 for i in range(5)], axis=-1).reshape(n_pad, -1)
     return (digits[:n, :k_up] - 1).astype(np.int8)
 
 

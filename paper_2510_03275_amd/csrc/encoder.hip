@@ -327,8 +327,9 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
 }
 
 // One thread per byte of the base-3 buffer (in buffer order: panel, chunk,
-// row of the panel, byte): five codes of the 2-bit fields -> d0 + 3 d1 + ...
-// + 81 d4 with d = code + 1; codes past k_up are code 0, rows past n zero bytes.
+// row of the panel, byte): five codes of the 2-bit fields, digits d = code + 1
+// (the first most significant) -> v = 81 d0 + ... + d4 -> the byte
+// ceil(256 v / 243); codes past k_up are code 0, rows past n zero bytes.
 __global__ void repack_base3_kernel(const uint32_t* __restrict__ fields, int64_t n, int64_t k_up,
                                     int64_t nch2, int64_t nch3, int64_t total, uint8_t* __restrict__ out) {
   for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
@@ -337,9 +338,9 @@ __global__ void repack_base3_kernel(const uint32_t* __restrict__ fields, int64_t
     const int64_t rr = (e / kChunkBytes) % kPanel;
     const int64_t c = (e / (kChunkBytes * kPanel)) % nch3;
     const int64_t r = (e / (kChunkBytes * kPanel * nch3)) * kPanel + rr;
-    uint32_t v = 0, pw = 1;
+    uint32_t v = 0;
     if (r < n) {
-      for (int i = 0; i < 5; ++i, pw *= 3) {
+      for (int i = 0; i < 5; ++i) {
         const int64_t j = c * kBase3PerChunk + 5 * byte + i;
         int code = 0;
         if (j < k_up) {
@@ -349,15 +350,17 @@ __global__ void repack_base3_kernel(const uint32_t* __restrict__ fields, int64_t
           const uint32_t f = (word >> (2 * (q % 16))) & 3u;
           code = f == 1u ? 1 : (f == 3u ? -1 : 0);
         }
-        v += static_cast<uint32_t>(code + 1) * pw;
+        v = 3u * v + static_cast<uint32_t>(code + 1);
       }
     }
-    out[e] = static_cast<uint8_t>(v);
+    out[e] = static_cast<uint8_t>((256u * v + 242u) / 243u);
   }
 }
 
-// One thread per 32-bit word of the 2-bit fields (16 codes): each code's
-// base-3 digit d gives the field of code d - 1 (00: 0, 01: +1, 11: -1).
+// One thread per 32-bit word of the 2-bit fields (16 codes): digit i of a
+// byte q is the integer part of 3 r after i such steps (r <- fraction part),
+// starting from r = q / 256; digit d gives the field of code d - 1
+// (00: 0, 01: +1, 11: -1).
 __global__ void unpack_base3_kernel(const uint8_t* __restrict__ b3, int64_t k_up, int64_t nch2,
                                     int64_t nch3, int64_t total_words, uint32_t* __restrict__ fields) {
   for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total_words;
@@ -373,9 +376,12 @@ __global__ void unpack_base3_kernel(const uint8_t* __restrict__ b3, int64_t k_up
       if (j >= k_up) break;
       const int64_t c3 = j / kBase3PerChunk;
       const int q = static_cast<int>(j % kBase3PerChunk);
-      uint32_t v = rowp[c3 * kPanel * kChunkBytes + q / 5];
-      for (int t = 0; t < q % 5; ++t) v /= 3u;
-      const uint32_t d = v % 3u;
+      uint32_t r = rowp[c3 * kPanel * kChunkBytes + q / 5], d = 0;
+      for (int t = 0; t <= q % 5; ++t) {
+        r *= 3u;
+        d = r >> 8;
+        r &= 255u;
+      }
       word |= (d == 2u ? 1u : (d == 0u ? 3u : 0u)) << (2 * i);
     }
     fields[e] = word;

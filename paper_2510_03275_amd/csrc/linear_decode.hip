@@ -377,6 +377,28 @@ __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
     p[i] = 0.0f;
 }
 
+// Byte K of x, masked with 60, in one instruction (a byte select on the
+// operand): with x = w << 2 it is 4 times nibble 2K of w, with x = w >> 2 four
+// times nibble 2K + 1.
+template <int K>
+__device__ inline uint32_t byte_and60(uint32_t x) {
+  uint32_t r;
+  if constexpr (K == 0)
+    asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_0" : "=v"(r) : "v"(x));
+  else if constexpr (K == 1)
+    asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1" : "=v"(r) : "v"(x));
+  else if constexpr (K == 2)
+    asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_2" : "=v"(r) : "v"(x));
+  else
+    asm("v_and_b32_sdwa %0, 60, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_3" : "=v"(r) : "v"(x));
+  return r;
+}
+
+template <int NIB>
+__device__ inline uint32_t nibble_offset(uint32_t w4, uint32_t w2) {
+  return byte_and60<NIB / 2>(NIB % 2 ? w2 : w4);
+}
+
 // Entries 4h .. 4h+3 of a 4-bit group's table.  Binary: bits b0..b3 of the
 // entry select +x or -x for four consecutive samples; ternary: fields
 // f0 = e & 3, f1 = e >> 2 weight two samples by {00: 0, 01: +1, 11: -1, 10: 0}.
@@ -482,13 +504,16 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
     const uint32_t words[4] = {q[c].x, q[c].y, q[c].z, q[c].w};
 #pragma unroll
     for (int wi = 0; wi < 4; ++wi) {
+      // byte offset of entry e = nibble value: 4 * e
+      const uint32_t w4 = words[wi] << 2, w2 = words[wi] >> 2;
+      const uint32_t offs[8] = {nibble_offset<0>(w4, w2), nibble_offset<1>(w4, w2), nibble_offset<2>(w4, w2),
+                                nibble_offset<3>(w4, w2), nibble_offset<4>(w4, w2), nibble_offset<5>(w4, w2),
+                                nibble_offset<6>(w4, w2), nibble_offset<7>(w4, w2)};
 #pragma unroll
       for (int nib = 0; nib < 8; ++nib) {
-        // byte offset of entry e = nibble value: 4 * e
-        const uint32_t off = nib == 0 ? (words[wi] << 2) & 60u : (words[wi] >> (4 * nib - 2)) & 60u;
 #pragma unroll
         for (int i = 0; i < MR; ++i)
-          acc[i] += *reinterpret_cast<const float*>(lbytes + (i * kRowFloats + (c * kGroupsPerChunk + wi * 8 + nib) * 16) * 4 + off);
+          acc[i] += *reinterpret_cast<const float*>(lbytes + (i * kRowFloats + (c * kGroupsPerChunk + wi * 8 + nib) * 16) * 4 + offs[nib]);
       }
       // Make each word's sums complete before the next word's table reads
       // (otherwise the compiler sinks the adds and keeps every read live:
@@ -518,10 +543,20 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
   }
 }
 
+// 4 * ((x >> 8) & 255) in one instruction (a byte select on the shifted operand).
+__device__ inline uint32_t byte1_times4(uint32_t x) {
+  uint32_t r;
+  asm("v_lshlrev_b32_sdwa %0, 2, %1 dst_sel:DWORD dst_unused:UNUSED_PAD src0_sel:DWORD src1_sel:BYTE_1"
+      : "=v"(r) : "v"(x));
+  return r;
+}
+
 // Base-3 codes (one activation row): byte p of a chunk holds codes 5p .. 5p+4
-// as b = sum_i (c_i + 1) 3^i.  Per byte two tables: 27 entries for its first
-// three codes and 9 for its last two; a lookup splits b = lo + 27 hi with
-// hi = (19 b) >> 9 (exact for b < 243).  Each table spans at most 27
+// as q = ceil(256 v / 243), v = 81 d0 + 27 d1 + 9 d2 + 3 d3 + d4 (d = code + 1).
+// Per byte two tables: 27 entries for its first three codes, indexed by
+// 9 d0 + 3 d1 + d2 = (27 q) >> 8, and 9 for its last two, indexed by
+// 3 d3 + d4 = (9 ((27 q) & 255)) >> 8 (both exact for every stored byte):
+// a multiply and a byte select each.  Each table spans at most 27
 // consecutive words, so a wave's reads of one table hit distinct banks or
 // the same word.  Otherwise as the 2-bit table GEMV: loads first, tables of
 // the segment shared by four panels, one wave per panel.
@@ -548,17 +583,18 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
   const int nch = static_cast<int>(min<int64_t>(SEG, n_chunks - c0));
   const int64_t code0 = c0 * kBase3PerChunk;
 
-  // 1. Loads.  Threads [0, kGroups) build the 27-entry tables, threads
-  //    [kGroups, 2 kGroups) the 9-entry ones.
+  // 1. Loads.  Threads [0, kGroups) build the 27-entry tables (samples
+  //    5g .. 5g+2), threads [kGroups, 2 kGroups) the 9-entry ones (5g+3, 5g+4);
+  //    xs = {the two low-order samples, the leading one}.
   const bool is_lo = tid < kGroups;
   const int g = is_lo ? tid : tid - kGroups;
   const bool gok = tid < 2 * kGroups && g < nch * kBytes;
   float xs[3] = {0.f, 0.f, 0.f};
   if (gok) {
-    const float* xp = xt + code0 + 5 * g + (is_lo ? 0 : 3);
+    const float* xp = xt + code0 + 5 * g + (is_lo ? 1 : 3);
     xs[0] = xp[0];
     xs[1] = xp[1];
-    if (is_lo) xs[2] = xp[2];
+    if (is_lo) xs[2] = xp[-1];
   }
   __builtin_amdgcn_sched_barrier(0);
   uint4 q[SEG];
@@ -569,14 +605,14 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
   }
   __builtin_amdgcn_sched_barrier(0);
 
-  // 2. Tables: entry a + 3 b (+ 9 c) = (a - 1) x0 + (b - 1) x1 (+ (c - 1) x2).
+  // 2. Tables: entry (9 c +) 3 a + b = ((c - 1) xs[2] +) (a - 1) xs[0] + (b - 1) xs[1].
   if (tid < 2 * kGroups) {
     float* dst = lut + g * kGF + (is_lo ? 0 : 27);
     float t9[9];
 #pragma unroll
-    for (int b = 0; b < 3; ++b)
+    for (int a = 0; a < 3; ++a)
 #pragma unroll
-      for (int a = 0; a < 3; ++a) t9[a + 3 * b] = static_cast<float>(a - 1) * xs[0] + static_cast<float>(b - 1) * xs[1];
+      for (int b = 0; b < 3; ++b) t9[3 * a + b] = static_cast<float>(a - 1) * xs[0] + static_cast<float>(b - 1) * xs[1];
     if (is_lo) {
 #pragma unroll
       for (int c = 0; c < 3; ++c)
@@ -599,12 +635,12 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
     for (int wi = 0; wi < 4; ++wi) {
 #pragma unroll
       for (int k = 0; k < 4; ++k) {
-        const uint32_t b = (words[wi] >> (8 * k)) & 255u;
-        const uint32_t hi = (b * 19u) >> 9;
-        const uint32_t lo = b - 27u * hi;
-        const float* tg = lut + (c * kBytes + wi * 4 + k) * kGF;
-        acc += tg[lo];
-        acc += tg[27 + hi];
+        const uint32_t t = ((words[wi] >> (8 * k)) & 255u) * 27u;
+        const uint32_t lead4 = byte1_times4(t);                   // 4 ((27 q) >> 8)
+        const uint32_t tail4 = byte1_times4((t & 255u) * 9u);     // 4 ((9 ((27 q) & 255)) >> 8)
+        const char* tg = reinterpret_cast<const char*>(lut + (c * kBytes + wi * 4 + k) * kGF);
+        acc += *reinterpret_cast<const float*>(tg + lead4);
+        acc += *reinterpret_cast<const float*>(tg + 27 * 4 + tail4);
       }
       asm volatile("" : "+v"(acc));
     }

@@ -651,8 +651,8 @@ sdq_status sdq_unpack_codes(const sdq_layout* L, const void* codes_host, int8_t*
       for (int64_t j = 0; j < L->k_up; ++j) {
         const int64_t c = j / kBase3PerChunk, q = j % kBase3PerChunk;
         const int64_t chunk = ((r / kPanel) * L->n_chunks + c) * kPanel + (r % kPanel);
-        int v = bytes[chunk * kChunkBytes + q / 5];
-        for (int i = 0; i < q % 5; ++i) v /= 3;
+        int v = 243 * bytes[chunk * kChunkBytes + q / 5] / 256;
+        for (int i = q % 5; i < 4; ++i) v /= 3;
         out[r * L->k_up + j] = static_cast<int8_t>(v % 3 - 1);
       }
     return SDQ_OK;

@@ -61,8 +61,10 @@ def test_round_trip(levels, n, k_up):
 # --- base-3 packing of ternary codes (five codes per byte) ---
 
 def test_base3_worked_bytes():
-    # codes (+1, 0, -1, -1, +1) -> digits (2, 1, 0, 0, 2) -> 2 + 3 + 0 + 0 + 162 = 167;
-    # all zeros -> 1 + 3 + 9 + 27 + 81 = 121; all +1 -> 242; all -1 -> 0.
+    # codes (+1, 0, -1, -1, +1) -> digits (2, 1, 0, 0, 2), first most significant
+    # -> v = 162 + 27 + 0 + 0 + 2 = 191 -> q = ceil(256 * 191 / 243) = ceil(201.2) = 202;
+    # all zeros -> v = 121 -> ceil(127.5) = 128; all +1 -> v = 242 -> ceil(254.9) = 255;
+    # all -1 -> 0.
     from oracle import layout as LY
     codes = np.zeros((1, 80), np.int8)
     codes[0, :5] = [1, 0, -1, -1, 1]
@@ -70,7 +72,7 @@ def test_base3_worked_bytes():
     codes[0, 10:15] = -1
     buf = LY.pack_base3(codes)
     assert buf.size == 64 * 16
-    assert list(buf[:4]) == [167, 242, 0, 121]
+    assert list(buf[:4]) == [202, 255, 0, 128]
     assert np.all(buf[16:] == 0)                       # padding rows
 
 
@@ -81,8 +83,31 @@ def test_base3_round_trip_and_size(n, k_up):
     codes = rng.integers(-1, 2, size=(n, k_up)).astype(np.int8)
     buf = LY.pack_base3(codes)
     assert buf.size == LY.packed_bytes_base3(n, k_up) == -(-n // 64) * 64 * -(-k_up // 80) * 16
-    assert np.all(buf.reshape(-1) <= 242)
+    valid = {-(-256 * v // 243) for v in range(243)}
+    assert set(np.unique(buf).tolist()) <= valid
     assert np.array_equal(LY.unpack_base3(buf, n, k_up), codes)
+
+
+def test_base3_digits_by_multiplication():
+    # The stored byte q is v / 243 rounded up to an 8-bit fraction, so the
+    # base-3 digits of v come out most significant first by repeatedly
+    # multiplying by 3 and taking the integer part (r <- 3 r; d = r >> 8;
+    # r <- r & 255), and the leading three and trailing two digits as
+    # (27 q) >> 8 and (9 ((27 q) & 255)) >> 8.  Checked for every v in [0, 243)
+    # against plain base-3 digits, and the oracle's unpack agrees.
+    from oracle import layout as LY
+    codes = np.array([[(v // 3 ** (4 - i)) % 3 - 1 for v in range(243) for i in range(5)]], np.int8)
+    buf = LY.pack_base3(codes)                     # one row, 1215 codes: 16 chunks
+    qs = buf.reshape(16, 64, 16)[:, 0, :].reshape(-1)[:243]
+    for v, q in enumerate(qs.tolist()):
+        r, ds = q, []
+        for _ in range(5):
+            r *= 3
+            ds.append(r >> 8)
+            r &= 255
+        assert ds == [(v // 3 ** (4 - i)) % 3 for i in range(5)], v
+        assert (27 * q) >> 8 == v // 9 and (9 * ((27 * q) & 255)) >> 8 == v % 9
+    assert np.array_equal(LY.unpack_base3(buf, 1, 1215), codes)
 
 
 def test_base3_is_smaller_than_two_bit_fields():
