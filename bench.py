@@ -53,16 +53,17 @@ MALL_BYTES = 256 * 1024 * 1024
 # what the same counters read for a 268,435,456-byte device copy.  Valid only
 # for the kernel sources they were taken with: a source whose hash differs
 # reports traffic null.
-TRAFFIC_FETCH_SCALE = 1.999747
+TRAFFIC_FETCH_SCALE = 1.999693
 TRAFFIC_WRITE_SCALE = 1.000000
 TRAFFIC_SOURCES = {
-    "linear_decode.hip": "925a235594d95c21abf8a6a482df168eb7a6955f33c7243e48d084a91093f47d",
-    "linear_prefill.hip": "51bbe2189571169ddb5c051b3526727e6481f6276588046ee9d7855c046b1d41",
+    "linear_decode.hip": "a4129ecaee97d8f93e951173464dbf1a7a14081baea142b61e662d6aacaaeedc",
+    "linear_prefill.hip": "1bb4f7a18e3177450ae4e60e374d5c1db38f41b35c5afdfef0ad40ac95bea620",
 }
 TRAFFIC_KIB = {   # kernel -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB)
-    "gemv_lut_kernel<1,2,2>": ("linear_decode.hip", 4420.88, 1040.0),
-    "gemv_lut_kernel<1,3,4>": ("linear_decode.hip", 57888.78, 3584.0),
-    "gemm_prefill_kernel<3>": ("linear_prefill.hip", 317410.33, 65536.0),
+    "gemv_lut_kernel<1,2,2>": ("linear_decode.hip", 4415.38, 1040.0),
+    "gemv_lut_kernel<1,3,4>": ("linear_decode.hip", 57864.16, 7168.0),
+    "gemv_lut_base3_kernel<4>": ("linear_decode.hip", 46482.12, 5824.0),
+    "gemm_prefill_kernel<3>": ("linear_prefill.hip", 311655.89, 65536.0),
 }
 
 
