@@ -19,7 +19,7 @@ streams its codes from HBM.  The line also carries:
                bf16 activations (TFLOP/s, fp16 MFMA roofline), MultiOSR on
                the LLaMA-7B layer's seven linears, the 80-layer LLaMA-70B
                stack (560 linears quantised, one token through all of them),
-               the continuous-precision sweep (output error and weight SNR
+               the same stack on base-3 codes, the continuous-precision sweep (output error and weight SNR
                against OSR 1..4 for each Hadamard choice, and MultiOSR against
                a uniform OSR), and Algorithm 1's block compensation (Hessian,
                factor, compensated encoding: times and held-out error);
@@ -267,11 +267,11 @@ def bench_multiosr(torch, P, synth, SG):
             "moments_s_incl_generation": t1 - t0, "allocate_ms": (t2 - t1) * 1e3}
 
 
-def bench_stack(torch, P, synth, SG, replays: int = 3):
+def bench_stack(torch, P, synth, SG, replays: int = 3, base3: bool = False):
     """The 80-layer LLaMA-70B stack: MultiOSR from the measured variances of all
-    560 linears, every linear quantised on the device (codes kept resident),
-    then one decoded token (m = 1, and m = 8) through all 560 sdq_linear calls
-    in one graph."""
+    560 linears, every linear quantised on the device (codes kept resident, as
+    2-bit fields or base-3 bytes), then one decoded token (m = 1, and m = 8)
+    through all 560 sdq_linear calls in one graph."""
     wl = synth.workload(5)
     t0 = time.perf_counter()
     out = torch.zeros(2, dtype=torch.float64, device="cuda")
@@ -292,12 +292,14 @@ def bench_stack(torch, P, synth, SG, replays: int = 3):
     encs = []
     for lin, o in zip(wl.linears, osr):
         w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
-        encs.append(P.quantize(w, float(o), wl.levels))
+        encs.append(P.quantize(w, float(o), wl.levels,
+                               packing=P.SDQ_PACK_BASE3 if base3 else P.SDQ_PACK_FIELDS))
         del w
     torch.cuda.synchronize()
     t2 = time.perf_counter()
     code_bytes = sum(P.sdq_codes_bytes(e.layout) for e in encs)
-    res = {"workload": "llama70b_stack_80x7_multiosr_ternary", "linears": len(encs),
+    res = {"workload": "llama70b_stack_80x7_multiosr_ternary" + ("_base3" if base3 else ""),
+           "linears": len(encs),
            "weighted_mean_osr": float(sum(float(o) * lin.n * lin.k for o, lin in zip(osr, wl.linears))
                                       / sum(lin.n * lin.k for lin in wl.linears)),
            "code_bytes": int(code_bytes),
@@ -638,10 +640,11 @@ def main() -> int:
                           "decode_70b_base3": bench_decode_70b(torch, P, synth, SG, base3=True),
                           "prefill": bench_prefill(torch, P, synth, SG),
                           "multiosr": bench_multiosr(torch, P, synth, SG)}
-        try:
-            line["phases"]["stack_70b"] = bench_stack(torch, P, synth, SG)
-        except Exception as exc:  # noqa: BLE001 -- report, keep the headline line
-            line["phases"]["stack_70b"] = {"error": repr(exc)}
+        for key, b3 in (("stack_70b", False), ("stack_70b_base3", True)):
+            try:
+                line["phases"][key] = bench_stack(torch, P, synth, SG, base3=b3)
+            except Exception as exc:  # noqa: BLE001 -- report, keep the headline line
+                line["phases"][key] = {"error": repr(exc)}
         try:
             line["phases"]["precision_sweep"] = bench_sweep(torch, P, synth, SG)
         except Exception as exc:  # noqa: BLE001

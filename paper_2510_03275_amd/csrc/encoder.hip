@@ -23,6 +23,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <utility>
 
 #include "sdq_internal.h"
 
@@ -326,65 +327,119 @@ __global__ __launch_bounds__(64 * kScanWaves) void scan_kernel(
   }
 }
 
-// One thread per byte of the base-3 buffer (in buffer order: panel, chunk,
-// row of the panel, byte): five codes of the 2-bit fields, digits d = code + 1
-// (the first most significant) -> v = 81 d0 + ... + d4 -> the byte
-// ceil(256 v / 243); codes past k_up are code 0, rows past n zero bytes.
-__global__ void repack_base3_kernel(const uint32_t* __restrict__ fields, int64_t n, int64_t k_up,
-                                    int64_t nch2, int64_t nch3, int64_t total, uint8_t* __restrict__ out) {
+// Base-3 <-> 2-bit fields.  One thread per (row, 80-code chunk): the base-3
+// chunk is 16 bytes, the same codes as 2-bit fields are five 32-bit words
+// (word i holds codes 16 i .. 16 i + 15, code j of a row at word j / 16 of the
+// fields layout).  Code 5p + i of a chunk is field 5p + i of the 160-bit
+// string of the five words: bits 10p .. 10p + 9 hold byte p's five fields.
+// Consecutive threads take consecutive rows of a panel, so each wave reads
+// or writes a chunk of 64 rows as 1 KB contiguous.
+
+// The five fields of a byte of 2-bit fields' string, from the 160-bit string
+// held in w[5].
+template <int P>
+__device__ inline uint32_t ten_bits(const uint32_t (&w)[5]) {
+  constexpr int off = 10 * P, wi = off / 32, sh = off % 32;
+  uint32_t f = w[wi] >> sh;
+  if constexpr (sh > 22) f |= w[wi + 1] << (32 - sh);
+  return f & 1023u;
+}
+
+template <int P>
+__device__ inline void put_ten_bits(uint32_t (&w)[5], uint32_t f) {
+  constexpr int off = 10 * P, wi = off / 32, sh = off % 32;
+  w[wi] |= f << sh;
+  if constexpr (sh > 22) w[wi + 1] |= f >> (32 - sh);
+}
+
+// Byte of one group of five fields: digits d = code + 1 (field 00 -> 1,
+// 01 -> 2, 11 -> 0), the first code most significant, v = sum d_i 3^(4-i),
+// stored as ceil(256 v / 243).
+__device__ inline uint32_t base3_byte(uint32_t f) {
+  uint32_t v = 0;
+#pragma unroll
+  for (int i = 0; i < 5; ++i) v = 3u * v + (((f >> (2 * i)) + 1u) & 3u);
+  return (256u * v + 242u) / 243u;
+}
+
+template <int P>
+__device__ inline void repack_byte(const uint32_t (&w)[5], uint32_t (&out)[4]) {
+  out[P / 4] |= base3_byte(ten_bits<P>(w)) << (8 * (P % 4));
+}
+
+template <int... Ps>
+__device__ inline void repack_all(const uint32_t (&w)[5], uint32_t (&out)[4], std::integer_sequence<int, Ps...>) {
+  (repack_byte<Ps>(w, out), ...);
+}
+
+// total = (n_pad / 64) * nch3 * 64 threads' work; rows past n are zero bytes.
+__global__ void repack_base3_kernel(const uint32_t* __restrict__ fields, int64_t n, int64_t nch2,
+                                    int64_t nch3, int64_t total, uint4* __restrict__ out) {
   for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
        e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-    const int byte = static_cast<int>(e % kChunkBytes);
-    const int64_t rr = (e / kChunkBytes) % kPanel;
-    const int64_t c = (e / (kChunkBytes * kPanel)) % nch3;
-    const int64_t r = (e / (kChunkBytes * kPanel * nch3)) * kPanel + rr;
-    uint32_t v = 0;
-    if (r < n) {
+    const int64_t rr = e % kPanel;
+    const int64_t c3 = (e / kPanel) % nch3;
+    const int64_t pn = e / (kPanel * nch3);
+    uint32_t o[4] = {0u, 0u, 0u, 0u};
+    if (pn * kPanel + rr < n) {
+      uint32_t w[5];
+#pragma unroll
       for (int i = 0; i < 5; ++i) {
-        const int64_t j = c * kBase3PerChunk + 5 * byte + i;
-        int code = 0;
-        if (j < k_up) {
-          const int64_t c2 = j / 64;
-          const int q = static_cast<int>(j % 64);
-          const uint32_t word = fields[(((r / kPanel) * nch2 + c2) * kPanel + rr) * 4 + q / 16];
-          const uint32_t f = (word >> (2 * (q % 16))) & 3u;
-          code = f == 1u ? 1 : (f == 3u ? -1 : 0);
-        }
-        v = 3u * v + static_cast<uint32_t>(code + 1);
+        const int64_t gw = c3 * 5 + i;               // field words past the last chunk: padding, code 0
+        w[i] = gw < nch2 * 4 ? fields[((pn * nch2 + gw / 4) * kPanel + rr) * 4 + gw % 4] : 0u;
       }
+      repack_all(w, o, std::make_integer_sequence<int, 16>{});
     }
-    out[e] = static_cast<uint8_t>((256u * v + 242u) / 243u);
+    out[e] = make_uint4(o[0], o[1], o[2], o[3]);
   }
 }
 
-// One thread per 32-bit word of the 2-bit fields (16 codes): digit i of a
-// byte q is the integer part of 3 r after i such steps (r <- fraction part),
-// starting from r = q / 256; digit d gives the field of code d - 1
-// (00: 0, 01: +1, 11: -1).
-__global__ void unpack_base3_kernel(const uint8_t* __restrict__ b3, int64_t k_up, int64_t nch2,
-                                    int64_t nch3, int64_t total_words, uint32_t* __restrict__ fields) {
-  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total_words;
-       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
-    const int wd = static_cast<int>(e % 4);
-    const int64_t rr = (e / 4) % kPanel;
-    const int64_t c2 = (e / (4 * kPanel)) % nch2;
-    const int64_t pn = e / (4 * kPanel * nch2);
-    const uint8_t* rowp = b3 + (pn * nch3 * kPanel + rr) * kChunkBytes;   // chunk 0 of this row
-    uint32_t word = 0;
-    for (int i = 0; i < 16; ++i) {
-      const int64_t j = c2 * 64 + wd * 16 + i;
-      if (j >= k_up) break;
-      const int64_t c3 = j / kBase3PerChunk;
-      const int q = static_cast<int>(j % kBase3PerChunk);
-      uint32_t r = rowp[c3 * kPanel * kChunkBytes + q / 5], d = 0;
-      for (int t = 0; t <= q % 5; ++t) {
-        r *= 3u;
-        d = r >> 8;
-        r &= 255u;
-      }
-      word |= (d == 2u ? 1u : (d == 0u ? 3u : 0u)) << (2 * i);
+template <int P>
+__device__ inline void unpack_byte(const uint32_t (&by)[4], const uint32_t* pat, uint32_t (&w)[5]) {
+  put_ten_bits<P>(w, pat[(by[P / 4] >> (8 * (P % 4))) & 255u]);
+}
+
+template <int... Ps>
+__device__ inline void unpack_all(const uint32_t (&by)[4], const uint32_t* pat, uint32_t (&w)[5],
+                                  std::integer_sequence<int, Ps...>) {
+  (unpack_byte<Ps>(by, pat, w), ...);
+}
+
+// groups = max(nch3, ceil(4 nch2 / 5)) five-word groups per row, so that every
+// field word (padding ones included) is written; rows past n are zero.
+__global__ __launch_bounds__(256) void unpack_base3_kernel(const uint4* __restrict__ b3, int64_t n,
+                                                           int64_t nch2, int64_t nch3, int64_t groups,
+                                                           int64_t total, uint32_t* __restrict__ fields) {
+  // Byte -> its five codes as 2-bit fields: digit i of q is the integer part
+  // of 3 r after i + 1 steps of r <- fraction part of 3 r, from r = q / 256.
+  __shared__ uint32_t pat[256];
+  {
+    uint32_t r = threadIdx.x, f = 0;
+#pragma unroll
+    for (int i = 0; i < 5; ++i) {
+      r *= 3u;
+      f |= (((r >> 8) + 3u) & 3u) << (2 * i);        // digit 0, 1, 2 -> field 11, 00, 01
+      r &= 255u;
     }
-    fields[e] = word;
+    pat[threadIdx.x] = f;
+  }
+  __syncthreads();
+  for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
+       e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t rr = e % kPanel;
+    const int64_t g = (e / kPanel) % groups;
+    const int64_t pn = e / (kPanel * groups);
+    uint32_t w[5] = {0u, 0u, 0u, 0u, 0u};
+    if (pn * kPanel + rr < n && g < nch3) {
+      const uint4 v = b3[(pn * nch3 + g) * kPanel + rr];
+      const uint32_t by[4] = {v.x, v.y, v.z, v.w};
+      unpack_all(by, pat, w, std::make_integer_sequence<int, 16>{});
+    }
+#pragma unroll
+    for (int i = 0; i < 5; ++i) {
+      const int64_t gw = g * 5 + i;
+      if (gw < nch2 * 4) fields[((pn * nch2 + gw / 4) * kPanel + rr) * 4 + gw % 4] = w[i];
+    }
   }
 }
 
@@ -392,10 +447,11 @@ __global__ void unpack_base3_kernel(const uint8_t* __restrict__ b3, int64_t k_up
 
 sdq_status launch_unpack_base3(const void* codes, const sdq_layout* L, uint32_t* fields, hipStream_t stream) {
   const sdq_layout F = fields_view(L);
-  const int64_t words = F.n_pad * F.n_chunks * (kChunkBytes / 4);
-  const unsigned grid = static_cast<unsigned>(std::min<int64_t>((words + 255) / 256, 16384));
-  unpack_base3_kernel<<<grid, 256, 0, stream>>>(static_cast<const uint8_t*>(codes), L->k_up, F.n_chunks,
-                                                L->n_chunks, words, fields);
+  const int64_t groups = std::max<int64_t>(L->n_chunks, (4 * F.n_chunks + 4) / 5);
+  const int64_t total = L->n_pad * groups;
+  const unsigned grid = static_cast<unsigned>(std::min<int64_t>((total + 255) / 256, 16384));
+  unpack_base3_kernel<<<grid, 256, 0, stream>>>(static_cast<const uint4*>(codes), L->n, F.n_chunks, L->n_chunks,
+                                                groups, total, fields);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "base-3 unpack launch");
   return SDQ_OK;
@@ -464,10 +520,10 @@ sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T,
 
 sdq_status launch_repack_base3(const uint32_t* fields, const sdq_layout* L, void* codes, hipStream_t stream) {
   const sdq_layout F = fields_view(L);
-  const int64_t total = L->n_pad * L->n_chunks * kChunkBytes;
+  const int64_t total = L->n_pad * L->n_chunks;
   const unsigned grid = static_cast<unsigned>(std::min<int64_t>((total + 255) / 256, 16384));
-  repack_base3_kernel<<<grid, 256, 0, stream>>>(fields, L->n, L->k_up, F.n_chunks, L->n_chunks, total,
-                                                static_cast<uint8_t*>(codes));
+  repack_base3_kernel<<<grid, 256, 0, stream>>>(fields, L->n, F.n_chunks, L->n_chunks, total,
+                                                static_cast<uint4*>(codes));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "base-3 repack launch");
   return SDQ_OK;
