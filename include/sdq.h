@@ -192,10 +192,10 @@ sdq_status sdq_quantize_check(const void* workspace_dev, void* stream);
  * sdq_hessian_factor: Algorithm 1 line 4, u_dev = Cholesky((H + lambda I)^-1)^T,
  * the upper factor U with U^T U = (H + lambda I)^-1 (fp64 [k x k], lower part
  * zero), computed without forming the inverse (a blocked Cholesky of the
- * index-reversed matrix and a blocked triangular inverse).  h_dev: symmetric
+ * index-reversed matrix and a recursive blocked triangular inverse).  h_dev: symmetric
  * fp64 [k x k]; k a multiple of 64; lambda >= 0 absolute (GPTQ takes 1 % of the
  * mean diagonal).  workspace: sdq_hessian_factor_workspace_bytes(k) bytes
- * (about 16 k^2).  A non-positive pivot does not fail the call; it is reported
+ * (about 18 k^2).  A non-positive pivot does not fail the call; it is reported
  * by sdq_hessian_check(workspace) as SDQ_ERR_NOT_SPD.
  * Errors: SDQ_ERR_SHAPE, SDQ_ERR_ARG, SDQ_ERR_WORKSPACE.
  *

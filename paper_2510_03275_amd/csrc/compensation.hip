@@ -110,7 +110,10 @@ __global__ __launch_bounds__(256) void gemm64_kernel(
 // stride sa1 / sx1; grid y: batches, stride sa2 / sx2).  factor = 1: Cholesky
 // of the block's lower part in place (A = L L^T, the upper part zeroed); a
 // pivot that is not positive sets *info and is replaced by 1.  Then X = L^-1
-// (lower) by forward substitution, one column per thread.
+// (lower) in three levels: the four 16 x 16 diagonal blocks by forward
+// substitution (one column per thread), then pairs of diagonal blocks are
+// joined as X21 = -X22 (L21 X11), 16 -> 32 and 32 -> 64, every output of a
+// product on its own thread.
 __global__ __launch_bounds__(256) void potrf64_kernel(double* A, int64_t lda, int64_t sa1,
                                                       int64_t sa2, double* X, int64_t ldx,
                                                       int64_t sx1, int64_t sx2, int factor,
@@ -149,13 +152,36 @@ __global__ __launch_bounds__(256) void potrf64_kernel(double* A, int64_t lda, in
       A[i * lda + k] = k <= i ? a[i][k] : 0.0;
     }
   }
+  __shared__ double rd[kT];          // 1 / L[i][i]
+  __shared__ double tt[32 * 32];     // L21 X11 of the current level
+  if (tid < kT) rd[tid] = 1.0 / a[tid][tid];
+  for (int e = tid; e < kT * kT; e += 256) x[e / kT][e % kT] = 0.0;
+  __syncthreads();
   if (tid < kT) {
-    const int c = tid;
-    for (int i = 0; i < kT; ++i) {
+    const int o = 16 * (tid / 16), c = tid % 16;
+    for (int i = c; i < 16; ++i) {
       double s = i == c ? 1.0 : 0.0;
-      for (int k = c; k < i; ++k) s -= a[i][k] * x[k][c];
-      x[i][c] = i < c ? 0.0 : s / a[i][i];
+      for (int k = c; k < i; ++k) s -= a[o + i][o + k] * x[o + k][o + c];
+      x[o + i][o + c] = s * rd[o + i];
     }
+  }
+  __syncthreads();
+  for (int b = 16; b < kT; b *= 2) {
+    const int pairs = kT / (2 * b);
+    for (int e = tid; e < pairs * b * b; e += 256) {
+      const int pr = e / (b * b), i = (e / b) % b, j = e % b, r = 2 * b * pr;
+      double s = 0.0;
+      for (int k = j; k < b; ++k) s += a[r + b + i][r + k] * x[r + k][r + j];
+      tt[(pr * b + i) * b + j] = s;
+    }
+    __syncthreads();
+    for (int e = tid; e < pairs * b * b; e += 256) {
+      const int pr = e / (b * b), i = (e / b) % b, j = e % b, r = 2 * b * pr;
+      double s = 0.0;
+      for (int k = 0; k <= i; ++k) s += x[r + b + i][r + b + k] * tt[(pr * b + k) * b + j];
+      x[r + b + i][r + j] = -s;
+    }
+    __syncthreads();
   }
   __syncthreads();
   for (int e = tid; e < kT * kT; e += 256) {
@@ -242,18 +268,47 @@ void gemm64(int64_t M, int64_t N, int64_t K, double alpha, const TA* A, int64_t 
 
 // Lower-triangular inverse X = L^-1 of a batch of n x n matrices (n a multiple
 // of 64; batch stride s): the diagonal 64-blocks of X must already hold the
-// inverses of L's; X's strictly upper part zero; tmp holds 64 x n per batch.
-// Row block i: X[i, :i] = -X_ii (L[i, :i] X[:i, :i]).
+// inverses of L's, X's strictly upper part zero; tmp holds n^2 / 4 per batch.
+// For a lower-triangular [L11 0; L21 L22] with X11 = L11^-1 and X22 = L22^-1,
+// the missing block is X21 = -X22 (L21 X11).  A power-of-two size (64 2^j)
+// joins its diagonal blocks pairwise up a binary tree, two b x b x b products
+// per pair, batched over the pairs of a level (one matrix) or over the
+// matrices (one launch per pair); any other size splits off its largest
+// power-of-two leading block, inverts the rest recursively and joins the two.
+void trtri_pow2(const double* L, double* X, int64_t n, int64_t ld, int64_t s, int batch, double* tmp,
+                hipStream_t stream) {
+  for (int64_t b = kT; b < n; b *= 2) {
+    const int64_t pairs = n / (2 * b);
+    const int64_t ps = 2 * b * (ld + 1);                  // diagonal step between pairs
+    auto join = [&](int64_t off, int nbat, int64_t mstride) {
+      gemm64(b, b, b, 1.0, L + off + b * ld, ld, int64_t{1}, X + off, ld, int64_t{1}, 0.0, tmp, b,
+             int64_t{1}, stream, 0, nbat, mstride, mstride, b * b);
+      gemm64(b, b, b, -1.0, X + off + b * ld + b, ld, int64_t{1}, tmp, b, int64_t{1}, 0.0, X + off + b * ld,
+             ld, int64_t{1}, stream, 0, nbat, mstride, b * b, mstride);
+    };
+    if (batch == 1) {
+      join(0, static_cast<int>(pairs), ps);
+    } else {
+      for (int64_t pr = 0; pr < pairs; ++pr) join(pr * ps, batch, s);
+    }
+  }
+}
+
 void trtri_lower(const double* L, double* X, int64_t n, int64_t ld, int64_t s, int batch, double* tmp,
                  hipStream_t stream) {
-  const int64_t t = n / kT;
-  for (int64_t i = 1; i < t; ++i) {
-    const int64_t w = i * kT;
-    gemm64(int64_t{kT}, w, w, 1.0, L + i * kT * ld, ld, int64_t{1}, X, ld, int64_t{1}, 0.0, tmp, n,
-           int64_t{1}, stream, 0, batch, s, s, kT * n);
-    gemm64(int64_t{kT}, w, int64_t{kT}, -1.0, X + i * kT * ld + i * kT, ld, int64_t{1}, tmp, n,
-           int64_t{1}, 0.0, X + i * kT * ld, ld, int64_t{1}, stream, 0, batch, s, kT * n, s);
+  int64_t n1 = kT;
+  while (2 * n1 < n) n1 *= 2;
+  if (2 * n1 == n || n1 == n) {
+    trtri_pow2(L, X, n, ld, s, batch, tmp, stream);
+    return;
   }
+  const int64_t n2 = n - n1;                              // 0 < n2 < n1
+  trtri_pow2(L, X, n1, ld, s, batch, tmp, stream);
+  trtri_lower(L + n1 * (ld + 1), X + n1 * (ld + 1), n2, ld, s, batch, tmp, stream);
+  gemm64(n2, n1, n1, 1.0, L + n1 * ld, ld, int64_t{1}, X, ld, int64_t{1}, 0.0, tmp, n1, int64_t{1}, stream, 0,
+         batch, s, s, n2 * n1);
+  gemm64(n2, n1, n2, -1.0, X + n1 * ld + n1, ld, int64_t{1}, tmp, n1, int64_t{1}, 0.0, X + n1 * ld, ld,
+         int64_t{1}, stream, 0, batch, s, n2 * n1, s);
 }
 
 }  // namespace
@@ -269,7 +324,7 @@ sdq_status launch_hessian_accumulate(const float* x, int64_t m, int64_t k, doubl
 }
 
 size_t hessian_factor_ws_bytes(int64_t k) {
-  return 256 + align_up(static_cast<size_t>(k) * k * 8, 256) * 2 + align_up(static_cast<size_t>(kT) * k * 8, 256);
+  return 256 + align_up(static_cast<size_t>(k) * k * 8, 256) * 2 + align_up(static_cast<size_t>(k) * k * 2, 256);
 }
 
 sdq_status launch_hessian_factor(const double* h, int64_t k, double lam, double* u, void* ws,
