@@ -129,21 +129,28 @@ __global__ __launch_bounds__(256) void potrf64_kernel(double* A, int64_t lda, in
   }
   __syncthreads();
   if (factor) {
+    // Column j: lanes j .. 63 of wave 0 read the pivot before lane j writes
+    // its square root (one instruction stream).  Update: thread t owns column
+    // t % 64, rows t / 64 + 4 q, of the trailing part.
+    const int kk = tid % kT;
     for (int j = 0; j < kT; ++j) {
-      if (tid == 0) {
+      if (tid >= j && tid < kT) {
         double d = a[j][j];
         if (!(d > 0.0)) {
-          info[0] = 1;
+          if (tid == j) info[0] = 1;
           d = 1.0;
         }
-        a[j][j] = sqrt(d);
+        const double sd = sqrt(d);
+        a[tid][j] = tid == j ? sd : a[tid][j] / sd;
       }
       __syncthreads();
-      if (tid > j && tid < kT) a[tid][j] /= a[j][j];
-      __syncthreads();
-      for (int e = tid; e < kT * kT; e += 256) {
-        const int i = e / kT, k = e % kT;
-        if (k > j && i >= k) a[i][k] -= a[i][j] * a[k][j];
+      if (kk > j) {
+        const double akj = a[kk][j];
+#pragma unroll
+        for (int q = 0; q < kT / 4; ++q) {
+          const int i = tid / kT + 4 * q;
+          if (i >= kk) a[i][kk] -= a[i][j] * akj;
+        }
       }
       __syncthreads();
     }
