@@ -462,7 +462,7 @@ def bench_compensation(torch, P, synth, SG, n: int = 4096, k: int = 4096, m_cal:
     for name, enc in (("plain", enc_p), ("compensated", enc_c)):
         y = P.linear(x_test, enc).double().cpu().numpy()
         errs[name] = float(np.linalg.norm(y - y_ref) / np.linalg.norm(y_ref))
-    flops_h = 2.0 * m_cal * k * k
+    flops_h = 1.0 * m_cal * k * (k + 1)   # symmetric rank-m update: one triangle plus the diagonal
     flops_f = 2.0 * k ** 3 / 3.0          # Cholesky k^3/3 plus triangular inverse k^3/3
     nb = k // 256
     m_up = int(round(osr * 256))
@@ -479,7 +479,9 @@ def bench_compensation(torch, P, synth, SG, n: int = 4096, k: int = 4096, m_cal:
             "roofline": {"bound": "alu", "achieved": tf(flops_h, ms_h), "peak": F64_PEAK_TFLOPS,
                          "unit": "TFLOP/s", "frac": tf(flops_h, ms_h) / F64_PEAK_TFLOPS, "traffic": None,
                          "kernel": "gemm64_kernel<float,float> (Hessian)",
-                         "note": "fp64 FMA GEMM; flops = 2 * m * k^2"}}
+                         "note": "fp64 matrix-core GEMM over the tiles on or below the diagonal "
+                                 "(each added at its transposed position too); flops = m * k * (k + 1), "
+                                 "the count of a symmetric rank-m update"}}
 
 
 def bench_sweep(torch, P, synth, SG):

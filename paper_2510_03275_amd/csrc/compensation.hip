@@ -15,11 +15,11 @@
 //            the later columns take the optimal-brain-surgeon correction of the
 //            jointly quantized block, W_F -= E_b U_QQ^-1 U_QF.
 //
-// All of it is dense fp64 linear algebra: one register-tiled VALU GEMM with
-// general strides (64 x 64 tile per workgroup, 4 x 4 outputs per thread,
-// 16-deep k steps through LDS) serves the Hessian, the panel solves, the
-// trailing updates, the triangular inverses and the block corrections; a
-// 64 x 64 Cholesky-and-inverse kernel works on diagonal blocks in LDS.
+// All of it is dense fp64 linear algebra: one GEMM on the fp64 matrix cores
+// with general strides (64 x 64 tile per workgroup, 16-deep k slices through
+// LDS) serves the Hessian, the panel solves, the trailing updates, the
+// triangular inverses and the block corrections; a 64 x 64 Cholesky-and-
+// inverse kernel works on diagonal blocks in LDS.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -31,12 +31,26 @@ namespace {
 
 constexpr int kT = 64;     // factorisation panel / GEMM tile
 constexpr int kTK = 16;    // GEMM k step
+constexpr int kStage = kT * kTK / 256;   // operand elements staged per thread and k step
 
 // C = beta C + alpha A B; element (i, p) of A at A[i * rsa + p * csa], likewise
-// B and C; blockIdx.z selects a batch (strides bsa, bsb, bsc).  lower_only skips
-// tiles strictly above the diagonal of C.  beta == 0 never reads C.  A and B
+// B and C; blockIdx.z selects a batch (strides bsa, bsb, bsc).  lower_only = 1
+// skips tiles strictly above the diagonal of C; lower_only = 2 (a symmetric
+// product, M = N) skips them too but also updates the transposed position of
+// every tile below the diagonal, so both triangles are written.  beta == 0
+// never reads C.  A and B
 // may overlap C only where every output tile depends on the same rows of A
-// alone (an in-place panel solve with N <= 64).
+// alone (an in-place panel solve with N <= 64): a workgroup reads all of its
+// operands before it writes.
+//
+// fp64 matrix cores: a 64 x 64 tile per workgroup, four waves in a 2 x 2 grid
+// of 32 x 32 (four v_mfma_f64_16x16x4f64 accumulators each).  Operands go
+// through LDS in 16-deep k slices (converted to fp64 on the way), the next
+// slice loaded into registers while the current one is multiplied.  Lane
+// layout of the instruction: lane l supplies A[l % 16][l / 16] and
+// B[l / 16][l % 16] and receives D[l / 16 + 4 v][l % 16] in item v.
+typedef double double4_t __attribute__((ext_vector_type(4)));
+
 template <typename TA, typename TB>
 __global__ __launch_bounds__(256) void gemm64_kernel(
     int64_t M, int64_t N, int64_t K, double alpha, const TA* A, int64_t rsa, int64_t csa,
@@ -45,65 +59,95 @@ __global__ __launch_bounds__(256) void gemm64_kernel(
   __shared__ double As[kTK][kT + 2];
   __shared__ double Bs[kTK][kT + 2];
   const int tid = threadIdx.x;
-  const int tx = tid % 16, ty = tid / 16;
+  const int lane = tid % 64, wave = tid / 64;
+  const int wr = wave / 2, wc = wave % 2;
   const int64_t i0 = static_cast<int64_t>(blockIdx.y) * kT;
   const int64_t j0 = static_cast<int64_t>(blockIdx.x) * kT;
   if (lower_only && i0 + kT - 1 < j0) return;
   A += static_cast<int64_t>(blockIdx.z) * bsa;
   B += static_cast<int64_t>(blockIdx.z) * bsb;
   C += static_cast<int64_t>(blockIdx.z) * bsc;
-  double acc[4][4];
-#pragma unroll
-  for (int u = 0; u < 4; ++u)
-#pragma unroll
-    for (int v = 0; v < 4; ++v) acc[u][v] = 0.0;
-  const bool a_pfast = csa == 1;     // consecutive threads along the contiguous index
+  // Staging: element e = tid + 256 q of the slice, consecutive threads along
+  // the operand's contiguous index.
+  const bool a_pfast = csa == 1;
   const bool b_jfast = csb == 1;
+  int aii[kStage], app[kStage], bjj[kStage], bpp[kStage];
+#pragma unroll
+  for (int q = 0; q < kStage; ++q) {
+    const int e = tid + 256 * q;
+    aii[q] = a_pfast ? e / kTK : e % kT;
+    app[q] = a_pfast ? e % kTK : e / kT;
+    bjj[q] = b_jfast ? e % kT : e / kTK;
+    bpp[q] = b_jfast ? e / kT : e % kTK;
+  }
+  TA ra[kStage];
+  TB rb[kStage];
+  auto load = [&](int64_t p0) {
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+      const int64_t gi = i0 + aii[q], gp = p0 + app[q];
+      ra[q] = gi < M && gp < K ? A[gi * rsa + gp * csa] : TA(0);
+      const int64_t gj = j0 + bjj[q], gq = p0 + bpp[q];
+      rb[q] = gj < N && gq < K ? B[gq * rsb + gj * csb] : TB(0);
+    }
+  };
+  auto store = [&]() {
+#pragma unroll
+    for (int q = 0; q < kStage; ++q) {
+      As[app[q]][aii[q]] = static_cast<double>(ra[q]);
+      Bs[bpp[q]][bjj[q]] = static_cast<double>(rb[q]);
+    }
+  };
+  double4_t acc[2][2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+#pragma unroll
+    for (int c = 0; c < 2; ++c) acc[r][c] = double4_t{0.0, 0.0, 0.0, 0.0};
+  const int lr = lane % 16, lk = lane / 16;
+  load(0);
+  store();
+  __syncthreads();
   for (int64_t p0 = 0; p0 < K; p0 += kTK) {
+    const bool more = p0 + kTK < K;
+    if (more) load(p0 + kTK);
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = tid + 256 * q;
-      const int ii = a_pfast ? e / kTK : e % kT;
-      const int pp = a_pfast ? e % kTK : e / kT;
-      const int64_t gi = i0 + ii, gp = p0 + pp;
-      As[pp][ii] = gi < M && gp < K ? static_cast<double>(A[gi * rsa + gp * csa]) : 0.0;
-    }
+    for (int kk = 0; kk < kTK / 4; ++kk) {
+      double a[2], b[2];
 #pragma unroll
-    for (int q = 0; q < 4; ++q) {
-      const int e = tid + 256 * q;
-      const int jj = b_jfast ? e % kT : e / kTK;
-      const int pp = b_jfast ? e / kT : e % kTK;
-      const int64_t gj = j0 + jj, gp = p0 + pp;
-      Bs[pp][jj] = gj < N && gp < K ? static_cast<double>(B[gp * rsb + gj * csb]) : 0.0;
+      for (int r = 0; r < 2; ++r) a[r] = As[4 * kk + lk][32 * wr + 16 * r + lr];
+#pragma unroll
+      for (int c = 0; c < 2; ++c) b[c] = Bs[4 * kk + lk][32 * wc + 16 * c + lr];
+#pragma unroll
+      for (int r = 0; r < 2; ++r)
+#pragma unroll
+        for (int c = 0; c < 2; ++c) acc[r][c] = __builtin_amdgcn_mfma_f64_16x16x4f64(a[r], b[c], acc[r][c], 0, 0, 0);
     }
     __syncthreads();
-#pragma unroll
-    for (int pp = 0; pp < kTK; ++pp) {
-      double a[4], b[4];
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        a[u] = As[pp][ty * 4 + u];
-        b[u] = Bs[pp][tx * 4 + u];
-      }
-#pragma unroll
-      for (int u = 0; u < 4; ++u)
-#pragma unroll
-        for (int v = 0; v < 4; ++v) acc[u][v] = __builtin_fma(a[u], b[v], acc[u][v]);
+    if (more) {
+      store();
+      __syncthreads();
     }
-    __syncthreads();
   }
 #pragma unroll
-  for (int u = 0; u < 4; ++u)
+  for (int r = 0; r < 2; ++r)
 #pragma unroll
-    for (int v = 0; v < 4; ++v) {
-      const int64_t gi = i0 + ty * 4 + u, gj = j0 + tx * 4 + v;
-      if (gi < M && gj < N) {
-        double* c = C + gi * rsc + gj * csc;
-        double val = alpha * acc[u][v];
-        if (beta != 0.0) val += beta * *c;
-        *c = val;
+    for (int c = 0; c < 2; ++c)
+#pragma unroll
+      for (int v = 0; v < 4; ++v) {
+        const int64_t gi = i0 + 32 * wr + 16 * r + lk + 4 * v, gj = j0 + 32 * wc + 16 * c + lr;
+        if (gi < M && gj < N) {
+          double* cp = C + gi * rsc + gj * csc;
+          double val = alpha * acc[r][c][v];
+          if (beta != 0.0) val += beta * *cp;
+          *cp = val;
+          if (lower_only == 2 && i0 > j0) {
+            double* mp = C + gj * rsc + gi * csc;
+            double mv = alpha * acc[r][c][v];
+            if (beta != 0.0) mv += beta * *mp;
+            *mp = mv;
+          }
+        }
       }
-    }
 }
 
 // One 64 x 64 diagonal block per workgroup (grid x: blocks along a diagonal,
@@ -324,7 +368,7 @@ void trtri_lower(const double* L, double* X, int64_t n, int64_t ld, int64_t s, i
 
 sdq_status launch_hessian_accumulate(const float* x, int64_t m, int64_t k, double* h, hipStream_t stream) {
   // H[i][j] += 2 sum_p X[p][i] X[p][j]
-  gemm64(k, k, m, 2.0, x, int64_t{1}, k, x, k, int64_t{1}, 1.0, h, k, int64_t{1}, stream);
+  gemm64(k, k, m, 2.0, x, int64_t{1}, k, x, k, int64_t{1}, 1.0, h, k, int64_t{1}, stream, 2);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "hessian launch");
   return SDQ_OK;

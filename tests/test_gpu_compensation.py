@@ -38,6 +38,20 @@ def test_hessian_accumulates_twice_the_gram_matrix(m, k):
     assert np.max(np.abs(got - want)) <= 1e-12 * np.max(np.abs(want))
 
 
+@pytest.mark.parametrize("m,k", [(300, 100), (257, 320)])
+def test_hessian_adds_to_any_starting_matrix(m, k):
+    # Only tiles on or below the diagonal are multiplied, each added at its own
+    # and its transposed position: a non-symmetric starting H keeps both triangles.
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    x = _calib_x(3 * k, m, k)
+    h0 = np.random.default_rng(k).standard_normal((k, k))
+    h = torch.from_numpy(h0.copy()).cuda()
+    P.sdq_hessian_accumulate(torch.from_numpy(x).cuda(), h)
+    want = h0 + OC.hessian_fp64(x)
+    assert np.max(np.abs(h.cpu().numpy() - want)) <= 1e-12 * np.max(np.abs(want))
+
+
 @pytest.mark.parametrize("k", [64, 128, 320, 1024])
 def test_factor_matches_oracle(k):
     torch = require_gpu()
