@@ -285,6 +285,16 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
 #pragma unroll
       for (int cg = 0; cg < 4; ++cg) acc[pg][cg] = v4i{0, 0, 0, 0};
     const int64_t c_first = b * m_up / kCpc;        // block b's first code chunk
+    // The block's plane scale of this lane's activation row of each group,
+    // loaded now (unconditionally, from a clamped row: a load under a branch
+    // is waited for on the spot) and used when the block ends.
+    float sxv[NPG];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      const int a = pg * 4 + kg;
+      const float v = sx[static_cast<int64_t>(min(a, m - 1)) * nb + b];
+      sxv[pg] = a < m ? v : 0.0f;
+    }
     for (int c0 = 0; c0 < cpb; c0 += CH) {
       uint4 q[CH];
       uint4 av[CH][SPC][NPG];
@@ -341,14 +351,12 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
     // Block done: dequantise with the block's scale of this lane's activation row.
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
-      const int a = pg * 4 + kg;
-      const float sxv = a < m ? sx[static_cast<int64_t>(a) * nb + b] : 0.0f;
 #pragma unroll
       for (int cg = 0; cg < 4; ++cg) {
         const float v = (static_cast<float>(acc[pg][cg][0]) * 65536.0f +
                          static_cast<float>(acc[pg][cg][1]) * 256.0f) +
                         static_cast<float>(acc[pg][cg][2]);
-        accf[pg][cg] += sxv * v;
+        accf[pg][cg] += sxv[pg] * v;
       }
     }
   }
