@@ -729,20 +729,23 @@ int mfma_cpb(const sdq_layout* L) {
 }
 
 // Blocks per wave of the MFMA GEMV (each split over K costs one atomic add per
-// output); SDQ_MFMA_BPW overrides.
-int mfma_bpw(const sdq_layout* L) {
+// output); SDQ_MFMA_BPW overrides.  Measured on MI355X (70B shapes and
+// 8192 x 8192, OSR 2): one block per wave is best up to two plane groups
+// (m <= 8); from three on, the longer-lived waves of two blocks each win
+// (m = 16: 64 -> 56 us on 28672 x 8192, 72 -> 59 us on 8192 x 28672).
+int mfma_bpw(const sdq_layout* L, int64_t m) {
   static const char* env = std::getenv("SDQ_MFMA_BPW");
   if (env) {
     const int v = std::atoi(env);
     if (v >= 1) return v;
   }
   (void)L;
-  return 1;
+  return npg_for(m) >= 3 ? 2 : 1;
 }
 
 // Workgroups along K per panel (each covers 4 * bpw blocks).
-int mfma_splits(const sdq_layout* L) {
-  const int bpw = mfma_bpw(L);
+int mfma_splits(const sdq_layout* L, int64_t m) {
+  const int bpw = mfma_bpw(L, m);
   return static_cast<int>((L->nb + 4 * bpw - 1) / (4 * bpw));
 }
 
@@ -791,8 +794,8 @@ template <int LEVELS, int NPG, int CH>
 void launch_mfma_ch(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
                     int64_t m, float* y, bool accumulate, hipStream_t stream) {
   const int64_t n_panels = L->n_pad / kPanel;
-  const int bpw = mfma_bpw(L);
-  const int splits = mfma_splits(L);
+  const int bpw = mfma_bpw(L, m);
+  const int splits = mfma_splits(L, m);
   // K groups fastest: consecutive workgroups sweep one panel's chunks.
   const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(n_panels));
   gemv_mfma_kernel<LEVELS, NPG, CH><<<grid, dim3(256), 0, stream>>>(
@@ -896,7 +899,7 @@ bool decode_reads_base3(const sdq_layout* L, int64_t m) {
 }
 
 bool decode_needs_zero_y(const sdq_layout* L, int64_t m) {
-  if (use_mfma(L, m)) return mfma_splits(L) > 1;
+  if (use_mfma(L, m)) return mfma_splits(L, m) > 1;
   return segs_for(L, pick_seg(L, round_mr(m))) > 1;
 }
 
