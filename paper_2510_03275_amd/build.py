@@ -31,6 +31,10 @@ COMMON = [
 PER_FILE = {
     "encoder.hip": ["-ffp-contract=off"],
     "sdq_api.cpp": ["-ffp-contract=off"],
+    # fp64 GEMM: keep the MFMA accumulators in VGPRs (left to its heuristics the
+    # compiler carries them across the k loop in VGPRs but runs the MFMAs on
+    # AGPR copies, 64 moves and a pipeline drain per k step).
+    "compensation.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 
