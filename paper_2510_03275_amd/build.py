@@ -4,7 +4,8 @@
 
 Every call recompiles all sources.  Device code is built with packed-fp32
 instructions disabled and with floating-point contraction off in the encoder
-(its sources also say so with a pragma), and without fast-math.
+(its sources also say so with a pragma), and without fast-math; the fp64 GEMM
+and the prefill expansion keep their matrix-core accumulators in VGPRs.
 """
 from __future__ import annotations
 
@@ -20,8 +21,8 @@ BUILD = os.path.join(HERE, "_build")
 LIB = os.path.join(HERE, "libsdq.so")
 ARCH = os.environ.get("SDQ_OFFLOAD_ARCH", "gfx950")
 
-SOURCES = ["sdq_api.cpp", "encoder.hip", "linear_decode.hip", "linear_prefill.hip", "moments.hip",
-           "compensation.hip"]
+SOURCES = ["sdq_api.cpp", "encoder.hip", "linear_decode.hip", "linear_prefill.hip", "expand_prefill.hip",
+           "moments.hip", "compensation.hip"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
@@ -35,6 +36,7 @@ PER_FILE = {
     # compiler carries them across the k loop in VGPRs but runs the MFMAs on
     # AGPR copies, 64 moves and a pipeline drain per k step).
     "compensation.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    "expand_prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

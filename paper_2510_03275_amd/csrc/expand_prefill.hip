@@ -1,0 +1,254 @@
+// Prefill path of sdq_linear (m > 16 activation rows), the expansion, on the
+// fp16 matrix cores (v_mfma_f32_32x32x16_f16, fp32 accumulation):
+//
+//   expand   x_tilde_b = x_b E with E = Had D^T (B x M) for every block b: a
+//            batched GEMM.  E is held as an fp16 pair hi + lo, so x E_hi + x E_lo
+//            reproduces the fp64 product to ~2^-22 relative for fp16 / bf16
+//            inputs (both exact in fp16 at these magnitudes); fp32 inputs add
+//            x_lo E_hi.  The result is rounded once to fp16 (without Had also
+//            kept as an fp16 pair, the GEMM then running over both halves).
+//
+// Built with the matrix-core accumulators in VGPRs (the build sets the
+// compiler's MFMA VGPR form for this file): left to its heuristics the
+// compiler runs the MFMAs on AGPR copies of accumulators it carries through
+// the t loop in VGPRs.
+//
+// MFMA operand convention: lane l supplies row (A) or column (B) l % 32 and
+// the eight consecutive k of group l / 32; accumulator v holds row
+// 8*(v/4) + 4*(l/32) + v%4, column l%32.
+#include <hip/hip_runtime.h>
+
+#include <algorithm>
+#include <cstdlib>
+#include <hip/hip_fp16.h>
+#include <hip/hip_bf16.h>
+
+#include "sdq_internal.h"
+
+namespace sdq {
+namespace {
+
+typedef _Float16 half8 __attribute__((ext_vector_type(8)));
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+__device__ inline floatx16 mfma32(const half8& a, const half8& b, const floatx16& c) {
+  return __builtin_amdgcn_mfma_f32_32x32x16_f16(a, b, c, 0, 0, 0);
+}
+
+// Workgroups are dealt to the eight XCDs round-robin by index, and each XCD
+// has its own L2.  Map workgroup `id` of `n` to a tile so that every XCD
+// receives one contiguous range of tile indices (tiles that share operands
+// are then numbered next to each other).
+constexpr int kXcds = 8;
+__device__ inline int64_t xcd_tile(int64_t id, int64_t n) {
+  const int64_t xcd = id % kXcds, j = id / kXcds;
+  const int64_t per = n / kXcds, rem = n % kXcds;
+  return xcd * per + (xcd < rem ? xcd : rem) + j;
+}
+
+// Tiled expansion: workgroup tile kXTM activation rows x 128 samples of one
+// block, t in steps of 64 through LDS (x as fp16 hi (+ lo for fp32 inputs),
+// E^T as fp16 hi and lo), so each operand element fetched from memory feeds
+// many MFMA products.  The four waves form a 2 x 2 grid: wave (wr, wc) owns
+// rows kXTM/2 * wr .. and samples 64 wc .. 64 wc + 63 (RT x 2 accumulator
+// tiles of 32 x 32), which balances its A and B fragment reads from LDS.  LDS
+// rows are padded to 72 halves: fragment reads of 16 consecutive rows fall on
+// distinct banks.
+constexpr int kXTN = 128, kXTK = 64, kXLd = kXTK + 8;
+
+template <sdq_dtype XT, int kXTM>
+__global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
+    const void* __restrict__ x, int64_t m, int64_t k, int B, int m_up,
+    int64_t k_up, int64_t k_up_pad, const uint16_t* __restrict__ et_hi,
+    const uint16_t* __restrict__ et_lo, _Float16* __restrict__ xt_out,
+    _Float16* __restrict__ xt_lo_out) {
+  constexpr bool NEED_LO = XT == SDQ_F32;
+  __shared__ __attribute__((aligned(16))) _Float16 xs[NEED_LO ? 2 : 1][kXTM * kXLd];
+  __shared__ __attribute__((aligned(16))) _Float16 es[2][kXTN * kXLd];
+  const int tid = threadIdx.x;
+  const int lane = tid % 64;
+  const int wave = tid / 64;
+  // Tile order: sample tiles fastest (they share the x tile), then row tiles,
+  // then blocks; dealt to the XCDs in contiguous ranges.
+  const int n_st = (m_up + kXTN - 1) / kXTN;
+  const int64_t n_rt = (m + kXTM - 1) / kXTM;
+  const int64_t tile = xcd_tile(blockIdx.x, static_cast<int64_t>(gridDim.x));
+  const int st = static_cast<int>(tile % n_st);
+  const int64_t i0 = ((tile / n_st) % n_rt) * kXTM;
+  const int64_t b = tile / (n_st * n_rt);
+  const int c0 = st * kXTN;                         // first sample of the tile
+  if (b == 0 && st == 0) {
+    const int64_t pad = k_up_pad - k_up;            // zero the padding columns of these rows
+    for (int64_t idx = tid; idx < kXTM * pad; idx += 256) {
+      const int64_t i = i0 + idx / pad;
+      if (i < m) {
+        xt_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
+        if (xt_lo_out) xt_lo_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
+      }
+    }
+  }
+  constexpr int RT = kXTM / 64;                    // 32-row tiles per wave
+  constexpr int XIT = kXTM * 8 / 256;               // x loads per thread per t tile
+  const int wr = wave / 2, wc = wave % 2;
+  floatx16 acc[RT][2];
+#pragma unroll
+  for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+    for (int ct = 0; ct < 2; ++ct)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[rt][ct][v] = 0.0f;
+  const int kg = (lane / 32) * 8;
+  // Registers staging the next t tile, raw: x (kXTM rows x 64 t, eight threads
+  // per row, 8 values each; rows past m load row m - 1 and are zeroed when
+  // stored) and E^T (128 samples x 64 t, hi and lo; samples past M load
+  // sample M - 1 and are zeroed).  All loads are unconditional, so they are
+  // in flight together; conversion happens when the tile is stored to LDS.
+  constexpr int XW = XT == SDQ_F32 ? 2 : 1;          // uint4 per 8 values
+  uint4 xr[XIT][XW], eh[4], el[4];
+#define SDQ_FETCH(T0)                                                                          \
+  do {                                                                                         \
+    _Pragma("unroll") for (int it = 0; it < XIT; ++it) {                                       \
+      const int idx_ = tid + 256 * it;                                                         \
+      const int64_t row_ = min<int64_t>(i0 + idx_ / 8, m - 1);                                 \
+      const int64_t e_ = row_ * k + b * B + (T0) + (idx_ % 8) * 8;                             \
+      if (XT == SDQ_F32) {                                                                     \
+        const uint4* p_ = reinterpret_cast<const uint4*>(static_cast<const float*>(x) + e_);   \
+        xr[it][0] = p_[0];                                                                     \
+        xr[it][XW - 1] = p_[1];                                                                \
+      } else {                                                                                 \
+        xr[it][0] = *reinterpret_cast<const uint4*>(static_cast<const uint16_t*>(x) + e_);     \
+      }                                                                                        \
+    }                                                                                          \
+    _Pragma("unroll") for (int it = 0; it < 4; ++it) {                                         \
+      const int idx_ = tid + 256 * it;                                                         \
+      const int c_ = idx_ / 8;                                                                 \
+      const int cc_ = c0 + c_ < m_up ? c0 + c_ : m_up - 1;                                     \
+      const int64_t off_ = static_cast<int64_t>(cc_) * B + (T0) + (idx_ % 8) * 8;              \
+      eh[it] = *reinterpret_cast<const uint4*>(et_hi + off_);                                  \
+      el[it] = *reinterpret_cast<const uint4*>(et_lo + off_);                                  \
+    }                                                                                          \
+  } while (0)
+  SDQ_FETCH(0);
+  for (int t0 = 0; t0 < B; t0 += kXTK) {
+    __syncthreads();                                // previous tile's reads are done
+#pragma unroll
+    for (int it = 0; it < XIT; ++it) {
+      const int idx = tid + 256 * it;
+      const int r = idx / 8, sg = idx % 8;
+      const bool ok = i0 + r < m;
+      half8 hi, lo;
+      if (XT == SDQ_F16) {
+        hi = *reinterpret_cast<const half8*>(&xr[it][0]);
+      } else if (XT == SDQ_BF16) {
+        const uint32_t w[4] = {xr[it][0].x, xr[it][0].y, xr[it][0].z, xr[it][0].w};
+#pragma unroll
+        for (int q = 0; q < 8; ++q)
+          hi[q] = static_cast<_Float16>(__uint_as_float(((w[q / 2] >> (16 * (q % 2))) & 0xFFFFu) << 16));
+      } else {
+        const uint4 u0 = xr[it][0], u1 = xr[it][XW - 1];
+        const uint32_t w[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const float f = __uint_as_float(w[q]);
+          hi[q] = static_cast<_Float16>(f);
+          lo[q] = static_cast<_Float16>(f - static_cast<float>(hi[q]));
+        }
+      }
+      if (!ok) {
+#pragma unroll
+        for (int q = 0; q < 8; ++q) { hi[q] = 0; lo[q] = 0; }
+      }
+      *reinterpret_cast<half8*>(&xs[0][r * kXLd + sg * 8]) = hi;
+      if (NEED_LO) *reinterpret_cast<half8*>(&xs[NEED_LO ? 1 : 0][r * kXLd + sg * 8]) = lo;
+    }
+#pragma unroll
+    for (int it = 0; it < 4; ++it) {
+      const int idx = tid + 256 * it;
+      const int c = idx / 8, sg = idx % 8;
+      const uint32_t keep = c0 + c < m_up ? ~0u : 0u;   // a mask, not a select of addresses
+      const uint4 h = eh[it], l = el[it];
+      *reinterpret_cast<uint4*>(&es[0][c * kXLd + sg * 8]) = make_uint4(h.x & keep, h.y & keep, h.z & keep, h.w & keep);
+      *reinterpret_cast<uint4*>(&es[1][c * kXLd + sg * 8]) = make_uint4(l.x & keep, l.y & keep, l.z & keep, l.w & keep);
+    }
+    __syncthreads();
+    if (t0 + kXTK < B) SDQ_FETCH(t0 + kXTK);        // in flight during this tile's MFMAs
+#pragma unroll
+    for (int kk = 0; kk < kXTK; kk += 16) {
+      half8 a[RT], alo[RT], bh[2], bl[2];
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt) {
+        const int r = 32 * RT * wr + 32 * rt + lane % 32;
+        a[rt] = *reinterpret_cast<const half8*>(&xs[0][r * kXLd + kk + kg]);
+        if (NEED_LO) alo[rt] = *reinterpret_cast<const half8*>(&xs[NEED_LO ? 1 : 0][r * kXLd + kk + kg]);
+      }
+#pragma unroll
+      for (int ct = 0; ct < 2; ++ct) {
+        const int c = 64 * wc + 32 * ct + lane % 32;
+        bh[ct] = *reinterpret_cast<const half8*>(&es[0][c * kXLd + kk + kg]);
+        bl[ct] = *reinterpret_cast<const half8*>(&es[1][c * kXLd + kk + kg]);
+      }
+#pragma unroll
+      for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+        for (int ct = 0; ct < 2; ++ct) {
+          acc[rt][ct] = mfma32(a[rt], bh[ct], acc[rt][ct]);
+          acc[rt][ct] = mfma32(a[rt], bl[ct], acc[rt][ct]);
+          if (NEED_LO) acc[rt][ct] = mfma32(alo[rt], bh[ct], acc[rt][ct]);
+        }
+    }
+  }
+#pragma unroll
+  for (int ct = 0; ct < 2; ++ct) {
+    const int col = c0 + 64 * wc + 32 * ct + lane % 32;
+    if (col >= m_up) continue;
+#pragma unroll
+    for (int rt = 0; rt < RT; ++rt)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int64_t i = i0 + 32 * RT * wr + 32 * rt + 8 * (v / 4) + 4 * (lane / 32) + (v % 4);
+        if (i < m) {
+          const _Float16 hi = static_cast<_Float16>(acc[rt][ct][v]);
+          xt_out[i * k_up_pad + b * m_up + col] = hi;
+          if (xt_lo_out)
+            xt_lo_out[i * k_up_pad + b * m_up + col] =
+                static_cast<_Float16>(acc[rt][ct][v] - static_cast<float>(hi));
+        }
+      }
+  }
+}
+
+#undef SDQ_FETCH
+
+}  // namespace
+
+// Without Had the row scales follow the weights' outliers and the layer
+// output can be small next to s_r |x_tilde|: one fp16 rounding of x_tilde
+// then exceeds the 1e-3 budget.  Those layouts keep x_tilde as an fp16 pair
+// hi + lo and run the GEMM on both.
+bool prefill_split(const sdq_layout* L) { return L->hadamard == SDQ_HAD_NONE; }
+
+sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
+                                 const Tables* T, void* ws, hipStream_t stream) {
+  _Float16* xbuf = static_cast<_Float16*>(ws);
+  const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
+  _Float16* xlo = prefill_split(L)
+                      ? reinterpret_cast<_Float16*>(static_cast<char*>(ws) +
+                                                    align_up(static_cast<size_t>(m) * k_up_pad * 2, 256))
+                      : nullptr;
+  // Sample tiles fastest: neighbouring workgroups share the x tile.  B is a
+  // multiple of the 64-wide t step for every supported block.
+  constexpr int tm = 128;
+  const dim3 tgrid(static_cast<unsigned>(((L->m_up + kXTN - 1) / kXTN) * L->nb * ((m + tm - 1) / tm)));
+#define SDQ_XT(XT)                                                                              \
+  expand_prefill_tiled_kernel<XT, tm><<<tgrid, dim3(256), 0, stream>>>(                         \
+      x, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf, xlo)
+  if (xt == SDQ_F32) SDQ_XT(SDQ_F32);
+  else if (xt == SDQ_BF16) SDQ_XT(SDQ_BF16);
+  else SDQ_XT(SDQ_F16);
+#undef SDQ_XT
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return hip_error(e, "prefill expansion launch");
+  return SDQ_OK;
+}
+
+}  // namespace sdq

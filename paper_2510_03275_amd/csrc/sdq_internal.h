@@ -114,7 +114,9 @@ sdq_status launch_decode_contract(int64_t m, const void* codes, const float* sca
                                   const sdq_layout* L, float* y, bool accumulate, void* ws,
                                   bool y_ready, hipStream_t stream);
 
-// Prefill path (m > 16): expansion (fp16 x_tilde) then MFMA GEMM.
+// Prefill path (m > 16): expansion (fp16 x_tilde) then MFMA GEMM.  Layouts
+// without Had keep x_tilde as an fp16 pair (prefill_split).
+bool prefill_split(const sdq_layout* L);
 size_t prefill_ws_bytes(const sdq_layout* L, int64_t m);
 sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
                                  const Tables* T, void* ws, hipStream_t stream);
