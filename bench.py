@@ -53,17 +53,17 @@ MALL_BYTES = 256 * 1024 * 1024
 # what the same counters read for a 268,435,456-byte device copy.  Valid only
 # for the kernel sources they were taken with: a source whose hash differs
 # reports traffic null.
-TRAFFIC_FETCH_SCALE = 1.999743
+TRAFFIC_FETCH_SCALE = 1.999749
 TRAFFIC_WRITE_SCALE = 1.000000
 TRAFFIC_SOURCES = {
     "linear_decode.hip": "9f8138496cdb9a3c75e5b5eb612773b35b241e262c613aea1c16e0d40144cac7",
-    "linear_prefill.hip": "1bb4f7a18e3177450ae4e60e374d5c1db38f41b35c5afdfef0ad40ac95bea620",
+    "linear_prefill.hip": "048719858228d70c55034411451eba617ad64e0af491671d6426854d39f2608e",
 }
 TRAFFIC_KIB = {   # kernel -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB)
     "gemv_lut_kernel<1,2,2>": ("linear_decode.hip", 4421.38, 1040.0),
-    "gemv_lut_kernel<1,3,4>": ("linear_decode.hip", 57864.03, 7168.0),
+    "gemv_lut_kernel<1,3,4>": ("linear_decode.hip", 57863.91, 7168.0),
     "gemv_lut_base3_kernel<4>": ("linear_decode.hip", 46482.12, 5824.0),
-    "gemm_prefill_kernel<3>": ("linear_prefill.hip", 311822.34, 65536.0),
+    "gemm_prefill_kernel<3>": ("linear_prefill.hip", 311685.91, 65536.0),
 }
 
 
