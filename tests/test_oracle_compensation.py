@@ -84,3 +84,29 @@ def test_compensation_lowers_the_calibration_loss():
         yq = x @ L.reconstruct_fp64(r.codes, r.scales, 256, r.m_up).T
         errs.append(np.linalg.norm(yq - y) / np.linalg.norm(y))
     assert errs[1] < 0.75 * errs[0], errs
+
+
+def test_second_block_takes_the_normal_equation_correction():
+    # Two blocks: block 0 keeps its plain codes, and block 1 is the plain
+    # row-scaled encoding of W_1 + E_0 H_QF H_FF^-1 (H damped), the correction
+    # computed here from the Hessian's normal equations, not from its Cholesky
+    # factor.  (The two routes differ by fp64 rounding, which can move a value
+    # across an fp32 rounding boundary: a tiny share of codes may differ; a
+    # wrong sign, a missing U_QQ^-1 or a wrong block changes thousands.)
+    n, k, b = 16, 512, 256
+    w = synth.weight_rows(9, 0, n, k, 0.02, True)
+    x = _lowrank_x(2000, k, 10)
+    h = C.hessian_fp64(x)
+    lam = 0.01 * np.mean(np.diag(h))
+    u = C.inverse_cholesky_upper(h, lam)
+    r = C.encode_compensated(w, 2.0, 3, b, u)
+    plain = E.encode(w, 2.0, 3)
+    m_up = plain.m_up
+    assert np.array_equal(r.codes[:, :m_up], plain.codes[:, :m_up])
+    hd = h + lam * np.eye(k)
+    q, f = slice(0, b), slice(b, k)
+    e0 = w[:, q].astype(np.float64) - L.reconstruct_fp64(plain.codes[:, :m_up], plain.scales, b, m_up)
+    w1 = w[:, f].astype(np.float64) + e0 @ hd[q, f] @ np.linalg.inv(hd[f, f])
+    want = C.encode_block_with_scale(w1.astype(np.float32), 2.0, 3, b, plain.scales)
+    assert np.mean(want != r.codes[:, m_up:]) < 1e-3
+    assert np.mean(want != plain.codes[:, m_up:]) > 0.05     # the correction does change codes
