@@ -35,7 +35,7 @@ namespace {
 constexpr int kRotThreads = 256;
 constexpr int kUpBM = 128;        // rows per upsample tile (two panels)
 constexpr int kUpBN = 64;         // non-impulse samples per upsample tile
-constexpr int kUpBK = 32;         // t-chunk staged in LDS
+constexpr int kUpBK = 16;         // t-chunk staged in LDS (two buffers)
 constexpr int kUpThreads = 128;   // 16 x 8 threads, 8 x 8 outputs each
 constexpr int kScanWaves = 4;
 
@@ -171,15 +171,36 @@ __global__ __launch_bounds__(kRotThreads) void rotate_kernel(
   if (q == 0 && r < n) atomicMax(&rmax[r], __float_as_uint(mx));
 }
 
+typedef __attribute__((address_space(3))) void* lds_void_ptr;
+typedef __attribute__((address_space(1))) const void* gbl_void_ptr;
+
+// Plain s_barrier between compiler fences: __syncthreads() adds a release
+// fence, which would wait for the copies still in flight.
+__device__ inline void lds_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
 // Batched VALU GEMM over (block, row tile, sample tile).  Thread (tx, ty)
-// owns rows ty*8 .. ty*8+7 and tile columns tx*8 .. tx*8+7.
+// owns rows ty*8 .. ty*8+7 and tile columns tx*8 .. tx*8+7.  The t chunks
+// are copied from global memory straight into two LDS buffers
+// (global_load_lds_dwordx4: 1 KB per wave and copy, no staging registers);
+// chunk c + 2 is copied while chunk c + 1 is multiplied.  Every output adds
+// its products in increasing t, as a plain loop over t would.
 __global__ __launch_bounds__(kUpThreads) void upsample_kernel(
     const float* __restrict__ v, const float* __restrict__ unz, int64_t n, int64_t n_ws,
     int64_t k_up, int B, int m_up, int phases, int m_nz, int m_nz_pad, float* __restrict__ xup,
     uint32_t* __restrict__ rmax) {
-  __shared__ float As[kUpBK][kUpBM];
-  __shared__ float Bs[kUpBK][kUpBN];
+  static_assert(kUpThreads == 128 && kUpBK == 16 && kUpBM == 128 && kUpBN == 64,
+                "copy pattern: each wave copies 8 of the 16 t rows of both operands");
+  __shared__ __attribute__((aligned(1024))) float As0[kUpBK][kUpBM];
+  __shared__ __attribute__((aligned(1024))) float As1[kUpBK][kUpBM];
+  __shared__ __attribute__((aligned(1024))) float Bs0[kUpBK][kUpBN];
+  __shared__ __attribute__((aligned(1024))) float Bs1[kUpBK][kUpBN];
   const int tid = threadIdx.x;
+  const int lane = tid % 64;
+  const int wave = tid / 64;
   const int tx = tid % 8;
   const int ty = tid / 8;
   const int64_t rt = blockIdx.x;     // row tile
@@ -193,44 +214,61 @@ __global__ __launch_bounds__(kUpThreads) void upsample_kernel(
 #pragma unroll
     for (int j = 0; j < 8; ++j) acc[i][j] = 0.0f;
 
-  const float* vblk = v + b * B * n_ws;
-  for (int t0 = 0; t0 < B; t0 += kUpBK) {
-    // Stage A: kUpBK x 128 floats, B: kUpBK x 64 floats (float4 loads).
-#pragma unroll
-    for (int q = 0; q < (kUpBK * kUpBM / 4) / kUpThreads; ++q) {
-      const int idx = q * kUpThreads + tid;
-      const int tt = idx / (kUpBM / 4);
-      const int c4 = idx % (kUpBM / 4);
-      const float4 val = *reinterpret_cast<const float4*>(vblk + (t0 + tt) * n_ws + r0 + c4 * 4);
-      *reinterpret_cast<float4*>(&As[tt][c4 * 4]) = val;
-    }
-#pragma unroll
-    for (int q = 0; q < (kUpBK * kUpBN / 4) / kUpThreads; ++q) {
-      const int idx = q * kUpThreads + tid;
-      const int tt = idx / (kUpBN / 4);
-      const int c4 = idx % (kUpBN / 4);
-      const float4 val = *reinterpret_cast<const float4*>(unz + (t0 + tt) * m_nz_pad + j0 + c4 * 4);
-      *reinterpret_cast<float4*>(&Bs[tt][c4 * 4]) = val;
-    }
-    __syncthreads();
-#pragma unroll 4
-    for (int tt = 0; tt < kUpBK; ++tt) {
-      const float4 a0 = *reinterpret_cast<const float4*>(&As[tt][ty * 8]);
-      const float4 a1 = *reinterpret_cast<const float4*>(&As[tt][ty * 8 + 4]);
-      const float4 b0 = *reinterpret_cast<const float4*>(&Bs[tt][tx * 8]);
-      const float4 b1 = *reinterpret_cast<const float4*>(&Bs[tt][tx * 8 + 4]);
-      const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
-      const float c[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
-#pragma unroll
-      for (int i = 0; i < 8; ++i)
-#pragma unroll
-        for (int j = 0; j < 8; ++j) {
-          const float prod = a[i] * c[j];
-          acc[i][j] = acc[i][j] + prod;
-        }
-    }
-    __syncthreads();
+  // Copies of one chunk by wave w: t rows 8w .. 8w+7 of A (four copies of
+  // two 512-byte rows) and of B (two copies of four 256-byte rows).  Lane l
+  // of a copy lands 16 l bytes past the copy's LDS base, so the global
+  // source of lane l is the float4 that belongs there.
+  const float* a_src = v + b * B * n_ws + (8 * wave + lane / 32) * n_ws + r0 + (lane % 32) * 4;
+  const float* b_src = unz + (8 * wave + lane / 16) * m_nz_pad + j0 + (lane % 16) * 4;
+#define SDQ_UP_FILL(AS, BS, C)                                                                    \
+  do {                                                                                            \
+    const int64_t t0_ = static_cast<int64_t>(C) * kUpBK;                                          \
+    _Pragma("unroll") for (int j = 0; j < 4; ++j)                                                 \
+      __builtin_amdgcn_global_load_lds((gbl_void_ptr)(a_src + (t0_ + 2 * j) * n_ws),              \
+                                       (lds_void_ptr)(&AS[8 * wave + 2 * j][0]), 16, 0, 0);       \
+    _Pragma("unroll") for (int j = 0; j < 2; ++j)                                                 \
+      __builtin_amdgcn_global_load_lds((gbl_void_ptr)(b_src + (t0_ + 4 * j) * m_nz_pad),          \
+                                       (lds_void_ptr)(&BS[8 * wave + 4 * j][0]), 16, 0, 0);       \
+  } while (0)
+#define SDQ_UP_MUL(AS, BS)                                                                        \
+  do {                                                                                            \
+    _Pragma("unroll 4") for (int tt = 0; tt < kUpBK; ++tt) {                                      \
+      const float4 a0 = *reinterpret_cast<const float4*>(&AS[tt][ty * 8]);                        \
+      const float4 a1 = *reinterpret_cast<const float4*>(&AS[tt][ty * 8 + 4]);                    \
+      const float4 b0 = *reinterpret_cast<const float4*>(&BS[tt][tx * 8]);                        \
+      const float4 b1 = *reinterpret_cast<const float4*>(&BS[tt][tx * 8 + 4]);                    \
+      const float a[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};                        \
+      const float c[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};                        \
+      _Pragma("unroll") for (int i = 0; i < 8; ++i)                                               \
+        _Pragma("unroll") for (int j = 0; j < 8; ++j) {                                           \
+          const float prod = a[i] * c[j];                                                         \
+          acc[i][j] = acc[i][j] + prod;                                                           \
+        }                                                                                         \
+    }                                                                                             \
+  } while (0)
+
+  // nc = B / 16 is even (B is 64, 128 or 256).  Chunk c + 1 is copied while
+  // chunk c is multiplied; then a wait for this wave's copies (vmcnt 0) and
+  // a barrier make every wave's copies visible and order the refill of a
+  // buffer after every read of it.  No copy is in flight where the loop
+  // closes, so the compiler can tell each buffer's reads from the other
+  // buffer's copies and adds no wait of its own before them.
+  const int nc = B / kUpBK;
+  SDQ_UP_FILL(As0, Bs0, 0);
+  __builtin_amdgcn_s_waitcnt(0xF70);
+  lds_barrier();
+  for (int c = 0; c < nc; c += 2) {
+    SDQ_UP_FILL(As1, Bs1, c + 1);
+    SDQ_UP_MUL(As0, Bs0);
+    __builtin_amdgcn_s_waitcnt(0xF70);
+    lds_barrier();
+    if (c + 2 < nc) SDQ_UP_FILL(As0, Bs0, c + 2);
+    SDQ_UP_MUL(As1, Bs1);
+    __builtin_amdgcn_s_waitcnt(0xF70);
+    lds_barrier();
   }
+#undef SDQ_UP_FILL
+#undef SDQ_UP_MUL
   // Store: sample j -> m = (j / (P-1)) * P + j % (P-1) + 1; rows are contiguous.
   float mx[8];
 #pragma unroll
