@@ -570,6 +570,23 @@ def traffic_probe(torch, P, synth, SG) -> None:
         torch.cuda.empty_cache()
 
 
+def encoder_probe(torch, P, synth, SG) -> None:
+    """A short eager run for hardware-counter passes over the encoder: three
+    sdq_quantize calls on the LLaMA-7B down_proj layer (4096 x 11008, OSR 1.5,
+    binary), after the weight generation.  Prints what it ran."""
+    wl = synth.workload(2)
+    lin = wl.linears[0]
+    w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
+    L = P.sdq_layout_init(w.shape[0], w.shape[1], wl.osr, wl.levels)
+    codes = torch.empty(P.sdq_codes_bytes(L), dtype=torch.uint8, device="cuda")
+    scales = torch.empty(L.n, dtype=torch.float32, device="cuda")
+    ws = torch.empty(P.sdq_quantize_workspace_bytes(L), dtype=torch.uint8, device="cuda")
+    for _ in range(3):
+        P.sdq_quantize(w, L, codes, scales, ws)
+    torch.cuda.synchronize()
+    print(f"encoder probe: 3 x sdq_quantize {lin.n}x{lin.k} osr {wl.osr} levels {wl.levels}", flush=True)
+
+
 def P_codes_row_bytes(L):
     return L.n_chunks * 16
 
@@ -583,6 +600,8 @@ def main() -> int:
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--traffic-probe", action="store_true",
                     help="short eager run for rocprofv3 --pmc passes (prints no JSON line)")
+    ap.add_argument("--encoder-probe", action="store_true",
+                    help="three encoder calls on the headline layer, for rocprofv3 --pmc passes")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -600,6 +619,9 @@ def main() -> int:
     torch.cuda.synchronize()
     if args.traffic_probe:
         traffic_probe(torch, P, synth, SG)
+        return 0
+    if args.encoder_probe:
+        encoder_probe(torch, P, synth, SG)
         return 0
     t_start = time.perf_counter()
     dec = bench_decode(torch, P, synth, SG, args.steps, args.warmup)
