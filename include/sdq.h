@@ -43,7 +43,7 @@ typedef enum {
   SDQ_ERR_WORKSPACE = -6,  /* workspace pointer missing or too small             */
   SDQ_ERR_HIP = -7,        /* a HIP runtime call failed                          */
   SDQ_ERR_NOMEM = -8,      /* the coefficient-table cache could not allocate     */
-  SDQ_ERR_UNSUPPORTED = -9, /* a valid request this build does not implement     */
+  SDQ_ERR_UNSUPPORTED = -9, /* a valid request the library does not implement   */
   SDQ_ERR_NOT_SPD = -10    /* a Hessian (plus damping) is not positive definite  */
 } sdq_status;
 
@@ -182,14 +182,14 @@ sdq_status sdq_quantize(const float* w_dev, const sdq_layout* layout, void* code
 sdq_status sdq_quantize_check(const void* workspace_dev, void* stream);
 
 /*
- * Block compensation of Algorithm 1 (lines 3-8; GPTQ-style).  All in fp64.
+ * Block compensation of Algorithm 1 (its GPTQ-style block loop).  All in fp64.
  *
  * sdq_hessian_accumulate: H += 2 X^T X (the Hessian of Algorithm 1's caption
  * without its damping), for calibration activations x_dev (fp32 [m x k],
  * row-major) and h_dev (fp64 [k x k], row-major, both triangles written;
  * zero it before the first call).  Errors: SDQ_ERR_ARG.
  *
- * sdq_hessian_factor: Algorithm 1 line 4, u_dev = Cholesky((H + lambda I)^-1)^T,
+ * sdq_hessian_factor: Algorithm 1's factor step, u_dev = Cholesky((H + lambda I)^-1)^T,
  * the upper factor U with U^T U = (H + lambda I)^-1 (fp64 [k x k], lower part
  * zero), computed without forming the inverse (a blocked Cholesky of the
  * index-reversed matrix and a recursive blocked triangular inverse).  h_dev: symmetric
@@ -235,7 +235,7 @@ sdq_status sdq_quantize_compensated(const float* w_dev, const sdq_layout* layout
 size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
 
 /*
- * y = x W_hat^T for the encoded layer (Fig. 5 and Algorithm 1 line 6: W_hat is
+ * y = x W_hat^T for the encoded layer (Fig. 5 and Algorithm 1's reconstruction: W_hat is
  * the decimated, Hadamard-restored reconstruction of the codes).  Computed as
  * x_tilde = per-block (x_b Had) D^T (D: Resample back to B), then
  * y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j].  Equivalent to

@@ -18,7 +18,7 @@ Contents (each function cites the passage it follows):
 * ``encoder``     -- weight encoding: block Hadamard, Resample up, per-row
                      scale, Sigma-Delta scan (Algorithm 1, ``SDQuant``);
 * ``linear``      -- the fp64 plain definition y = x W_hat^T of the
-                     dequantized linear (Algorithm 1 line 6 reconstruction,
+                     dequantized linear (Algorithm 1's reconstruction,
                      Fig. 5) and the activation-expansion identity;
 * ``layout``      -- the packed code format of the library's C header,
                      re-implemented independently, and Eq. 14's ratio;

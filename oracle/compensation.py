@@ -2,12 +2,12 @@
 
 Algorithm 1 takes the inverse Hessian H^-1 = (2 X X^T + lambda I)^-1 of the
 layer's calibration inputs X, replaces it by its upper Cholesky factor U
-(H^-1 = U^T U, line 4), and walks the weight in blocks of B columns
-(lines 5-8): the block is quantized (Had, SDQuant, Had^T), its error E is
+(H^-1 = U^T U), and walks the weight in blocks of B columns: the
+block is quantized (Had, SDQuant, Had^T), its error E is
 formed, and the columns after it are corrected so that the layer output on
 X loses as little as possible.
 
-Readings (see the project notes for the measurements behind them):
+Readings:
 
 * the update.  The printed correction W_F -= E U[Q, F] (Q the block's
   columns, F the later ones) omits the normalisation that GPTQ's block
@@ -51,7 +51,7 @@ def hessian_fp64(x: np.ndarray) -> np.ndarray:
 
 
 def inverse_cholesky_upper(h: np.ndarray, lam: float) -> np.ndarray:
-    """Algorithm 1 line 4: U = Cholesky((H + lambda I)^-1)^T, so U^T U = (H + lambda I)^-1."""
+    """Algorithm 1, factor step: U = Cholesky((H + lambda I)^-1)^T, so U^T U = (H + lambda I)^-1."""
     h = np.asarray(h, dtype=np.float64)
     hinv = np.linalg.inv(h + lam * np.eye(h.shape[0]))
     hinv = 0.5 * (hinv + hinv.T)

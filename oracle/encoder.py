@@ -15,10 +15,10 @@ For every row r of W (N x K) and every block b of B consecutive columns
 4. the Sigma-Delta recursion (Eq. 7-8, ``sigma_delta.scan_f32``) runs over the
    M samples of each (row, block) from a zero state, giving codes in {-1, +1}
    (binary, Eq. 4) or {-1, 0, +1} (ternary, Eq. 6);
-5. codes are placed block-major: C[r, b*M + m] (Algorithm 1 line 6 writes block
+5. codes are placed block-major: C[r, b*M + m] (Algorithm 1 writes block
    i of Q_out to columns i*osr ... (i+B)*osr).
 
-The GPTQ-style compensation of Algorithm 1 (lines 7-8) is not applied: the
+The GPTQ-style compensation of Algorithm 1 (its column updates) is not applied: the
 raw weights are encoded.
 """
 from __future__ import annotations

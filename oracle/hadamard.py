@@ -2,7 +2,7 @@
 
 Section 3.3 defines a Hadamard matrix by H H^T = n I and builds it with the
 Sylvester recursion H_2k = [[H_k, H_k], [H_k, -H_k]] (Eq. 13).  Algorithm 1
-(line 6) multiplies each B-column weight block by ``Had`` before Sigma-Delta
+multiplies each B-column weight block by ``Had`` before Sigma-Delta
 quantization and by ``Had^T`` afterwards, so ``Had`` must be orthogonal.
 Three choices of ``Had`` (one B x B matrix shared by every block, as
 Algorithm 1's input list has it):

@@ -1,6 +1,6 @@
 """The dequantized linear layer in fp64.
 
-Plain definition.  Algorithm 1 line 6 defines the dequantized block as
+Plain definition.  Algorithm 1 defines the dequantized block as
 Q[:, block b] = Resample(Y_b, B) * Had^T, where Y_b are the block's
 Sigma-Delta outputs (codes times the row scale) and ``Resample`` brings the M
 upsampled samples back to B.  The layer output is the plain product

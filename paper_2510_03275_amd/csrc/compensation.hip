@@ -1,7 +1,7 @@
-// Block compensation of Algorithm 1 (lines 3-8), fp64 on the device.
+// Block compensation of Algorithm 1 (the block loop), fp64 on the device.
 //
 //   hessian  H += 2 X^T X for calibration activations X (m x K).
-//   factor   U = Cholesky((H + lambda I)^-1)^T (line 4), upper, U^T U = (H + lambda I)^-1.
+//   factor   U = Cholesky((H + lambda I)^-1)^T, upper, U^T U = (H + lambda I)^-1.
 //            Computed without forming the inverse: with J the index reversal,
 //            J (H + lambda I) J = L L^T (blocked Cholesky, 64-column panels)
 //            and U = J L^-1 J (blocked triangular inverse), because

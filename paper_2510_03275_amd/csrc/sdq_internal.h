@@ -124,7 +124,7 @@ sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* sc
                                    const sdq_layout* L, float* y, bool accumulate, void* ws,
                                    hipStream_t stream);
 
-// Block compensation (Algorithm 1 lines 3-8), fp64.
+// Block compensation (Algorithm 1's block loop), fp64.
 sdq_status launch_hessian_accumulate(const float* x, int64_t m, int64_t k, double* h, hipStream_t stream);
 size_t hessian_factor_ws_bytes(int64_t k);
 sdq_status launch_hessian_factor(const double* h, int64_t k, double lam, double* u, void* ws,

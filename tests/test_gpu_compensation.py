@@ -1,4 +1,4 @@
-"""GPU parity of the block compensation (Algorithm 1 lines 3-8) against the
+"""GPU parity of the block compensation (Algorithm 1's block loop) against the
 oracle: the Hessian, the Cholesky factor of its damped inverse, and the
 compensated codes."""
 import numpy as np

@@ -1,4 +1,4 @@
-"""Pins of the oracle's block compensation (Algorithm 1 lines 3-8)."""
+"""Pins of the oracle's block compensation (Algorithm 1's block loop)."""
 import numpy as np
 import pytest
 
@@ -72,7 +72,7 @@ def test_block_update_is_the_obs_optimum():
 
 
 def test_compensation_lowers_the_calibration_loss():
-    # The point of lines 7-8: on correlated inputs the compensated codes fit
+    # The point of the column updates: on correlated inputs the compensated codes fit
     # the layer output on X better than the plain ones (about 2x measured).
     w = synth.weight_rows(7, 0, 24, 768, 0.02, True)
     x = _lowrank_x(4096, 768, 8)

@@ -1,4 +1,4 @@
-"""Pins of the oracle's fp64 linear (Algorithm 1 line 6 reconstruction, Fig. 5)."""
+"""Pins of the oracle's fp64 linear (Algorithm 1's reconstruction, Fig. 5)."""
 import numpy as np
 import pytest
 from scipy import signal
