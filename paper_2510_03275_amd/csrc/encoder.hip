@@ -410,25 +410,37 @@ __device__ inline void repack_all(const uint32_t (&w)[5], uint32_t (&out)[4], st
   (repack_byte<Ps>(w, out), ...);
 }
 
-// total = (n_pad / 64) * nch3 * 64 threads' work; rows past n are zero bytes.
-__global__ void repack_base3_kernel(const uint32_t* __restrict__ fields, int64_t n, int64_t nch2,
-                                    int64_t nch3, int64_t total, uint4* __restrict__ out) {
+// Four base-3 slots per thread (the inverse of the unpack below): five whole
+// 2-bit chunks (20 field words, 320 codes) in, four 16-byte slots out, each
+// access 1 KB contiguous per wave.  total = n_pad * ceil(nch3 / 4); field
+// words past the last chunk are padding (code 0); rows past n get zero bytes.
+__global__ void repack_base3_kernel(const uint4* __restrict__ fields, int64_t n, int64_t nch2,
+                                    int64_t nch3, int64_t quads, int64_t total, uint4* __restrict__ out) {
   for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
        e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
     const int64_t rr = e % kPanel;
-    const int64_t c3 = (e / kPanel) % nch3;
-    const int64_t pn = e / (kPanel * nch3);
-    uint32_t o[4] = {0u, 0u, 0u, 0u};
-    if (pn * kPanel + rr < n) {
-      uint32_t w[5];
+    const int64_t g4 = (e / kPanel) % quads;
+    const int64_t pn = e / (kPanel * quads);
+    const bool row_ok = pn * kPanel + rr < n;
+    uint32_t f[20];
 #pragma unroll
-      for (int i = 0; i < 5; ++i) {
-        const int64_t gw = c3 * 5 + i;               // field words past the last chunk: padding, code 0
-        w[i] = gw < nch2 * 4 ? fields[((pn * nch2 + gw / 4) * kPanel + rr) * 4 + gw % 4] : 0u;
-      }
-      repack_all(w, o, std::make_integer_sequence<int, 16>{});
+    for (int c = 0; c < 5; ++c) {
+      const int64_t chunk = 5 * g4 + c;
+      const uint4 v = row_ok && chunk < nch2 ? fields[(pn * nch2 + chunk) * kPanel + rr]
+                                             : make_uint4(0u, 0u, 0u, 0u);
+      f[4 * c] = v.x; f[4 * c + 1] = v.y; f[4 * c + 2] = v.z; f[4 * c + 3] = v.w;
     }
-    out[e] = make_uint4(o[0], o[1], o[2], o[3]);
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t g = 4 * g4 + j;
+      if (g >= nch3) break;
+      uint32_t o[4] = {0u, 0u, 0u, 0u};
+      if (row_ok) {
+        const uint32_t w[5] = {f[5 * j], f[5 * j + 1], f[5 * j + 2], f[5 * j + 3], f[5 * j + 4]};
+        repack_all(w, o, std::make_integer_sequence<int, 16>{});
+      }
+      out[(pn * nch3 + g) * kPanel + rr] = make_uint4(o[0], o[1], o[2], o[3]);
+    }
   }
 }
 
@@ -443,11 +455,15 @@ __device__ inline void unpack_all(const uint32_t (&by)[4], const uint32_t* pat, 
   (unpack_byte<Ps>(by, pat, w), ...);
 }
 
-// groups = max(nch3, ceil(4 nch2 / 5)) five-word groups per row, so that every
-// field word (padding ones included) is written; rows past n are zero.
+// Four base-3 groups (16 bytes, 80 codes each) per thread: 320 codes are
+// exactly five 2-bit chunks of four words, so every load and every store is
+// one whole 16-byte slot (a wave's accesses are 1 KB contiguous).  quads =
+// ceil(groups / 4) with groups = max(nch3, ceil(4 nch2 / 5)), so every chunk
+// of the field layout is written; groups past nch3 and rows past n give
+// zero fields.
 __global__ __launch_bounds__(256) void unpack_base3_kernel(const uint4* __restrict__ b3, int64_t n,
-                                                           int64_t nch2, int64_t nch3, int64_t groups,
-                                                           int64_t total, uint32_t* __restrict__ fields) {
+                                                           int64_t nch2, int64_t nch3, int64_t quads,
+                                                           int64_t total, uint4* __restrict__ fields) {
   // Byte -> its five codes as 2-bit fields: digit i of q is the integer part
   // of 3 r after i + 1 steps of r <- fraction part of 3 r, from r = q / 256.
   __shared__ uint32_t pat[256];
@@ -465,18 +481,37 @@ __global__ __launch_bounds__(256) void unpack_base3_kernel(const uint4* __restri
   for (int64_t e = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; e < total;
        e += static_cast<int64_t>(gridDim.x) * blockDim.x) {
     const int64_t rr = e % kPanel;
-    const int64_t g = (e / kPanel) % groups;
-    const int64_t pn = e / (kPanel * groups);
-    uint32_t w[5] = {0u, 0u, 0u, 0u, 0u};
-    if (pn * kPanel + rr < n && g < nch3) {
-      const uint4 v = b3[(pn * nch3 + g) * kPanel + rr];
-      const uint32_t by[4] = {v.x, v.y, v.z, v.w};
-      unpack_all(by, pat, w, std::make_integer_sequence<int, 16>{});
+    const int64_t g4 = (e / kPanel) % quads;
+    const int64_t pn = e / (kPanel * quads);
+    const bool row_ok = pn * kPanel + rr < n;
+    uint4 v[4];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const int64_t g = 4 * g4 + j;
+      v[j] = row_ok && g < nch3 ? b3[(pn * nch3 + g) * kPanel + rr] : make_uint4(0u, 0u, 0u, 0u);
+    }
+    uint32_t w[4][5];
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+#pragma unroll
+      for (int i = 0; i < 5; ++i) w[j][i] = 0u;
+      // Slots past nch3 and rows past n are not read: their fields stay zero
+      // (code 0), where unpacking a zero byte would give five -1 codes.
+      const int64_t g = 4 * g4 + j;
+      if (row_ok && g < nch3) {
+        const uint32_t by[4] = {v[j].x, v[j].y, v[j].z, v[j].w};
+        unpack_all(by, pat, w[j], std::make_integer_sequence<int, 16>{});
+      }
     }
 #pragma unroll
-    for (int i = 0; i < 5; ++i) {
-      const int64_t gw = g * 5 + i;
-      if (gw < nch2 * 4) fields[((pn * nch2 + gw / 4) * kPanel + rr) * 4 + gw % 4] = w[i];
+    for (int c = 0; c < 5; ++c) {
+      const int64_t chunk = 5 * g4 + c;
+      if (chunk < nch2) {
+        uint32_t o[4];
+#pragma unroll
+        for (int t = 0; t < 4; ++t) o[t] = w[(4 * c + t) / 5][(4 * c + t) % 5];
+        fields[(pn * nch2 + chunk) * kPanel + rr] = make_uint4(o[0], o[1], o[2], o[3]);
+      }
     }
   }
 }
@@ -486,10 +521,11 @@ __global__ __launch_bounds__(256) void unpack_base3_kernel(const uint4* __restri
 sdq_status launch_unpack_base3(const void* codes, const sdq_layout* L, uint32_t* fields, hipStream_t stream) {
   const sdq_layout F = fields_view(L);
   const int64_t groups = std::max<int64_t>(L->n_chunks, (4 * F.n_chunks + 4) / 5);
-  const int64_t total = L->n_pad * groups;
+  const int64_t quads = (groups + 3) / 4;
+  const int64_t total = L->n_pad * quads;
   const unsigned grid = static_cast<unsigned>(std::min<int64_t>((total + 255) / 256, 16384));
   unpack_base3_kernel<<<grid, 256, 0, stream>>>(static_cast<const uint4*>(codes), L->n, F.n_chunks, L->n_chunks,
-                                                groups, total, fields);
+                                                quads, total, reinterpret_cast<uint4*>(fields));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "base-3 unpack launch");
   return SDQ_OK;
@@ -558,10 +594,11 @@ sdq_status launch_quantize(const float* w, const sdq_layout* L, const Tables* T,
 
 sdq_status launch_repack_base3(const uint32_t* fields, const sdq_layout* L, void* codes, hipStream_t stream) {
   const sdq_layout F = fields_view(L);
-  const int64_t total = L->n_pad * L->n_chunks;
+  const int64_t quads = (L->n_chunks + 3) / 4;
+  const int64_t total = L->n_pad * quads;
   const unsigned grid = static_cast<unsigned>(std::min<int64_t>((total + 255) / 256, 16384));
-  repack_base3_kernel<<<grid, 256, 0, stream>>>(fields, L->n, F.n_chunks, L->n_chunks, total,
-                                                static_cast<uint4*>(codes));
+  repack_base3_kernel<<<grid, 256, 0, stream>>>(reinterpret_cast<const uint4*>(fields), L->n, F.n_chunks,
+                                                L->n_chunks, quads, total, static_cast<uint4*>(codes));
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "base-3 repack launch");
   return SDQ_OK;
