@@ -20,6 +20,11 @@
  *    work is enqueued asynchronously on it; host-side argument errors are
  *    returned before anything is enqueued.
  *  - Matrices are row-major and densely packed unless stated otherwise.
+ *  - The weights, activations, packed codes and workspaces passed to
+ *    sdq_quantize, sdq_quantize_compensated, sdq_linear,
+ *    sdq_expand_activations and sdq_linear_expanded are read and written in
+ *    16-byte vectors and must be 16-byte aligned (every hipMalloc or PyTorch
+ *    allocation is); a misaligned one is rejected with SDQ_ERR_ARG.
  *  - Functions return SDQ_OK or a negative sdq_status; sdq_last_error()
  *    gives a message for the last failure on the calling thread.
  */

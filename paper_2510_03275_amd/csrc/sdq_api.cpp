@@ -338,6 +338,9 @@ double sdq_compression_ratio(const sdq_layout* L) {
   return bits * (static_cast<double>(L->m_up) / L->block) / 16.0;
 }
 
+// Weights, activations, codes and workspaces are accessed in 16-byte vectors.
+static bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
 size_t sdq_quantize_workspace_bytes(const sdq_layout* L) {
   if (check_layout(L) != SDQ_OK) return 0;
   return quant_ws_layout(L, nullptr, nullptr);
@@ -352,6 +355,8 @@ sdq_status sdq_quantize(const float* w, const sdq_layout* L, void* codes, float*
   const size_t need = quant_ws_layout(L, nullptr, nullptr);
   if (!ws || ws_bytes < need)
     return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned16(w) || !aligned16(codes) || !aligned16(ws))
+    return set_error(SDQ_ERR_ARG, "w, codes and the workspace must be 16-byte aligned");
   if (L->n == 0) return SDQ_OK;
   const Tables* T = nullptr;
   st = get_tables(L, &T);
@@ -420,6 +425,8 @@ sdq_status sdq_quantize_compensated(const float* w, const sdq_layout* L, const d
   const size_t need = comp_ws_bytes(L);
   if (!ws || ws_bytes < need)
     return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned16(w) || !aligned16(codes) || !aligned16(ws))
+    return set_error(SDQ_ERR_ARG, "w, codes and the workspace must be 16-byte aligned");
   if (L->n == 0) return SDQ_OK;
   const Tables* T = nullptr;
   st = get_tables(L, &T);
@@ -462,6 +469,7 @@ static sdq_status linear_common(const sdq_layout* L, int64_t m, size_t ws_bytes,
   const size_t need = linear_ws_bytes(L, m);
   if (!ws || ws_bytes < need)
     return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned16(ws)) return set_error(SDQ_ERR_ARG, "workspace is not 16-byte aligned");
   return SDQ_OK;
 }
 
@@ -469,6 +477,7 @@ static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_
                               void* ws, float* y_zero, void* stream) {
   if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
   if (!x) return set_error(SDQ_ERR_ARG, "x is NULL");
+  if (!aligned16(x)) return set_error(SDQ_ERR_ARG, "x is not 16-byte aligned");
   const sdq_layout F = fields_view(L);
   const sdq_layout* P = needs_unpack(L, m) ? &F : L;
   const Tables* T = nullptr;
@@ -483,6 +492,7 @@ static sdq_status contract_impl(int64_t m, const void* codes, const float* scale
                                 const sdq_layout* L, float* y, bool accumulate, void* ws,
                                 bool y_ready, void* stream) {
   if (!codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+  if (!aligned16(codes)) return set_error(SDQ_ERR_ARG, "codes are not 16-byte aligned");
   hipStream_t s = static_cast<hipStream_t>(stream);
   const sdq_layout F = fields_view(L);
   const sdq_layout* P = L;
@@ -521,6 +531,7 @@ sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
   if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
   if (m == 0 || L->n == 0) return SDQ_OK;
   if (!x || !codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+  if (!aligned16(x) || !aligned16(codes)) return set_error(SDQ_ERR_ARG, "x and codes must be 16-byte aligned");
   st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK) return st;
   // Decode: the expansion also zeroes y when the GEMV will add into it.

@@ -132,6 +132,22 @@ def test_quantize_and_linear_reject_bad_arguments_without_gpu_work():
                           ctypes.byref(L), ctypes.c_void_p(16), 0, None, 0, None) == -6
     assert lib.sdq_linear_expanded(1, ctypes.c_void_p(16), ctypes.c_void_p(16), ctypes.byref(L),
                                    ctypes.c_void_p(16), 1, None, 0, None) == -6
+    # misaligned weights, activations, codes or workspace: rejected before anything is enqueued
+    lneed = lib.sdq_linear_workspace_bytes(ctypes.byref(L), 1)
+    assert lib.sdq_quantize(ctypes.c_void_p(24), ctypes.byref(L), ctypes.c_void_p(16),
+                            ctypes.c_void_p(16), ctypes.c_void_p(16), need, None) == -1
+    assert lib.sdq_quantize(ctypes.c_void_p(16), ctypes.byref(L), ctypes.c_void_p(20),
+                            ctypes.c_void_p(16), ctypes.c_void_p(16), need, None) == -1
+    assert lib.sdq_quantize(ctypes.c_void_p(16), ctypes.byref(L), ctypes.c_void_p(16),
+                            ctypes.c_void_p(16), ctypes.c_void_p(40), need, None) == -1
+    assert lib.sdq_linear(ctypes.c_void_p(18), 0, 1, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                          ctypes.byref(L), ctypes.c_void_p(16), 0, ctypes.c_void_p(16), lneed, None) == -1
+    assert lib.sdq_linear(ctypes.c_void_p(16), 0, 1, ctypes.c_void_p(24), ctypes.c_void_p(16),
+                          ctypes.byref(L), ctypes.c_void_p(16), 0, ctypes.c_void_p(16), lneed, None) == -1
+    assert lib.sdq_linear(ctypes.c_void_p(16), 0, 1, ctypes.c_void_p(16), ctypes.c_void_p(16),
+                          ctypes.byref(L), ctypes.c_void_p(16), 0, ctypes.c_void_p(8), lneed, None) == -1
+    assert lib.sdq_linear_expanded(1, ctypes.c_void_p(16), ctypes.c_void_p(16), ctypes.byref(L),
+                                   ctypes.c_void_p(16), 1, ctypes.c_void_p(4), lneed, None) == -1
     # m == 0 is a successful no-op
     assert lib.sdq_linear(None, 0, 0, None, None, ctypes.byref(L), None, 0, None, 0, None) == 0
     assert lib.sdq_linear(None, 0, 0, None, None, ctypes.byref(L), None, 1, None, 0, None) == 0
