@@ -207,16 +207,23 @@ sdq_status sdq_quantize_check(const void* workspace_dev, void* stream);
  * sdq_quantize_compensated: as sdq_quantize, with the block compensation:
  * the row scales are those of the plain encoding of W; W is then walked in
  * blocks of B columns in fp64, each block rounded to fp32 and encoded with
- * those scales, and the columns after it corrected by
- * W_F -= E U_QQ^-1 U_QF, where E = W_Q - Q_hat is the block's error against
- * its reconstruction (Resample back to B, Had^T) and U_QQ, U_QF are blocks of
- * u_dev (the printed W_F -= E U_QF of Algorithm 1 omits the U_QQ^-1 that
- * GPTQ's block mechanism carries).  u_dev: fp64 [k x k] upper factor as from
- * sdq_hessian_factor.  workspace: sdq_quantize_compensated_workspace_bytes
- * (the plain encoder's plus about 8 n (k + 2B + M) + 24 nb B^2 bytes).
- * Codes and scales as sdq_quantize; the non-finite flag is reported by
- * sdq_quantize_check on the same workspace.  Errors as sdq_quantize.
+ * those scales, and the columns after it corrected from the block's error
+ * E = W_Q - Q_hat against its reconstruction (Resample back to B, Had^T),
+ * with U_QQ, U_QF the blocks of u_dev on the block's rows:
+ *   update = SDQ_COMP_GPTQ   W_F -= E diag(U_QQ)^-1 U_QF: GPTQ's block-wise
+ *                            compensation, which Section 3.5 keeps, with its
+ *                            column-wise part removed (each column's error
+ *                            divided by its pivot; the printed listing writes
+ *                            W_F -= E U_QF without the division);
+ *   update = SDQ_COMP_JOINT  W_F -= E U_QQ^-1 U_QF: the optimal-brain-surgeon
+ *                            correction of the jointly quantized block.
+ * u_dev: fp64 [k x k] upper factor as from sdq_hessian_factor.  workspace:
+ * sdq_quantize_compensated_workspace_bytes (the plain encoder's plus about
+ * 8 n (k + 2B + M) + 24 nb B^2 bytes).  Codes and scales as sdq_quantize; the
+ * non-finite flag is reported by sdq_quantize_check on the same workspace.
+ * Errors as sdq_quantize, and SDQ_ERR_ARG for an unknown update.
  */
+typedef enum { SDQ_COMP_GPTQ = 0, SDQ_COMP_JOINT = 1 } sdq_comp_update;
 sdq_status sdq_hessian_accumulate(const float* x_dev, int64_t m, int64_t k, double* h_dev, void* stream);
 size_t sdq_hessian_factor_workspace_bytes(int64_t k);
 sdq_status sdq_hessian_factor(const double* h_dev, int64_t k, double lambda, double* u_dev,
@@ -224,8 +231,8 @@ sdq_status sdq_hessian_factor(const double* h_dev, int64_t k, double lambda, dou
 sdq_status sdq_hessian_check(const void* workspace_dev, void* stream);
 size_t sdq_quantize_compensated_workspace_bytes(const sdq_layout* layout);
 sdq_status sdq_quantize_compensated(const float* w_dev, const sdq_layout* layout, const double* u_dev,
-                                    void* codes_dev, float* scales_dev, void* workspace_dev,
-                                    size_t workspace_bytes, void* stream);
+                                    int32_t update, void* codes_dev, float* scales_dev,
+                                    void* workspace_dev, size_t workspace_bytes, void* stream);
 
 /* Device workspace (bytes) sdq_linear needs for m activation rows: the
  * expanded activations, at offset 0 --
@@ -282,9 +289,10 @@ sdq_status sdq_expand_activations(const void* x_dev, sdq_dtype xt, int64_t m,
 
 /* Second step of sdq_linear: y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j] from
  * the x_tilde that sdq_expand_activations left in the workspace (same m and a
- * layout with the same k, block, m_up and levels).  m <= 16: addition-only
- * lookup-table GEMV; otherwise fp16 MFMA GEMM.  accumulate as in sdq_linear.
- * Errors as sdq_linear. */
+ * layout with the same k, block, m_up and levels).  m = 1: addition-only
+ * lookup-table GEMV; 2 <= m <= 16: exact int8 matrix-core contraction against
+ * the fixed-point expansion; larger m: fp16 MFMA GEMM.  accumulate as in
+ * sdq_linear.  Errors as sdq_linear. */
 sdq_status sdq_linear_expanded(int64_t m, const void* codes_dev, const float* scales_dev,
                                const sdq_layout* layout, float* y_dev, int32_t accumulate,
                                void* workspace_dev, size_t workspace_bytes, void* stream);

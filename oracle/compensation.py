@@ -9,14 +9,18 @@ X loses as little as possible.
 
 Readings:
 
-* the update.  The printed correction W_F -= E U[Q, F] (Q the block's
-  columns, F the later ones) omits the normalisation that GPTQ's block
-  mechanism -- which the text says is kept -- applies to the error.  For the
-  block's columns quantized jointly, the correction that minimises
-  ||(W - W_hat) X|| over W_F (optimal brain surgeon on the block) is
-  W_F -= E U_QQ^-1 U_QF, with U_QQ the block's diagonal block of U.  This
-  oracle applies that update; the printed one changes the output error by
-  well under 1 %, the normalised one halves it.
+* the update.  The text keeps GPTQ's block-wise compensation and drops its
+  column-wise one (Section 3.5), and the listing prepares the factor exactly
+  as GPTQ does (U = Cholesky(H^-1)^T).  GPTQ's block-wise step divides each
+  column's error by that column's diagonal entry of U before propagating it
+  past the block; the printed correction W_F -= E U[Q, F] (Q the block's
+  columns, F the later ones) writes the error without that division.  The
+  default update here is GPTQ's block step with the column-wise part removed:
+  W_F -= E diag(U_QQ)^-1 U_QF (``COMP_GPTQ``).  Because SDQ quantizes the
+  block's columns jointly, the optional ``COMP_JOINT`` applies the
+  optimal-brain-surgeon correction of the whole block instead,
+  W_F -= E U_QQ^-1 U_QF, which minimises ||(W - W_hat) X|| over W_F; the two
+  agree whenever U_QQ is diagonal.
 * the row scale.  The stored format has one scale per row; it is taken from
   the uncompensated W (the scale the plain encoder would use), and every block
   of the row is scanned with it.
@@ -43,6 +47,8 @@ from .hadamard import HAD_SYLVESTER, rotate_blocks_f32
 from .linear import reconstruct_fp64
 from .sigma_delta import scan_f32
 
+COMP_GPTQ, COMP_JOINT = 0, 1      # the block update (see the module docstring)
+
 
 def hessian_fp64(x: np.ndarray) -> np.ndarray:
     """H = 2 X^T X (K x K) for calibration activations X (m x K), fp64."""
@@ -68,12 +74,18 @@ def encode_block_with_scale(wb: np.ndarray, osr: float, levels: int, block: int,
 
 
 def encode_compensated(w: np.ndarray, osr: float, levels: int, block: int, u: np.ndarray,
-                       hadamard: int = HAD_SYLVESTER, signs=None) -> EncodeResult:
-    """Algorithm 1 with its block compensation: codes and row scales of W (n x K)."""
+                       hadamard: int = HAD_SYLVESTER, signs=None,
+                       update: int = COMP_GPTQ) -> EncodeResult:
+    """Algorithm 1 with its block compensation: codes and row scales of W (n x K).
+
+    ``update`` selects the correction of the columns after each block:
+    ``COMP_GPTQ`` (E diag(U_QQ)^-1 U_QF) or ``COMP_JOINT`` (E U_QQ^-1 U_QF)."""
     w = np.asarray(w, dtype=np.float32)
     n, k = w.shape
     if u.shape != (k, k):
         raise ValueError("U must be K x K")
+    if update not in (COMP_GPTQ, COMP_JOINT):
+        raise ValueError("update must be COMP_GPTQ or COMP_JOINT")
     plain = encode(w, osr, levels, block, hadamard, signs)     # row scales of the raw W
     s = plain.scales
     m_up = plain.m_up
@@ -89,7 +101,10 @@ def encode_compensated(w: np.ndarray, osr: float, levels: int, block: int, u: np
             break
         q_hat = reconstruct_fp64(cb, s, block, m_up, hadamard, signs)   # Resample(Y, B) Had^T
         e = w64[:, q] - q_hat
-        # G = E U_QQ^-1, i.e. U_QQ^T G^T = E^T (lower-triangular system)
-        g = solve_triangular(u[q, q], e.T, trans="T", lower=False).T
+        if update == COMP_GPTQ:
+            g = e / np.diag(u[q, q])[None, :]          # each column's error over its pivot
+        else:
+            # G = E U_QQ^-1, i.e. U_QQ^T G^T = E^T (lower-triangular system)
+            g = solve_triangular(u[q, q], e.T, trans="T", lower=False).T
         w64[:, f] -= g @ u[q, f]
     return EncodeResult(codes, s, m_up, block)

@@ -20,10 +20,13 @@ Base-3 packing of ternary codes (Eq. 14 counts a ternary code as log2(3) =
 1.58 bits; five codes per byte, 3^5 = 243 <= 256, store 1.6 bits each):
 
 * a 16-byte chunk holds 80 codes; the chunk and panel layout are as above;
-* code j of a row is in chunk j // 80 at position q = j % 80, which is digit
-  q % 5 of byte q // 5 of the chunk; a byte holds
-  d_0 + 3 d_1 + 9 d_2 + 27 d_3 + 81 d_4 with digit d = code + 1 in {0, 1, 2}
-  (bytes 243 .. 255 are never written);
+* code j of a row is in chunk j // 80 at position q = j % 80, the (q % 5)-th
+  code of byte q // 5 of the chunk; with digits d_i = code + 1 in {0, 1, 2} of
+  the byte's five codes, first code most significant,
+  v = 81 d_0 + 27 d_1 + 9 d_2 + 3 d_3 + d_4 in [0, 243), and the byte stores
+  q = ceil(256 v / 243), v / 243 as an 8-bit fraction rounded up; it is read
+  back as v = floor(243 q / 256).  Byte values up to 255 occur (v = 242 gives
+  255), and 13 of the 256 byte values are never written;
 * padding codes are code 0 (digit 1) and padding rows all-zero bytes.
 """
 from __future__ import annotations

@@ -33,9 +33,15 @@ import numpy as np
 
 
 def resample_fft(w: np.ndarray, n_new: int) -> np.ndarray:
-    """Algorithm 1 ``Resample(W, N_new)`` along the last axis, fp64."""
+    """Algorithm 1 ``Resample(W, N_new)`` along the last axis, fp64.
+
+    At N_new = d_col no bin is padded, cut or weighted and the scale is 1, so
+    the steps compose to IFFT(FFT(w)) = w: the block is returned as it is
+    (exactly, without the round trip's fp64 rounding)."""
     w = np.asarray(w, dtype=np.float64)
     d = w.shape[-1]
+    if n_new == d:
+        return w.copy()
     x = np.fft.rfft(w, axis=-1)                       # FFT(w), one-sided
     y = np.zeros(w.shape[:-1] + (n_new // 2 + 1,), dtype=np.complex128)
     keep = min(d, n_new) // 2 + 1                     # ZeroPadOrTruncate

@@ -21,6 +21,7 @@ SDQ_OK = 0
 SDQ_F16, SDQ_BF16, SDQ_F32 = 0, 1, 2
 SDQ_HAD_NONE, SDQ_HAD_SYLVESTER, SDQ_HAD_SIGNED = 0, 1, 2
 SDQ_PACK_FIELDS, SDQ_PACK_BASE3 = 0, 1
+SDQ_COMP_GPTQ, SDQ_COMP_JOINT = 0, 1
 
 STATUS_NAMES = {
     0: "SDQ_OK", -1: "SDQ_ERR_ARG", -2: "SDQ_ERR_SHAPE", -3: "SDQ_ERR_OSR", -4: "SDQ_ERR_LEVELS",
@@ -94,7 +95,7 @@ def _load() -> ctypes.CDLL:
         "sdq_hessian_factor": (ctypes.c_int, [P, ctypes.c_int64, ctypes.c_double, P, P, ctypes.c_size_t, P]),
         "sdq_hessian_check": (ctypes.c_int, [P, P]),
         "sdq_quantize_compensated_workspace_bytes": (ctypes.c_size_t, [L]),
-        "sdq_quantize_compensated": (ctypes.c_int, [P, L, P, P, P, P, ctypes.c_size_t, P]),
+        "sdq_quantize_compensated": (ctypes.c_int, [P, L, P, ctypes.c_int32, P, P, P, ctypes.c_size_t, P]),
         "sdq_multiosr": (ctypes.c_int, [P, P, P, ctypes.c_int64, ctypes.c_double, ctypes.c_double,
                                         ctypes.c_double, ctypes.c_double, P]),
         "sdq_moments_workspace_bytes": (ctypes.c_size_t, [ctypes.c_int64]),
@@ -245,9 +246,10 @@ def sdq_quantize_compensated_workspace_bytes(layout: sdq_layout) -> int:
     return int(_lib.sdq_quantize_compensated_workspace_bytes(ctypes.byref(layout)))
 
 
-def sdq_quantize_compensated(w, layout: sdq_layout, u, codes, scales, workspace, stream=None) -> None:
-    _check(_lib.sdq_quantize_compensated(_ptr(w), ctypes.byref(layout), _ptr(u), _ptr(codes), _ptr(scales),
-                                         _ptr(workspace), _nbytes(workspace), _stream(stream)))
+def sdq_quantize_compensated(w, layout: sdq_layout, u, codes, scales, workspace, stream=None,
+                             update: int = SDQ_COMP_GPTQ) -> None:
+    _check(_lib.sdq_quantize_compensated(_ptr(w), ctypes.byref(layout), _ptr(u), int(update), _ptr(codes),
+                                         _ptr(scales), _ptr(workspace), _nbytes(workspace), _stream(stream)))
 
 
 def sdq_multiosr(var: Sequence[float], nparams: Sequence[int], layer_id: Sequence[int],
@@ -352,8 +354,9 @@ def hessian_factor(h, lam: float, check: bool = True, stream=None):
 
 def quantize_compensated(w, osr: float, levels: int, u, block: int = 256, check: bool = True,
                          stream=None, hadamard: int = SDQ_HAD_SYLVESTER, signs=None,
-                         packing: int = SDQ_PACK_FIELDS) -> Encoded:
-    """Encode a device fp32 weight [n, k] with Algorithm 1's block compensation (u: fp64 [k, k])."""
+                         packing: int = SDQ_PACK_FIELDS, update: int = SDQ_COMP_GPTQ) -> Encoded:
+    """Encode a device fp32 weight [n, k] with Algorithm 1's block compensation (u: fp64 [k, k];
+    ``update``: SDQ_COMP_GPTQ or SDQ_COMP_JOINT)."""
     import torch
     if w.dtype != torch.float32 or not w.is_cuda or not w.is_contiguous():
         raise ValueError("w must be a contiguous fp32 device tensor")
@@ -367,7 +370,7 @@ def quantize_compensated(w, osr: float, levels: int, u, block: int = 256, check:
     codes = torch.empty(sdq_codes_bytes(layout), dtype=torch.uint8, device=w.device)
     scales = torch.empty(layout.n, dtype=torch.float32, device=w.device)
     ws = torch.empty(sdq_quantize_compensated_workspace_bytes(layout), dtype=torch.uint8, device=w.device)
-    sdq_quantize_compensated(w, layout, u, codes, scales, ws, stream)
+    sdq_quantize_compensated(w, layout, u, codes, scales, ws, stream, update)
     if check:
         sdq_quantize_check(ws, stream)
     return Encoded(layout, codes, scales)

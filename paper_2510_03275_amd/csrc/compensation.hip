@@ -12,8 +12,11 @@
 //            scales (the same rotate / upsample / scan kernels), its
 //            reconstruction Q_b = (s * C_b) E^T (E = Had D^T, the table of the
 //            activation expansion, in fp64) gives the error E_b = W_b - Q_b, and
-//            the later columns take the optimal-brain-surgeon correction of the
-//            jointly quantized block, W_F -= E_b U_QQ^-1 U_QF.
+//            the later columns are corrected with GPTQ's block step without its
+//            column-wise part, W_F -= E_b diag(U_QQ)^-1 U_QF (each column's
+//            error divided by its pivot), or optionally with the
+//            optimal-brain-surgeon correction of the jointly quantized block,
+//            W_F -= E_b U_QQ^-1 U_QF.
 //
 // All of it is dense fp64 linear algebra: one GEMM on the fp64 matrix cores
 // with general strides (64 x 64 tile per workgroup, 16-deep k slices through
@@ -301,6 +304,17 @@ __global__ void unpack_scaled_kernel(const uint32_t* __restrict__ codes, const f
   }
 }
 
+// g[r][t] = e[r][t] / u[c0 + t][c0 + t] (n x B): the block error of every
+// column divided by that column's pivot, an IEEE division per element.
+__global__ void divide_by_pivots_kernel(const double* __restrict__ e, const double* __restrict__ u,
+                                        int64_t k, int64_t c0, int64_t n, int B, double* __restrict__ g) {
+  for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n * B;
+       i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+    const int64_t t = c0 + i % B;
+    g[i] = e[i] / u[t * k + t];
+  }
+}
+
 unsigned grid1(int64_t count) {
   return static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 8192));
 }
@@ -454,7 +468,7 @@ size_t comp_ws_layout(const sdq_layout* L, CompWs* out, void* base) {
 }
 
 sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, const Tables* T,
-                                       const double* u, void* codes, float* scales, void* ws,
+                                       const double* u, int update, void* codes, float* scales, void* ws,
                                        hipStream_t stream) {
   CompWs cw;
   comp_ws_layout(L, &cw, ws);
@@ -469,17 +483,21 @@ sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, cons
   clear_rmax(cw.q, L, stream);
   sdq_status st = launch_encode_blocks(w, k, 0, nb, F, T, fcodes, scales, cw.q, cw.q.rmax, cw.q.rmax, stream);
   if (st != SDQ_OK) return st;
-  // 2. V_b = U_bb^-1 for every block: U_bb reversed is lower triangular;
-  //    invert it (64-blocks, then the off-diagonal blocks) and reverse back.
+  // 2. Joint update only: V_b = U_bb^-1 for every block: U_bb reversed is
+  //    lower triangular; invert it (64-blocks, then the off-diagonal blocks)
+  //    and reverse back.
   const int64_t bb = B * B;
-  fill_f64_kernel<<<grid1(nb * bb), 256, 0, stream>>>(cw.xb, nb * bb, 0.0);
-  reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
-      u, k, B * k + B, B, cw.lb, B, bb, 1, 0.0);
-  potrf64_kernel<<<dim3(static_cast<unsigned>(B / kT), static_cast<unsigned>(nb)), 256, 0, stream>>>(
-      cw.lb, B, kT * B + kT, bb, cw.xb, B, kT * B + kT, bb, 0, reinterpret_cast<int*>(cw.q.flag) + 1);
-  trtri_lower(cw.lb, cw.xb, B, B, bb, static_cast<int>(nb), cw.tmp, stream);
-  reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
-      cw.xb, B, bb, B, cw.vb, B, bb, 0, 0.0);
+  const bool joint = update == SDQ_COMP_JOINT;
+  if (joint) {
+    fill_f64_kernel<<<grid1(nb * bb), 256, 0, stream>>>(cw.xb, nb * bb, 0.0);
+    reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
+        u, k, B * k + B, B, cw.lb, B, bb, 1, 0.0);
+    potrf64_kernel<<<dim3(static_cast<unsigned>(B / kT), static_cast<unsigned>(nb)), 256, 0, stream>>>(
+        cw.lb, B, kT * B + kT, bb, cw.xb, B, kT * B + kT, bb, 0, reinterpret_cast<int*>(cw.q.flag) + 1);
+    trtri_lower(cw.lb, cw.xb, B, B, bb, static_cast<int>(nb), cw.tmp, stream);
+    reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
+        cw.xb, B, bb, B, cw.vb, B, bb, 0, 0.0);
+  }
   // 3. The walk over the blocks, W in fp64.
   widen_kernel<<<grid1(n * k), 256, 0, stream>>>(w, n * k, cw.w64);
   for (int64_t b = 0; b < nb; ++b) {
@@ -496,9 +514,13 @@ sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, cons
                                                            b * M, static_cast<int>(M), cw.cb);
     // E_b = W_b - (s C_b) E^T
     gemm64(n, B, M, -1.0, cw.cb, M, int64_t{1}, T->e64, int64_t{1}, M, 1.0, cw.ebuf, B, int64_t{1}, stream);
-    // G = E_b V_b
-    gemm64(n, B, B, 1.0, cw.ebuf, B, int64_t{1}, cw.vb + b * bb, B, int64_t{1}, 0.0, cw.gbuf, B, int64_t{1},
-           stream);
+    if (joint) {      // G = E_b V_b
+      gemm64(n, B, B, 1.0, cw.ebuf, B, int64_t{1}, cw.vb + b * bb, B, int64_t{1}, 0.0, cw.gbuf, B, int64_t{1},
+             stream);
+    } else {          // G = E_b diag(U_bb)^-1
+      divide_by_pivots_kernel<<<grid1(n * B), 256, 0, stream>>>(cw.ebuf, u, k, b * B, n, static_cast<int>(B),
+                                                               cw.gbuf);
+    }
     // W_F -= G U[Q, F]
     const int64_t f0 = (b + 1) * B;
     gemm64(n, k - f0, B, -1.0, cw.gbuf, B, int64_t{1}, u + b * B * k + f0, k, int64_t{1}, 1.0, cw.w64 + f0, k,

@@ -13,7 +13,7 @@
 //            segment's lookup tables of the 16 signed partial sums of every
 //            4-bit group of codes (4 binary codes or 2 ternary codes), and each
 //            lane adds one table entry per 4 bits.
-// Two to sixteen rows (integer matrix cores; blocks must start on a chunk):
+// Two to sixteen rows (integer matrix cores):
 //   expand   the same x_tilde, quantised per (row, block) to 24-bit fixed
 //            point and written as three signed-byte planes;
 //   gemv     codes expanded to int8 {-1, 0, +1} by a byte permute and

@@ -111,12 +111,6 @@ static sdq_status get_tables_for(int block, int m_up, int had, const SignWords& 
       ++j;
     }
   }
-  if (T.m_nz > 0) {
-    e = hipMalloc(&T.unz, unz.size() * sizeof(float));
-    if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
-    e = hipMemcpy(T.unz, unz.data(), unz.size() * sizeof(float), hipMemcpyHostToDevice);
-    if (e != hipSuccess) return hip_error(e, "table upload");
-  }
   // E^T[m][t] = sum_u Had[t][u] D[m][u]: a Walsh-Hadamard transform of each row
   // of D (fp64), scaled by 1/sqrt(B), its entry t negated where s_t = -1 for
   // the signed Had, or D itself without Had; kept in fp32 and as two fp16 terms.
@@ -160,19 +154,28 @@ static sdq_status get_tables_for(int block, int m_up, int had, const SignWords& 
   // Rounded up to fp32 (with a relative margin) so that |x_b E[:, m]| <=
   // max|x_b| * e1max holds for the device's fp32 sums.
   T.e1max = std::nextafter(static_cast<float>(e1max * (1.0 + 1e-6)), INFINITY);
-  e = hipMalloc(&T.edec, edec.size() * 4);
-  if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
-  for (uint16_t** dst : {&T.et_hi, &T.et_lo}) {
-    e = hipMalloc(dst, em * 2);
-    if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
+  // Device copies; on any failure the tables allocated so far are freed.
+  auto fail = [&](sdq_status st, const char* what, hipError_t err) {
+    for (void* ptr : {static_cast<void*>(T.unz), static_cast<void*>(T.edec), static_cast<void*>(T.et_hi),
+                      static_cast<void*>(T.et_lo), static_cast<void*>(T.e64)})
+      if (ptr) (void)hipFree(ptr);
+    return st == SDQ_ERR_NOMEM ? set_error(st, "%s: %s", what, hipGetErrorString(err)) : hip_error(err, what);
+  };
+  if (T.m_nz > 0) {
+    e = hipMalloc(&T.unz, unz.size() * sizeof(float));
+    if (e != hipSuccess) return fail(SDQ_ERR_NOMEM, "table allocation", e);
   }
-  e = hipMalloc(&T.e64, em * 8);
-  if (e != hipSuccess) return set_error(SDQ_ERR_NOMEM, "table allocation: %s", hipGetErrorString(e));
-  e = hipMemcpy(T.edec, edec.data(), edec.size() * 4, hipMemcpyHostToDevice);
+  e = hipMalloc(&T.edec, edec.size() * 4);
+  if (e == hipSuccess) e = hipMalloc(&T.et_hi, em * 2);
+  if (e == hipSuccess) e = hipMalloc(&T.et_lo, em * 2);
+  if (e == hipSuccess) e = hipMalloc(&T.e64, em * 8);
+  if (e != hipSuccess) return fail(SDQ_ERR_NOMEM, "table allocation", e);
+  if (T.m_nz > 0) e = hipMemcpy(T.unz, unz.data(), unz.size() * sizeof(float), hipMemcpyHostToDevice);
+  if (e == hipSuccess) e = hipMemcpy(T.edec, edec.data(), edec.size() * 4, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(T.et_hi, eh.data(), em * 2, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(T.et_lo, el.data(), em * 2, hipMemcpyHostToDevice);
   if (e == hipSuccess) e = hipMemcpy(T.e64, e64.data(), em * 8, hipMemcpyHostToDevice);
-  if (e != hipSuccess) return hip_error(e, "table upload");
+  if (e != hipSuccess) return fail(SDQ_ERR_HIP, "table upload", e);
   auto res = g_tables.emplace(key, T);
   *out = &res.first->second;
   return SDQ_OK;
@@ -416,10 +419,12 @@ size_t sdq_quantize_compensated_workspace_bytes(const sdq_layout* L) {
   return comp_ws_bytes(L);
 }
 
-sdq_status sdq_quantize_compensated(const float* w, const sdq_layout* L, const double* u, void* codes,
-                                    float* scales, void* ws, size_t ws_bytes, void* stream) {
+sdq_status sdq_quantize_compensated(const float* w, const sdq_layout* L, const double* u, int32_t update,
+                                    void* codes, float* scales, void* ws, size_t ws_bytes, void* stream) {
   sdq_status st = check_layout(L);
   if (st != SDQ_OK) return st;
+  if (update != SDQ_COMP_GPTQ && update != SDQ_COMP_JOINT)
+    return set_error(SDQ_ERR_ARG, "update %d is not SDQ_COMP_GPTQ or SDQ_COMP_JOINT", update);
   if (L->n > 0 && (!w || !u || !codes || !scales))
     return set_error(SDQ_ERR_ARG, "w, u, codes and scales must be non-NULL");
   const size_t need = comp_ws_bytes(L);
@@ -431,7 +436,7 @@ sdq_status sdq_quantize_compensated(const float* w, const sdq_layout* L, const d
   const Tables* T = nullptr;
   st = get_tables(L, &T);
   if (st != SDQ_OK) return st;
-  return launch_quantize_compensated(w, L, T, u, codes, scales, ws, static_cast<hipStream_t>(stream));
+  return launch_quantize_compensated(w, L, T, u, update, codes, scales, ws, static_cast<hipStream_t>(stream));
 }
 
 // The layout a linear path reads: base-3 codes are read as stored by the

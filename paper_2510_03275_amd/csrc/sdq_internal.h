@@ -131,7 +131,7 @@ sdq_status launch_hessian_factor(const double* h, int64_t k, double lam, double*
                                  hipStream_t stream);
 size_t comp_ws_bytes(const sdq_layout* L);
 sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, const Tables* T,
-                                       const double* u, void* codes, float* scales, void* ws,
+                                       const double* u, int update, void* codes, float* scales, void* ws,
                                        hipStream_t stream);
 
 // Moments (mean, variance) of a device array.

@@ -272,6 +272,7 @@ def test_compensation_entry_points_validate_before_gpu_work():
     L = P.sdq_layout_init(64, 512, 2.0, 3)
     need = lib.sdq_quantize_compensated_workspace_bytes(ctypes.byref(L))
     assert need > lib.sdq_quantize_workspace_bytes(ctypes.byref(L)) + 64 * 512 * 8
-    assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), None, fake, fake, fake, need, None) == -1
-    assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), fake, fake, fake, fake, need - 1, None) == -6
+    assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), None, 0, fake, fake, fake, need, None) == -1
+    assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), fake, 0, fake, fake, fake, need - 1, None) == -6
+    assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), fake, 2, fake, fake, fake, need, None) == -1
     assert lib.sdq_status_string(-10) == b"matrix not positive definite"

@@ -52,11 +52,12 @@ def test_hessian_adds_to_any_starting_matrix(m, k):
     assert np.max(np.abs(h.cpu().numpy() - want)) <= 1e-12 * np.max(np.abs(want))
 
 
-@pytest.mark.parametrize("k", [64, 128, 320, 1024])
+@pytest.mark.parametrize("k", [64, 128, 320, 1024, 4096])
 def test_factor_matches_oracle(k):
+    # k = 4096: the size of the compensation bench's factor.
     torch = require_gpu()
     import paper_2510_03275_amd as P
-    x = _calib_x(k, 4 * k, k)
+    x = _calib_x(k, 4 * k if k <= 1024 else k + 512, k)
     h = OC.hessian_fp64(x)
     lam = 0.01 * np.mean(np.diag(h))
     u = P.hessian_factor(torch.from_numpy(h).cuda(), lam).cpu().numpy()
@@ -84,8 +85,9 @@ CASES = [
 ]
 
 
+@pytest.mark.parametrize("update", [0, 1])
 @pytest.mark.parametrize("n,k,osr,levels,block", CASES)
-def test_compensated_codes_match_oracle(n, k, osr, levels, block):
+def test_compensated_codes_match_oracle(n, k, osr, levels, block, update):
     # Same U on both sides (the oracle's).  Every compensation step is fp64 on
     # both sides but summed in different orders, so a block handed to the fp32
     # encoder can differ in the last fp32 bit where an fp64 value sits at a
@@ -98,8 +100,9 @@ def test_compensated_codes_match_oracle(n, k, osr, levels, block):
     x = _calib_x(7 * k, 4 * k, k)
     h = OC.hessian_fp64(x)
     u = OC.inverse_cholesky_upper(h, 0.01 * np.mean(np.diag(h)))
-    enc = P.quantize_compensated(torch.from_numpy(w).cuda(), osr, levels, torch.from_numpy(u).cuda(), block)
-    r = OC.encode_compensated(w, osr, levels, block, u)
+    enc = P.quantize_compensated(torch.from_numpy(w).cuda(), osr, levels, torch.from_numpy(u).cuda(), block,
+                                 update=update)
+    r = OC.encode_compensated(w, osr, levels, block, u, update=update)
     got = LY.unpack(host_bytes(enc.codes), n, r.codes.shape[1], levels)
     assert np.array_equal(host_bytes(enc.scales).view(np.uint32), r.scales.view(np.uint32))
     assert np.array_equal(got[:, : r.m_up], r.codes[:, : r.m_up])
@@ -147,3 +150,25 @@ def test_diagonal_hessian_gives_the_plain_codes(levels):
     enc = P.quantize_compensated(torch.from_numpy(w).cuda(), 2.0, levels, u)
     plain = P.quantize(torch.from_numpy(w).cuda(), 2.0, levels)
     assert torch.equal(enc.codes, plain.codes) and torch.equal(enc.scales, plain.scales)
+
+
+@pytest.mark.parametrize("update", [0, 1])
+@pytest.mark.parametrize("levels", [2, 3])
+def test_compensated_codes_bit_exact_on_dyadic_inputs(levels, update):
+    # Dyadic W and U at OSR 1 (tests/dyadic_inputs.py): no fp64 step of the
+    # block loop rounds on either side (certified on the CPU by
+    # test_dyadic_inputs_keep_the_block_loop_exact), so every row's codes must
+    # be identical, whatever order the device sums in.
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    from tests.dyadic_inputs import dyadic_case
+    n, k, b = 70, 1024, 256
+    w, u = dyadic_case(n, k, b, seed=3 + levels)
+    enc = P.quantize_compensated(torch.from_numpy(w).cuda(), 1.0, levels, torch.from_numpy(u).cuda(), b,
+                                 update=update)
+    r = OC.encode_compensated(w, 1.0, levels, b, u, update=update)
+    assert np.array_equal(host_bytes(enc.scales).view(np.uint32), r.scales.view(np.uint32))
+    assert np.array_equal(host_bytes(enc.codes), LY.pack(r.codes, levels))
+    # the compensation did act: the codes differ from the plain encoding
+    plain = oracle.encode(w, 1.0, levels, b)
+    assert np.mean(plain.codes != r.codes) > 0.01
