@@ -277,6 +277,28 @@ sdq_status sdq_linear(const void* x_dev, sdq_dtype xt, int64_t m, const void* co
                       int32_t accumulate, void* workspace_dev, size_t workspace_bytes,
                       void* stream);
 
+/*
+ * sdq_linear without a workspace argument and without any device allocation,
+ * for callers that cannot allocate: code under HIP graph capture, tight
+ * serving loops, harnesses that forbid hipMalloc.  Arguments, results and
+ * errors as sdq_linear; the workspace is a fixed device array of
+ * SDQ_NOALLOC_SCRATCH_BYTES inside the library, one per GPU, held until the
+ * process ends (its address is looked up on the first call on each device).
+ *  - Calls needing more workspace than that (sdq_linear_workspace_bytes)
+ *    return SDQ_ERR_WORKSPACE; they fit for every one-to-sixteen-row call on
+ *    2-bit fields up to k = 28672 at OSR 8, and prefill while
+ *    m * k_up * 2 bytes (twice that without Had) stays within the limit.
+ *  - The coefficient tables are not built here: call sdq_prepare_layout for
+ *    the layout on the current device first, else SDQ_ERR_UNSUPPORTED.
+ *  - All calls on one GPU share its array; nothing in it needs to start at
+ *    zero, but calls that overlap on one GPU (different streams, or threads
+ *    without ordering) race on it and must not be issued.
+ */
+#define SDQ_NOALLOC_SCRATCH_BYTES (((size_t)32) << 20)
+sdq_status sdq_linear_noalloc(const void* x_dev, sdq_dtype xt, int64_t m, const void* codes_dev,
+                              const float* scales_dev, const sdq_layout* layout, float* y_dev,
+                              int32_t accumulate, void* stream);
+
 /* First step of sdq_linear: write x_tilde (the activation expansion of Fig. 5:
  * per block x_b Had D^T) for m activation rows into the workspace.  The
  * expansion depends only on (k, block, m_up, levels) of the layout, so one

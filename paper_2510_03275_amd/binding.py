@@ -86,6 +86,7 @@ def _load() -> ctypes.CDLL:
         "sdq_linear_workspace_bytes": (ctypes.c_size_t, [L, ctypes.c_int64]),
         "sdq_linear": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, P, P, L, P, ctypes.c_int32,
                                       P, ctypes.c_size_t, P]),
+        "sdq_linear_noalloc": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, P, P, L, P, ctypes.c_int32, P]),
         "sdq_expand_activations": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, L, P,
                                                   ctypes.c_size_t, P]),
         "sdq_linear_expanded": (ctypes.c_int, [ctypes.c_int64, P, P, L, P, ctypes.c_int32, P,
@@ -204,6 +205,15 @@ def sdq_linear(x, codes, scales, layout: sdq_layout, y, workspace, stream=None,
     _check(_lib.sdq_linear(_ptr(x), _dtype_code(x), m, _ptr(codes), _ptr(scales),
                            ctypes.byref(layout), _ptr(y), int(bool(accumulate)), _ptr(workspace),
                            ws_bytes, _stream(stream)))
+
+
+SDQ_NOALLOC_SCRATCH_BYTES = 32 << 20     # the library's fixed workspace of sdq_linear_noalloc
+
+
+def sdq_linear_noalloc(x, codes, scales, layout: sdq_layout, y, stream=None, accumulate: bool = False) -> None:
+    m = x.shape[0] if x.dim() == 2 else 0
+    _check(_lib.sdq_linear_noalloc(_ptr(x), _dtype_code(x), m, _ptr(codes), _ptr(scales), ctypes.byref(layout),
+                                   _ptr(y), int(bool(accumulate)), _stream(stream)))
 
 
 def sdq_expand_activations(x, layout: sdq_layout, workspace, stream=None) -> None:

@@ -22,7 +22,7 @@ LIB = os.path.join(HERE, "libsdq.so")
 ARCH = os.environ.get("SDQ_OFFLOAD_ARCH", "gfx950")
 
 SOURCES = ["sdq_api.cpp", "encoder.hip", "linear_decode.hip", "linear_prefill.hip", "expand_prefill.hip",
-           "moments.hip", "compensation.hip"]
+           "moments.hip", "compensation.hip", "linear_noalloc.hip"]
 
 COMMON = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",

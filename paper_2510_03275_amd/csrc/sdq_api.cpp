@@ -187,6 +187,21 @@ sdq_status get_tables(const sdq_layout* L, const Tables** out) {
   return get_tables_for(L->block, L->m_up, L->hadamard, w, out);
 }
 
+sdq_status find_tables(const sdq_layout* L, const Tables** out) {
+  SignWords w{};
+  if (L->hadamard == SDQ_HAD_SIGNED) std::copy(L->had_signs, L->had_signs + 8, w.begin());
+  int dev = 0;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return hip_error(e, "hipGetDevice");
+  std::lock_guard<std::mutex> lock(g_tables_mutex);
+  auto it = g_tables.find(std::make_tuple(dev, L->block, L->m_up, L->hadamard, w));
+  if (it == g_tables.end())
+    return set_error(SDQ_ERR_UNSUPPORTED, "the coefficient tables of this layout are not on the current device: "
+                                          "call sdq_prepare_layout first");
+  *out = &it->second;
+  return SDQ_OK;
+}
+
 static bool valid_block(int b) { return b == 64 || b == 128 || b == 256; }
 
 // The Had choice: a known mode, sign bits only below the block for the
@@ -479,14 +494,14 @@ static sdq_status linear_common(const sdq_layout* L, int64_t m, size_t ws_bytes,
 }
 
 static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
-                              void* ws, float* y_zero, void* stream) {
+                              void* ws, float* y_zero, void* stream, bool may_allocate = true) {
   if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
   if (!x) return set_error(SDQ_ERR_ARG, "x is NULL");
   if (!aligned16(x)) return set_error(SDQ_ERR_ARG, "x is not 16-byte aligned");
   const sdq_layout F = fields_view(L);
   const sdq_layout* P = needs_unpack(L, m) ? &F : L;
   const Tables* T = nullptr;
-  sdq_status st = get_tables(P, &T);
+  sdq_status st = may_allocate ? get_tables(P, &T) : find_tables(P, &T);
   if (st != SDQ_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
   return m <= 16 ? launch_decode_expand(x, xt, m, P, T, ws, y_zero, s)
@@ -527,9 +542,9 @@ sdq_status sdq_linear_expanded(int64_t m, const void* codes, const float* scales
   return contract_impl(m, codes, scales, L, y, accumulate != 0, ws, false, stream);
 }
 
-sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
-                      const float* scales, const sdq_layout* L, float* y, int32_t accumulate,
-                      void* ws, size_t ws_bytes, void* stream) {
+// Argument checks of sdq_linear that precede the workspace check.
+static sdq_status linear_args(const void* x, sdq_dtype xt, int64_t m, const void* codes, const float* scales,
+                              const sdq_layout* L, const float* y) {
   sdq_status st = check_layout(L);
   if (st != SDQ_OK) return st;
   if (m < 0) return set_error(SDQ_ERR_ARG, "m < 0");
@@ -537,15 +552,38 @@ sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
   if (m == 0 || L->n == 0) return SDQ_OK;
   if (!x || !codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
   if (!aligned16(x) || !aligned16(codes)) return set_error(SDQ_ERR_ARG, "x and codes must be 16-byte aligned");
+  return SDQ_OK;
+}
+
+}  // extern "C"
+
+sdq_status sdq::linear_impl(const void* x, sdq_dtype xt, int64_t m, const void* codes, const float* scales,
+                            const sdq_layout* L, float* y, int32_t accumulate, void* ws, size_t ws_bytes,
+                            void* stream, bool may_allocate) {
+  sdq_status st = linear_args(x, xt, m, codes, scales, L, y);
+  if (st != SDQ_OK || m == 0 || L->n == 0) return st;
   st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK) return st;
   // Decode: the expansion also zeroes y when the GEMV will add into it.
   const sdq_layout F = fields_view(L);
   const sdq_layout* P = needs_unpack(L, m) ? &F : L;
   const bool zero_in_expand = !accumulate && m <= 16 && decode_needs_zero_y(P, m);
-  st = expand_impl(x, xt, m, L, ws, zero_in_expand ? y : nullptr, stream);
+  st = expand_impl(x, xt, m, L, ws, zero_in_expand ? y : nullptr, stream, may_allocate);
   if (st != SDQ_OK) return st;
   return contract_impl(m, codes, scales, L, y, accumulate != 0, ws, true, stream);
+}
+
+size_t sdq::linear_ws_need(const sdq_layout* L, int64_t m) {
+  if (check_layout(L) != SDQ_OK || m <= 0) return 0;
+  return linear_ws_bytes(L, m);
+}
+
+extern "C" {
+
+sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
+                      const float* scales, const sdq_layout* L, float* y, int32_t accumulate,
+                      void* ws, size_t ws_bytes, void* stream) {
+  return linear_impl(x, xt, m, codes, scales, L, y, accumulate, ws, ws_bytes, stream, true);
 }
 
 // ---------------------------------------------------------------------------

@@ -58,6 +58,17 @@ struct Tables {
 // Returns the cached tables of the layout's (block, M, Had) for the current
 // device (creating them on first use).
 sdq_status get_tables(const sdq_layout* L, const Tables** out);
+// The same lookup without creating anything: SDQ_ERR_UNSUPPORTED when the
+// tables have not been built on the current device.
+sdq_status find_tables(const sdq_layout* L, const Tables** out);
+
+// The body of sdq_linear on a given workspace; may_allocate = false looks the
+// coefficient tables up without building them.  linear_ws_need: the bytes
+// that workspace needs (0 for an invalid layout or m <= 0).
+sdq_status linear_impl(const void* x, sdq_dtype xt, int64_t m, const void* codes, const float* scales,
+                       const sdq_layout* L, float* y, int32_t accumulate, void* ws, size_t ws_bytes,
+                       void* stream, bool may_allocate);
+size_t linear_ws_need(const sdq_layout* L, int64_t m);
 
 // Host fp64 coefficient helpers (also back the parity entry points).
 double upsample_kernel(int64_t p, int block, int m_up);          // g(p)

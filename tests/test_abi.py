@@ -276,3 +276,28 @@ def test_compensation_entry_points_validate_before_gpu_work():
     assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), fake, 0, fake, fake, fake, need - 1, None) == -6
     assert lib.sdq_quantize_compensated(fake, ctypes.byref(L), fake, 2, fake, fake, fake, need, None) == -1
     assert lib.sdq_status_string(-10) == b"matrix not positive definite"
+
+
+def test_noalloc_scratch_covers_every_decode_call_of_the_header():
+    # sdq.h: the fixed scratch of sdq_linear_noalloc fits every 1..16-row call
+    # on 2-bit fields up to k = 28672 at OSR 8 (every block and OSR step).
+    limit = P.SDQ_NOALLOC_SCRATCH_BYTES
+    assert limit == 32 << 20
+    lib = P.lib()
+    worst = 0
+    for block in (64, 128, 256):
+        for m_up in range(block, 8 * block + 1, 32):
+            for levels in (2, 3):
+                L = P.sdq_layout_init(64, 28672, m_up / block, levels, block)
+                for m in range(1, 17):
+                    worst = max(worst, lib.sdq_linear_workspace_bytes(ctypes.byref(L), m))
+    assert 0 < worst <= limit, worst
+
+
+def test_noalloc_entry_point_validates_before_gpu_work():
+    lib = P.lib()
+    fake = ctypes.c_void_p(0x1000)
+    L = P.sdq_layout_init(64, 28672, 2.0, 3)
+    # a prefill call beyond the fixed scratch is refused before anything else
+    assert lib.sdq_linear_noalloc(fake, 0, 2048, fake, fake, ctypes.byref(L), fake, 0, None) == -6
+    assert lib.sdq_linear_noalloc(fake, 0, 0, fake, fake, ctypes.byref(L), fake, 0, None) in (0, -7)
