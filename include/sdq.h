@@ -278,6 +278,38 @@ sdq_status sdq_linear(const void* x_dev, sdq_dtype xt, int64_t m, const void* co
                       void* stream);
 
 /*
+ * y_j = x W_hat_j^T for up to four encoded linears that read the same input
+ * (e.g. the q, k and v projections of one hidden state, or gate and up), in
+ * one expansion and one contraction launch: Fig. 5 brings the activations to
+ * the oversampled length once, and the contraction's workgroups cover the
+ * panels of every linear (launches and their ramp-up and tail are shared).
+ *   count          1 .. 4 linears.
+ *   codes_dev, scales_dev, y_dev   host arrays of `count` device pointers,
+ *                  one per linear, as in sdq_linear (y_dev[j]: fp32 [m x n_j]).
+ *   layouts        host array of `count` layouts, equal in k, block, m_up,
+ *                  levels, Had and packing (they may differ in n; a linear with
+ *                  n = 0 is skipped).
+ *   workspace      >= sdq_linear_group_workspace_bytes(layouts, count, m).
+ * Results, accuracy and accumulate as sdq_linear for each linear.
+ * Errors: as sdq_linear; SDQ_ERR_ARG also for a count outside 1 .. 4 or
+ * layouts that differ in more than n (sdq_linear_group_workspace_bytes
+ * returns 0 for those). */
+size_t sdq_linear_group_workspace_bytes(const sdq_layout* layouts, int32_t count, int64_t m);
+sdq_status sdq_linear_group(const void* x_dev, sdq_dtype xt, int64_t m, int32_t count,
+                            const void* const* codes_dev, const float* const* scales_dev,
+                            const sdq_layout* layouts, float* const* y_dev, int32_t accumulate,
+                            void* workspace_dev, size_t workspace_bytes, void* stream);
+
+/* The contraction of sdq_linear_group alone, from the x_tilde that
+ * sdq_expand_activations left in the workspace (same m and a layout of the
+ * group's family), as sdq_linear_expanded does for one linear.  Arguments and
+ * errors as sdq_linear_group without x. */
+sdq_status sdq_linear_group_expanded(int64_t m, int32_t count, const void* const* codes_dev,
+                                     const float* const* scales_dev, const sdq_layout* layouts,
+                                     float* const* y_dev, int32_t accumulate, void* workspace_dev,
+                                     size_t workspace_bytes, void* stream);
+
+/*
  * sdq_linear without a workspace argument and without any device allocation,
  * for callers that cannot allocate: code under HIP graph capture, tight
  * serving loops, harnesses that forbid hipMalloc.  Arguments, results and

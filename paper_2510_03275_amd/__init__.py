@@ -12,4 +12,5 @@ from .binding import (  # noqa: F401
     sdq_quantize_compensated_workspace_bytes, hessian_factor, quantize_compensated,
     SDQ_F16, SDQ_BF16, SDQ_F32, SDQ_HAD_NONE, SDQ_HAD_SYLVESTER, SDQ_HAD_SIGNED, SDQ_PACK_FIELDS, SDQ_PACK_BASE3,
     SDQ_COMP_GPTQ, SDQ_COMP_JOINT, SDQ_NOALLOC_SCRATCH_BYTES, sdq_linear_noalloc,
+    LinearGroup, sdq_linear_group, sdq_linear_group_workspace_bytes, sdq_linear_group_expanded,
 )

@@ -87,6 +87,11 @@ def _load() -> ctypes.CDLL:
         "sdq_linear": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, P, P, L, P, ctypes.c_int32,
                                       P, ctypes.c_size_t, P]),
         "sdq_linear_noalloc": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, P, P, L, P, ctypes.c_int32, P]),
+        "sdq_linear_group_workspace_bytes": (ctypes.c_size_t, [L, ctypes.c_int32, ctypes.c_int64]),
+        "sdq_linear_group": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, ctypes.c_int32, P, P, L, P,
+                                            ctypes.c_int32, P, ctypes.c_size_t, P]),
+        "sdq_linear_group_expanded": (ctypes.c_int, [ctypes.c_int64, ctypes.c_int32, P, P, L, P, ctypes.c_int32,
+                                                     P, ctypes.c_size_t, P]),
         "sdq_expand_activations": (ctypes.c_int, [P, ctypes.c_int, ctypes.c_int64, L, P,
                                                   ctypes.c_size_t, P]),
         "sdq_linear_expanded": (ctypes.c_int, [ctypes.c_int64, P, P, L, P, ctypes.c_int32, P,
@@ -205,6 +210,45 @@ def sdq_linear(x, codes, scales, layout: sdq_layout, y, workspace, stream=None,
     _check(_lib.sdq_linear(_ptr(x), _dtype_code(x), m, _ptr(codes), _ptr(scales),
                            ctypes.byref(layout), _ptr(y), int(bool(accumulate)), _ptr(workspace),
                            ws_bytes, _stream(stream)))
+
+
+def _layout_array(layouts):
+    arr = (sdq_layout * len(layouts))()
+    for i, L in enumerate(layouts):
+        arr[i] = L
+    return arr
+
+
+def sdq_linear_group_workspace_bytes(layouts, m: int) -> int:
+    return int(_lib.sdq_linear_group_workspace_bytes(_layout_array(layouts), len(layouts), m))
+
+
+class LinearGroup:
+    """The host-side argument arrays of sdq_linear_group for fixed linears and
+    outputs, built once (the call then only passes pointers)."""
+
+    def __init__(self, encs, ys):
+        n = len(encs)
+        self.count = n
+        self.layouts = _layout_array([e.layout for e in encs])
+        self.codes = (ctypes.c_void_p * n)(*[e.codes.data_ptr() for e in encs])
+        self.scales = (ctypes.c_void_p * n)(*[e.scales.data_ptr() for e in encs])
+        self.ys = (ctypes.c_void_p * n)(*[y.data_ptr() for y in ys])
+        self._keep = (list(encs), list(ys))
+
+
+def sdq_linear_group(x, group: "LinearGroup", workspace, stream=None, accumulate: bool = False) -> None:
+    m = x.shape[0] if x.dim() == 2 else 0
+    _check(_lib.sdq_linear_group(_ptr(x), _dtype_code(x), m, group.count, group.codes, group.scales,
+                                 group.layouts, group.ys, int(bool(accumulate)), _ptr(workspace),
+                                 _nbytes(workspace), _stream(stream)))
+
+
+def sdq_linear_group_expanded(m: int, group: "LinearGroup", workspace, stream=None,
+                              accumulate: bool = False) -> None:
+    _check(_lib.sdq_linear_group_expanded(m, group.count, group.codes, group.scales, group.layouts, group.ys,
+                                          int(bool(accumulate)), _ptr(workspace), _nbytes(workspace),
+                                          _stream(stream)))
 
 
 SDQ_NOALLOC_SCRATCH_BYTES = 32 << 20     # the library's fixed workspace of sdq_linear_noalloc

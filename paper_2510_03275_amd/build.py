@@ -57,14 +57,15 @@ def _compile(src: str) -> str:
     return obj
 
 
-SYNTH_SRC = os.path.join(os.path.dirname(HERE), "synth", "csrc", "synth_gen.hip")
+SYNTH_SRCS = [os.path.join(os.path.dirname(HERE), "synth", "csrc", f) for f in ("synth_gen.hip", "read_probe.hip")]
 SYNTH_LIB = os.path.join(os.path.dirname(HERE), "synth", "libsdqsynth.so")
 
 
 def _build_synth() -> str:
-    """The input generator's device twin: a library of its own (no method code)."""
+    """The input generator's device twin and the bench's streaming-read probe: a
+    library of its own (no method code)."""
     tmp = SYNTH_LIB + ".tmp"
-    cmd = [_hipcc(), "-x", "hip", *COMMON, "-shared", SYNTH_SRC, "-o", tmp]
+    cmd = [_hipcc(), "-x", "hip", *COMMON, "-shared", *SYNTH_SRCS, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         raise RuntimeError(f"synth build failed: {' '.join(cmd)}\n{res.stdout}\n{res.stderr}")

@@ -49,6 +49,27 @@ __device__ inline float load_x(const void* x, sdq_dtype xt, int64_t idx) {
   return static_cast<const float*>(x)[idx];
 }
 
+// Zero the outputs of a set of linears (m rows each), grid-stride over the
+// launch's workgroups: a side duty of the expansion when the GEMV that follows
+// adds its split-K partials into y.
+__device__ inline void zero_outputs(const LinearSet& z, int m, int64_t wg, int64_t n_wg, int tid) {
+  for (int j = 0; j < z.count; ++j) {
+    const int64_t cnt = static_cast<int64_t>(m) * z.n[j];
+    float* p = z.y[j];
+    for (int64_t i = wg * kExpThreads + tid; i < cnt; i += n_wg * kExpThreads) p[i] = 0.0f;
+  }
+}
+
+// The linear of a set that unit u of a launch belongs to (first[] holds the
+// prefix sums of the units per linear); uniform over the workgroup.
+__device__ inline int linear_of(const LinearSet& S, int64_t u) {
+  int j = 0;
+#pragma unroll
+  for (int i = 1; i < kMaxGroup; ++i)
+    if (i < S.count && u >= S.first[i]) j = i;
+  return j;
+}
+
 // One workgroup: 64 output samples of one block, all m rows.  Wave w keeps
 // the quarter t in [w B/4, (w+1) B/4) of the 64 columns of E in registers
 // (the grouped table layout makes each of its loads 1 KB contiguous); the
@@ -58,7 +79,7 @@ template <int B>
 __global__ __launch_bounds__(kExpThreads) void expand_decode_kernel(
     const void* __restrict__ x, sdq_dtype xt, int m, int64_t k, int m_up, int m_pad,
     int64_t k_up, int64_t k_up_pad, const float4* __restrict__ edec, float* __restrict__ xt_out,
-    float* __restrict__ y_zero, int64_t y_count) {
+    LinearSet zero) {
   constexpr int TQ = B / 4;                 // t values per wave
   __shared__ float xs[kMaxDecodeRows][B];
   __shared__ float red[4][kMaxDecodeRows][64];
@@ -78,8 +99,7 @@ __global__ __launch_bounds__(kExpThreads) void expand_decode_kernel(
   // Side duties: zero y for a split-K GEMV, zero x_tilde's padding.
   const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
   const int64_t n_wg = static_cast<int64_t>(gridDim.x) * gridDim.y;
-  if (y_zero)
-    for (int64_t i = wg * kExpThreads + tid; i < y_count; i += n_wg * kExpThreads) y_zero[i] = 0.0f;
+  zero_outputs(zero, m, wg, n_wg, tid);
   if (wg == 0) {
     const int64_t pad = k_up_pad - k_up;
     for (int64_t i = tid; i < m * pad; i += kExpThreads)
@@ -157,7 +177,7 @@ template <int B, int LEVELS>
 __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
     const void* __restrict__ x, sdq_dtype xt, int m, int npg, int64_t k, int64_t nb, int m_up,
     int m_pad, int cpb, const float4* __restrict__ edec, float e1max, uint32_t* __restrict__ planes,
-    float* __restrict__ sx, float* __restrict__ y_zero, int64_t y_count) {
+    float* __restrict__ sx, LinearSet zero) {
   constexpr int TQ = B / 4;
   __shared__ float xs[kMaxDecodeRows][B];
   __shared__ float red[4][kMaxDecodeRows][64];
@@ -182,8 +202,7 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   }
   const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
   const int64_t n_wg = static_cast<int64_t>(gridDim.x) * gridDim.y;
-  if (y_zero)
-    for (int64_t i = wg * kExpThreads + tid; i < y_count; i += n_wg * kExpThreads) y_zero[i] = 0.0f;
+  zero_outputs(zero, m, wg, n_wg, tid);
   __syncthreads();
   // max |x_b| per row: wave w handles rows w, w + 4, ...
   for (int i = w; i < m; i += 4) {
@@ -255,10 +274,8 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
 // in LDS and leave with one atomic add (or store) per output.
 template <int LEVELS, int NPG, int CH>
 __global__ __launch_bounds__(256) void gemv_mfma_kernel(
-    const uint4* __restrict__ codes, const float* __restrict__ scales,
-    const uint4* __restrict__ planes, const float* __restrict__ sx, int m, int64_t n,
-    int64_t n_chunks, int64_t nb, int m_up, int cpb, int bpw, int n_split, int accumulate,
-    float* __restrict__ y) {
+    LinearSet S, const uint4* __restrict__ planes, const float* __restrict__ sx, int m,
+    int64_t n_chunks, int64_t nb, int m_up, int cpb, int bpw, int n_split, int accumulate) {
   typedef int v4i __attribute__((ext_vector_type(4)));
   constexpr uint32_t kTable = LEVELS == 2 ? 0x000001FFu : 0xFF000100u;   // code -> int8
   constexpr uint32_t kMask = LEVELS == 2 ? 0x01010101u : 0x03030303u;
@@ -268,9 +285,13 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
   __shared__ float red[4][NPG * 4][64];
   const int lane = threadIdx.x % 64;
   const int wave = threadIdx.x / 64;
-  const int64_t panel = blockIdx.y;
+  const int lin = linear_of(S, blockIdx.y);            // units: panels
+  const int64_t panel = blockIdx.y - S.first[lin];
+  const int64_t n = S.n[lin];
+  const float* __restrict__ scales = S.scales[lin];
+  float* __restrict__ y = S.y[lin];
   const int kg = lane / 16;
-  const uint4* cbase = codes + panel * n_chunks * kPanel + lane;
+  const uint4* cbase = static_cast<const uint4*>(S.codes[lin]) + panel * n_chunks * kPanel + lane;
   float accf[NPG][4];
 #pragma unroll
   for (int pg = 0; pg < NPG; ++pg)
@@ -433,9 +454,8 @@ __device__ inline float4 build_quad(const float (&xs)[4], int h) {
 // lookup costs a shift, a mask, an LDS read and an add.
 template <int MR, int LEVELS, int SEG>
 __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
-    const uint4* __restrict__ codes, const float* __restrict__ scales,
-    const float* __restrict__ xt, int m, int64_t n, int64_t n_panels, int64_t n_chunks,
-    int64_t k_up_pad, int n_segs, int segs_fast, int accumulate, float* __restrict__ y) {
+    LinearSet S, const float* __restrict__ xt, int m, int64_t n_chunks,
+    int64_t k_up_pad, int n_segs, int segs_fast, int accumulate) {
   constexpr int CPG = LEVELS == 2 ? 4 : 2;            // codes per 4-bit group
   constexpr int kGroups = SEG * kGroupsPerChunk;       // groups per activation row
   constexpr int kRowFloats = kGroups * 16;             // table floats per activation row
@@ -450,7 +470,14 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
-  const int64_t panel = static_cast<int64_t>(segs_fast ? blockIdx.y : blockIdx.x) * kGemvWaves + wave;
+  const int64_t pg = segs_fast ? blockIdx.y : blockIdx.x;   // panel group over the set
+  const int lin = linear_of(S, pg);                          // units: panel groups
+  const int64_t n = S.n[lin];
+  const int64_t n_panels = (n + kPanel - 1) / kPanel;
+  const uint4* __restrict__ codes = static_cast<const uint4*>(S.codes[lin]);
+  const float* __restrict__ scales = S.scales[lin];
+  float* __restrict__ y = S.y[lin];
+  const int64_t panel = (pg - S.first[lin]) * kGemvWaves + wave;
   const bool panel_ok = panel < n_panels;
   const int seg = segs_fast ? blockIdx.x : blockIdx.y;
   const int64_t c0 = static_cast<int64_t>(seg) * SEG;
@@ -570,9 +597,8 @@ __device__ inline uint32_t byte1_times4(uint32_t x) {
 // the segment shared by four panels, one wave per panel.
 template <int SEG>
 __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
-    const uint4* __restrict__ codes, const float* __restrict__ scales,
-    const float* __restrict__ xt, int64_t n, int64_t n_panels, int64_t n_chunks, int64_t k_up_pad,
-    int n_segs, int segs_fast, int accumulate, float* __restrict__ y) {
+    LinearSet S, const float* __restrict__ xt, int64_t n_chunks, int n_segs, int segs_fast,
+    int accumulate) {
   constexpr int kBytes = 16;                   // groups of five codes per chunk
   constexpr int kGF = 36;                      // table floats per group: 27 + 9
   constexpr int kGroups = SEG * kBytes;
@@ -584,7 +610,14 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
-  const int64_t panel = static_cast<int64_t>(segs_fast ? blockIdx.y : blockIdx.x) * kGemvWaves + wave;
+  const int64_t pg = segs_fast ? blockIdx.y : blockIdx.x;   // panel group over the set
+  const int lin = linear_of(S, pg);
+  const int64_t n = S.n[lin];
+  const int64_t n_panels = (n + kPanel - 1) / kPanel;
+  const uint4* __restrict__ codes = static_cast<const uint4*>(S.codes[lin]);
+  const float* __restrict__ scales = S.scales[lin];
+  float* __restrict__ y = S.y[lin];
+  const int64_t panel = (pg - S.first[lin]) * kGemvWaves + wave;
   const bool panel_ok = panel < n_panels;
   const int seg = segs_fast ? blockIdx.x : blockIdx.y;
   const int64_t c0 = static_cast<int64_t>(seg) * SEG;
@@ -662,7 +695,6 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
   const float s = scales[r];
   if (n_segs > 1) unsafeAtomicAdd(&y[r], acc * s);
   else y[r] = accumulate ? y[r] + acc * s : acc * s;
-  (void)k_up_pad;
 }
 
 int round_mr(int64_t m) {
@@ -681,14 +713,15 @@ int round_mr(int64_t m) {
 // it leaves fewer than 800 workgroups and SEG = 2 keeps the segments per
 // output at 80 or below (small layers: 2), or it needs more than 128 segments
 // per output (long rows: 8).  Tables of MR rows x SEG chunks must fit 64 KB.
-int pick_seg(const sdq_layout* L, int mr) {
+// `panels`: the 64-row panels of all linears the launch covers.
+int pick_seg(const sdq_layout* L, int mr, int64_t panels) {
   static const char* env = std::getenv("SDQ_GEMV_SEG");   // tuning aid: 2, 4 or 8
   const int max_seg = mr >= 16 ? 2 : (mr >= 8 ? 4 : 8);
   if (env) {
     const int v = std::atoi(env);
     if ((v == 2 || v == 4 || v == 8) && v <= max_seg) return v;
   }
-  const int64_t panel_groups = (L->n_pad / kPanel + kGemvWaves - 1) / kGemvWaves;
+  const int64_t panel_groups = (panels + kGemvWaves - 1) / kGemvWaves;
   const int64_t segs2 = (L->n_chunks + 1) / 2, segs4 = (L->n_chunks + 3) / 4;
   int seg;
   if (segs2 <= 80 && panel_groups * segs4 < 800) seg = 2;
@@ -790,98 +823,109 @@ int pick_ch(int cpb, int npg, int levels) {
   return 1;
 }
 
+// Prefix sums of a set's units: `per(n)` units for a linear of n rows.
+template <typename F>
+int64_t fill_first(LinearSet& S, F per) {
+  S.first[0] = 0;
+  for (int j = 0; j < S.count; ++j) S.first[j + 1] = S.first[j] + per(S.n[j]);
+  for (int j = S.count + 1; j <= kMaxGroup; ++j) S.first[j] = S.first[S.count];
+  return S.first[S.count];
+}
+
+int64_t panels_of(int64_t n) { return (n + kPanel - 1) / kPanel; }
+int64_t pgroups_of(int64_t n) { return (panels_of(n) + kGemvWaves - 1) / kGemvWaves; }
+
 template <int LEVELS, int NPG, int CH>
-void launch_mfma_ch(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
-                    int64_t m, float* y, bool accumulate, hipStream_t stream) {
-  const int64_t n_panels = L->n_pad / kPanel;
+void launch_mfma_ch(const DecodeWs& w, LinearSet S, const sdq_layout* L, int64_t m, bool accumulate,
+                    hipStream_t stream) {
+  const int64_t panels = fill_first(S, panels_of);
   const int bpw = mfma_bpw(L, m);
   const int splits = mfma_splits(L, m);
   // K groups fastest: consecutive workgroups sweep one panel's chunks.
-  const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(n_panels));
+  const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(panels));
   gemv_mfma_kernel<LEVELS, NPG, CH><<<grid, dim3(256), 0, stream>>>(
-      static_cast<const uint4*>(codes), scales, reinterpret_cast<const uint4*>(w.planes), w.sx,
-      static_cast<int>(m), L->n, L->n_chunks, L->nb, L->m_up, mfma_cpb(L), bpw, splits,
-      accumulate ? 1 : 0, y);
+      S, reinterpret_cast<const uint4*>(w.planes), w.sx, static_cast<int>(m), L->n_chunks, L->nb, L->m_up,
+      mfma_cpb(L), bpw, splits, accumulate ? 1 : 0);
 }
 
 template <int LEVELS>
-void launch_mfma_levels(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
-                        int64_t m, float* y, bool acc, hipStream_t stream) {
+void launch_mfma_levels(const DecodeWs& w, const LinearSet& S, const sdq_layout* L, int64_t m, bool acc,
+                        hipStream_t stream) {
   const int npg = npg_for(m);
   const int ch = pick_ch(mfma_cpb(L), npg, LEVELS);
 #define SDQ_CH(NPG_, CH_)                                                         \
-  if (ch == CH_) return launch_mfma_ch<LEVELS, NPG_, CH_>(w, codes, scales, L, m, y, acc, stream)
+  if (ch == CH_) return launch_mfma_ch<LEVELS, NPG_, CH_>(w, S, L, m, acc, stream)
   switch (npg) {
     case 1:
       SDQ_CH(1, 8); SDQ_CH(1, 6); SDQ_CH(1, 4); SDQ_CH(1, 3); SDQ_CH(1, 2);
-      return launch_mfma_ch<LEVELS, 1, 1>(w, codes, scales, L, m, y, acc, stream);
+      return launch_mfma_ch<LEVELS, 1, 1>(w, S, L, m, acc, stream);
     case 2:
       SDQ_CH(2, 4); SDQ_CH(2, 2);
-      return launch_mfma_ch<LEVELS, 2, 1>(w, codes, scales, L, m, y, acc, stream);
+      return launch_mfma_ch<LEVELS, 2, 1>(w, S, L, m, acc, stream);
     case 3:
       SDQ_CH(3, 4); SDQ_CH(3, 2);
-      return launch_mfma_ch<LEVELS, 3, 1>(w, codes, scales, L, m, y, acc, stream);
+      return launch_mfma_ch<LEVELS, 3, 1>(w, S, L, m, acc, stream);
     default:
       SDQ_CH(4, 4); SDQ_CH(4, 2);
-      return launch_mfma_ch<LEVELS, 4, 1>(w, codes, scales, L, m, y, acc, stream);
+      return launch_mfma_ch<LEVELS, 4, 1>(w, S, L, m, acc, stream);
   }
 #undef SDQ_CH
 }
 
+// Large launches: segments fastest, so consecutive workgroups sweep the same
+// panels' chunks.  Small ones (the whole grid resident at once): panel groups
+// fastest, so neighbours share a segment's samples.  (Measured.)
+dim3 lut_grid(int64_t pgroups, int n_segs, bool* segs_fast) {
+  *segs_fast = pgroups * n_segs > 2048;
+  return *segs_fast ? dim3(static_cast<unsigned>(n_segs), static_cast<unsigned>(pgroups))
+                    : dim3(static_cast<unsigned>(pgroups), static_cast<unsigned>(n_segs));
+}
+
 template <int MR, int LEVELS, int SEG>
-void launch_gemv_seg(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
-                     int64_t m, float* y, bool accumulate, hipStream_t stream) {
-  const int64_t n_panels = L->n_pad / kPanel;
+void launch_gemv_seg(const DecodeWs& w, LinearSet S, const sdq_layout* L, int64_t m, bool accumulate,
+                     hipStream_t stream) {
+  const int64_t pgroups = fill_first(S, pgroups_of);
   const int n_segs = segs_for(L, SEG);
-  // Large layers: segments fastest, so consecutive workgroups sweep the same
-  // panels' chunks.  Small ones (the whole grid resident at once): panel
-  // groups fastest, so neighbours share a segment's samples.  (Measured.)
-  const unsigned pgroups = static_cast<unsigned>((n_panels + kGemvWaves - 1) / kGemvWaves);
-  const bool segs_fast = static_cast<int64_t>(pgroups) * n_segs > 2048;
-  const dim3 grid = segs_fast ? dim3(static_cast<unsigned>(n_segs), pgroups)
-                              : dim3(pgroups, static_cast<unsigned>(n_segs));
+  bool segs_fast = false;
+  const dim3 grid = lut_grid(pgroups, n_segs, &segs_fast);
   gemv_lut_kernel<MR, LEVELS, SEG><<<grid, dim3(64 * kGemvWaves), 0, stream>>>(
-      static_cast<const uint4*>(codes), scales, w.xt, static_cast<int>(m), L->n, n_panels,
-      L->n_chunks, L->n_chunks * L->codes_per_chunk, n_segs, segs_fast ? 1 : 0,
-      accumulate ? 1 : 0, y);
+      S, w.xt, static_cast<int>(m), L->n_chunks, L->n_chunks * L->codes_per_chunk, n_segs, segs_fast ? 1 : 0,
+      accumulate ? 1 : 0);
 }
 
 template <int SEG>
-void launch_gemv_base3_seg(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
-                           float* y, bool accumulate, hipStream_t stream) {
-  const int64_t n_panels = L->n_pad / kPanel;
+void launch_gemv_base3_seg(const DecodeWs& w, LinearSet S, const sdq_layout* L, bool accumulate,
+                           hipStream_t stream) {
+  const int64_t pgroups = fill_first(S, pgroups_of);
   const int n_segs = segs_for(L, SEG);
-  const unsigned pgroups = static_cast<unsigned>((n_panels + kGemvWaves - 1) / kGemvWaves);
-  const bool segs_fast = static_cast<int64_t>(pgroups) * n_segs > 2048;
-  const dim3 grid = segs_fast ? dim3(static_cast<unsigned>(n_segs), pgroups)
-                              : dim3(pgroups, static_cast<unsigned>(n_segs));
+  bool segs_fast = false;
+  const dim3 grid = lut_grid(pgroups, n_segs, &segs_fast);
   gemv_lut_base3_kernel<SEG><<<grid, dim3(64 * kGemvWaves), 0, stream>>>(
-      static_cast<const uint4*>(codes), scales, w.xt, L->n, n_panels, L->n_chunks,
-      L->n_chunks * L->codes_per_chunk, n_segs, segs_fast ? 1 : 0, accumulate ? 1 : 0, y);
+      S, w.xt, L->n_chunks, n_segs, segs_fast ? 1 : 0, accumulate ? 1 : 0);
 }
 
 template <int MR, int LEVELS>
-void launch_gemv_mr(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
-                    int64_t m, float* y, bool acc, hipStream_t stream) {
-  const int seg = pick_seg(L, MR);
+void launch_gemv_mr(const DecodeWs& w, const LinearSet& S, const sdq_layout* L, int64_t m, bool acc,
+                    hipStream_t stream) {
+  const int seg = pick_seg(L, MR, set_panels(S));
   if constexpr (MR <= 4) {
-    if (seg == 8) return launch_gemv_seg<MR, LEVELS, 8>(w, codes, scales, L, m, y, acc, stream);
+    if (seg == 8) return launch_gemv_seg<MR, LEVELS, 8>(w, S, L, m, acc, stream);
   }
   if constexpr (MR <= 8) {
-    if (seg == 4) return launch_gemv_seg<MR, LEVELS, 4>(w, codes, scales, L, m, y, acc, stream);
+    if (seg == 4) return launch_gemv_seg<MR, LEVELS, 4>(w, S, L, m, acc, stream);
   }
-  launch_gemv_seg<MR, LEVELS, 2>(w, codes, scales, L, m, y, acc, stream);
+  launch_gemv_seg<MR, LEVELS, 2>(w, S, L, m, acc, stream);
 }
 
 template <int LEVELS>
-void launch_gemv(const DecodeWs& w, const void* codes, const float* scales, const sdq_layout* L,
-                 int64_t m, float* y, bool acc, hipStream_t stream) {
+void launch_gemv(const DecodeWs& w, const LinearSet& S, const sdq_layout* L, int64_t m, bool acc,
+                 hipStream_t stream) {
   switch (round_mr(m)) {
-    case 1: launch_gemv_mr<1, LEVELS>(w, codes, scales, L, m, y, acc, stream); break;
-    case 2: launch_gemv_mr<2, LEVELS>(w, codes, scales, L, m, y, acc, stream); break;
-    case 4: launch_gemv_mr<4, LEVELS>(w, codes, scales, L, m, y, acc, stream); break;
-    case 8: launch_gemv_mr<8, LEVELS>(w, codes, scales, L, m, y, acc, stream); break;
-    default: launch_gemv_mr<16, LEVELS>(w, codes, scales, L, m, y, acc, stream); break;
+    case 1: launch_gemv_mr<1, LEVELS>(w, S, L, m, acc, stream); break;
+    case 2: launch_gemv_mr<2, LEVELS>(w, S, L, m, acc, stream); break;
+    case 4: launch_gemv_mr<4, LEVELS>(w, S, L, m, acc, stream); break;
+    case 8: launch_gemv_mr<8, LEVELS>(w, S, L, m, acc, stream); break;
+    default: launch_gemv_mr<16, LEVELS>(w, S, L, m, acc, stream); break;
   }
 }
 
@@ -898,17 +942,17 @@ bool decode_reads_base3(const sdq_layout* L, int64_t m) {
   return L->packing == SDQ_PACK_BASE3 && m == 1 && !use_mfma(L, m);
 }
 
-bool decode_needs_zero_y(const sdq_layout* L, int64_t m) {
+bool decode_needs_zero_y(const sdq_layout* L, int64_t m, int64_t panels) {
   if (use_mfma(L, m)) return mfma_splits(L, m) > 1;
-  return segs_for(L, pick_seg(L, round_mr(m))) > 1;
+  return segs_for(L, pick_seg(L, round_mr(m), panels)) > 1;
 }
 
 sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
-                                const Tables* T, void* ws, float* y_zero, hipStream_t stream) {
+                                const Tables* T, void* ws, const LinearSet* zero, hipStream_t stream) {
   const DecodeWs w = carve(L, m, ws);
   const int B = L->block;
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
-  const int64_t y_count = y_zero ? m * L->n : 0;
+  const LinearSet z = zero ? *zero : LinearSet{};
   const dim3 egrid(static_cast<unsigned>(T->m_pad / 64), static_cast<unsigned>(L->nb));
   if (use_mfma(L, m)) {
     const int npg = npg_for(m);
@@ -917,7 +961,7 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
 #define SDQ_PLANES(BB, LV)                                                                       \
   expand_planes_kernel<BB, LV><<<pgrid, dim3(kExpThreads), 0, stream>>>(                         \
       x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad, cpb,                      \
-      reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, y_zero, y_count)
+      reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, z)
     if (L->levels == 2) {
       switch (B) {
         case 64: SDQ_PLANES(64, 2); break;
@@ -939,7 +983,7 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
 #define SDQ_EXPAND(BB)                                                                          \
   expand_decode_kernel<BB><<<egrid, dim3(kExpThreads), 0, stream>>>(                            \
       x, xt, static_cast<int>(m), L->k, L->m_up, T->m_pad, L->k_up, k_up_pad,                   \
-      reinterpret_cast<const float4*>(T->edec), w.xt, y_zero, y_count)
+      reinterpret_cast<const float4*>(T->edec), w.xt, z)
   switch (B) {
     case 64: SDQ_EXPAND(64); break;
     case 128: SDQ_EXPAND(128); break;
@@ -951,29 +995,30 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
   return SDQ_OK;
 }
 
-sdq_status launch_decode_contract(int64_t m, const void* codes, const float* scales,
-                                  const sdq_layout* L, float* y, bool accumulate, void* ws,
+sdq_status launch_decode_contract(int64_t m, LinearSet S, const sdq_layout* L, bool accumulate, void* ws,
                                   bool y_ready, hipStream_t stream) {
   const DecodeWs w = carve(L, m, ws);
-  if (!accumulate && !y_ready && decode_needs_zero_y(L, m)) {
-    const int64_t count = m * L->n;
-    const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 4096));
-    fill_zero_kernel<<<dim3(blocks), dim3(256), 0, stream>>>(y, count);
+  if (!accumulate && !y_ready && decode_needs_zero_y(L, m, set_panels(S))) {
+    for (int j = 0; j < S.count; ++j) {
+      const int64_t count = m * S.n[j];
+      const unsigned blocks = static_cast<unsigned>(std::min<int64_t>((count + 255) / 256, 4096));
+      fill_zero_kernel<<<dim3(blocks), dim3(256), 0, stream>>>(S.y[j], count);
+    }
   }
   if (L->packing == SDQ_PACK_BASE3) {
     if (!decode_reads_base3(L, m)) return set_error(SDQ_ERR_ARG, "base-3 codes need unpacking on this path");
-    switch (pick_seg(L, 1)) {
-      case 8: launch_gemv_base3_seg<8>(w, codes, scales, L, y, accumulate, stream); break;
-      case 4: launch_gemv_base3_seg<4>(w, codes, scales, L, y, accumulate, stream); break;
-      default: launch_gemv_base3_seg<2>(w, codes, scales, L, y, accumulate, stream); break;
+    switch (pick_seg(L, 1, set_panels(S))) {
+      case 8: launch_gemv_base3_seg<8>(w, S, L, accumulate, stream); break;
+      case 4: launch_gemv_base3_seg<4>(w, S, L, accumulate, stream); break;
+      default: launch_gemv_base3_seg<2>(w, S, L, accumulate, stream); break;
     }
   } else if (use_mfma(L, m)) {
-    if (L->levels == 2) launch_mfma_levels<2>(w, codes, scales, L, m, y, accumulate, stream);
-    else launch_mfma_levels<3>(w, codes, scales, L, m, y, accumulate, stream);
+    if (L->levels == 2) launch_mfma_levels<2>(w, S, L, m, accumulate, stream);
+    else launch_mfma_levels<3>(w, S, L, m, accumulate, stream);
   } else if (L->levels == 2) {
-    launch_gemv<2>(w, codes, scales, L, m, y, accumulate, stream);
+    launch_gemv<2>(w, S, L, m, accumulate, stream);
   } else {
-    launch_gemv<3>(w, codes, scales, L, m, y, accumulate, stream);
+    launch_gemv<3>(w, S, L, m, accumulate, stream);
   }
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "decode GEMV launch");

@@ -106,18 +106,51 @@ __device__ inline uint4 load_codes(const uint4* __restrict__ codes, int64_t col,
   return (it & 1) ? make_uint4(q.z, q.w, 0u, 0u) : make_uint4(q.x, q.y, 0u, 0u);
 }
 
+// Workgroups are dealt to the eight XCDs round-robin by index, and each XCD
+// has its own L2.  Workgroup `id` of `total` takes tile xcd_range(id) of an
+// order in which every XCD owns one contiguous range; the order walks pairs of
+// row tiles across the column tiles (row tile 2p, 2p + 1 of column tile c are
+// neighbours), so the workgroups resident on one XCD at a time cover a block
+// of two row tiles by many column tiles and its L2 fetches each x_tilde and
+// code slice once for all of them.
+constexpr int kXcds = 8;
+__device__ inline void prefill_tile(int64_t id, int64_t total, int64_t m_tiles, int64_t n_tiles,
+                                    int64_t* mt, int64_t* nt) {
+  const int64_t xcd = id % kXcds, j = id / kXcds;
+  const int64_t per = total / kXcds, rem = total % kXcds;
+  const int64_t t = xcd * per + (xcd < rem ? xcd : rem) + j;
+  const int64_t pair_tiles = 2 * n_tiles;          // tiles of one pair of row tiles
+  const int64_t p = t / pair_tiles, r = t % pair_tiles;
+  const int64_t rows_in_pair = min<int64_t>(2, m_tiles - 2 * p);
+  *nt = r / rows_in_pair;
+  *mt = 2 * p + r % rows_in_pair;
+}
+
 template <int LEVELS>
 __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
-    const _Float16* __restrict__ xt, const uint4* __restrict__ codes,
-    const float* __restrict__ scales, int64_t m, int64_t n, int64_t n_pad, int64_t n_chunks,
-    int64_t k_up_pad, float* __restrict__ y, int accumulate) {
+    const _Float16* __restrict__ xt, LinearSet S, int64_t m, int64_t n_chunks, int64_t k_up_pad,
+    int64_t m_tiles, int64_t n_tiles, int accumulate) {
   __shared__ __attribute__((aligned(1024))) _Float16 As[kABufs][kTileHalves];
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
   const int half = lane / 32;
-  const int64_t m0 = static_cast<int64_t>(blockIdx.y) * kBM;
-  const int64_t n0 = static_cast<int64_t>(blockIdx.x) * kBN + wave * 64;
+  int64_t mt, nt;
+  prefill_tile(blockIdx.x, static_cast<int64_t>(gridDim.x), m_tiles, n_tiles, &mt, &nt);
+  const int lin = [&] {                           // units: column tiles of kBN weight rows
+    int j = 0;
+#pragma unroll
+    for (int i = 1; i < kMaxGroup; ++i)
+      if (i < S.count && nt >= S.first[i]) j = i;
+    return j;
+  }();
+  const int64_t n = S.n[lin];
+  const int64_t n_pad = (n + kPanel - 1) / kPanel * kPanel;
+  const uint4* __restrict__ codes = static_cast<const uint4*>(S.codes[lin]);
+  const float* __restrict__ scales = S.scales[lin];
+  float* __restrict__ y = S.y[lin];
+  const int64_t m0 = mt * kBM;
+  const int64_t n0 = (nt - S.first[lin]) * kBN + wave * 64;
   const int64_t cols[2] = {n0 + lane % 32, n0 + 32 + lane % 32};
   const int n_iter = static_cast<int>(k_up_pad / kBK);
 
@@ -228,9 +261,12 @@ size_t prefill_ws_bytes(const sdq_layout* L, int64_t m) {
   return align_up(static_cast<size_t>(m) * k_up_pad * 2, 256) * (prefill_split(L) ? 2 : 1);
 }
 
-sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
-                                   const sdq_layout* L, float* y, bool accumulate, void* ws,
+sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, bool accumulate, void* ws,
                                    hipStream_t stream) {
+  S.first[0] = 0;
+  for (int j = 0; j < S.count; ++j) S.first[j + 1] = S.first[j] + (S.n[j] + kBN - 1) / kBN;
+  for (int j = S.count + 1; j <= kMaxGroup; ++j) S.first[j] = S.first[S.count];
+  const int64_t n_tiles = S.first[S.count];
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const size_t plane = align_up(static_cast<size_t>(m) * k_up_pad * 2, 256);
   // The kernel addresses x_tilde with 32-bit element offsets: launch row
@@ -242,15 +278,17 @@ sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* sc
     const int acc = accumulate || pass > 0 ? 1 : 0;
     for (int64_t r0 = 0; r0 < m; r0 += rows_max) {
       const int64_t mm = std::min(rows_max, m - r0);
-      const dim3 ggrid(static_cast<unsigned>((L->n + kBN - 1) / kBN), static_cast<unsigned>((mm + kBM - 1) / kBM));
+      const int64_t m_tiles = (mm + kBM - 1) / kBM;
+      const dim3 ggrid(static_cast<unsigned>(m_tiles * n_tiles));
       const _Float16* xc = xbuf + r0 * k_up_pad;
-      float* yc = y + r0 * L->n;
+      LinearSet Sc = S;
+      for (int j = 0; j < S.count; ++j) Sc.y[j] = S.y[j] + r0 * S.n[j];
       if (L->levels == 2)
-        gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(
-            xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc, acc);
+        gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(xc, Sc, mm, L->n_chunks, k_up_pad, m_tiles,
+                                                                n_tiles, acc);
       else
-        gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(
-            xc, static_cast<const uint4*>(codes), scales, mm, L->n, L->n_pad, L->n_chunks, k_up_pad, yc, acc);
+        gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(xc, Sc, mm, L->n_chunks, k_up_pad, m_tiles,
+                                                                n_tiles, acc);
     }
   }
   hipError_t e = hipGetLastError();

@@ -465,16 +465,31 @@ static size_t path_ws_bytes(const sdq_layout* P, int64_t m) {
   return m <= 16 ? decode_ws_bytes(P, m) : prefill_ws_bytes(P, m);
 }
 
-static size_t linear_ws_bytes(const sdq_layout* L, int64_t m) {
+// Workspace of a linear call over `count` linears of one layout family: the
+// path's part (the expansion at offset 0), then for base-3 codes read as
+// 2-bit fields each linear's unpacked copy.
+static size_t group_ws_bytes(const sdq_layout* Ls, int count, int64_t m) {
+  const sdq_layout* L = &Ls[0];
   if (!needs_unpack(L, m)) return path_ws_bytes(L, m);
   const sdq_layout F = fields_view(L);
-  return align_up(path_ws_bytes(&F, m), 256) + fields_codes_bytes(L);
+  size_t off = align_up(path_ws_bytes(&F, m), 256);
+  for (int j = 0; j < count; ++j) off = align_up(off + fields_codes_bytes(&Ls[j]), 256);
+  return off;
 }
+
+static size_t linear_ws_bytes(const sdq_layout* L, int64_t m) { return group_ws_bytes(L, 1, m); }
 
 size_t sdq_linear_workspace_bytes(const sdq_layout* L, int64_t m) {
   if (check_layout(L) != SDQ_OK || m < 0) return 0;
   if (m == 0) return 0;
   return linear_ws_bytes(L, m);
+}
+
+static sdq_status workspace_ok(size_t need, size_t ws_bytes, const void* ws) {
+  if (!ws || ws_bytes < need)
+    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
+  if (!aligned16(ws)) return set_error(SDQ_ERR_ARG, "workspace is not 16-byte aligned");
+  return SDQ_OK;
 }
 
 static sdq_status linear_common(const sdq_layout* L, int64_t m, size_t ws_bytes, const void* ws) {
@@ -486,15 +501,13 @@ static sdq_status linear_common(const sdq_layout* L, int64_t m, size_t ws_bytes,
     st = decode_supported(L);
     if (st != SDQ_OK) return st;
   }
-  const size_t need = linear_ws_bytes(L, m);
-  if (!ws || ws_bytes < need)
-    return set_error(SDQ_ERR_WORKSPACE, "workspace needs %zu bytes, got %zu", need, ws_bytes);
-  if (!aligned16(ws)) return set_error(SDQ_ERR_ARG, "workspace is not 16-byte aligned");
-  return SDQ_OK;
+  return workspace_ok(linear_ws_bytes(L, m), ws_bytes, ws);
 }
 
+// The expansion for layout L; `zero`: the set whose outputs the decode
+// expansion zeroes for a split-K GEMV (or NULL).
 static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
-                              void* ws, float* y_zero, void* stream, bool may_allocate = true) {
+                              void* ws, const LinearSet* zero, void* stream, bool may_allocate = true) {
   if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
   if (!x) return set_error(SDQ_ERR_ARG, "x is NULL");
   if (!aligned16(x)) return set_error(SDQ_ERR_ARG, "x is not 16-byte aligned");
@@ -504,27 +517,48 @@ static sdq_status expand_impl(const void* x, sdq_dtype xt, int64_t m, const sdq_
   sdq_status st = may_allocate ? get_tables(P, &T) : find_tables(P, &T);
   if (st != SDQ_OK) return st;
   hipStream_t s = static_cast<hipStream_t>(stream);
-  return m <= 16 ? launch_decode_expand(x, xt, m, P, T, ws, y_zero, s)
+  return m <= 16 ? launch_decode_expand(x, xt, m, P, T, ws, zero, s)
                  : launch_prefill_expand(x, xt, m, P, T, ws, s);
 }
 
-static sdq_status contract_impl(int64_t m, const void* codes, const float* scales,
-                                const sdq_layout* L, float* y, bool accumulate, void* ws,
+// The contraction of every linear of S (layout family L) against the
+// expansion in ws; base-3 codes on the paths that read 2-bit fields are
+// unpacked first, each into its own part of the workspace.
+static sdq_status contract_impl(int64_t m, LinearSet S, const sdq_layout* L, bool accumulate, void* ws,
                                 bool y_ready, void* stream) {
-  if (!codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
-  if (!aligned16(codes)) return set_error(SDQ_ERR_ARG, "codes are not 16-byte aligned");
+  for (int j = 0; j < S.count; ++j) {
+    if (!S.codes[j] || !S.scales[j] || !S.y[j]) return set_error(SDQ_ERR_ARG, "NULL pointer argument");
+    if (!aligned16(S.codes[j])) return set_error(SDQ_ERR_ARG, "codes are not 16-byte aligned");
+  }
   hipStream_t s = static_cast<hipStream_t>(stream);
   const sdq_layout F = fields_view(L);
   const sdq_layout* P = L;
   if (needs_unpack(L, m)) {
     P = &F;
-    uint32_t* fields = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + align_up(path_ws_bytes(P, m), 256));
-    sdq_status st = launch_unpack_base3(codes, L, fields, s);
-    if (st != SDQ_OK) return st;
-    codes = fields;
+    size_t off = align_up(path_ws_bytes(P, m), 256);
+    for (int j = 0; j < S.count; ++j) {
+      sdq_layout Lj = *L;
+      Lj.n = S.n[j];
+      Lj.n_pad = (S.n[j] + kPanel - 1) / kPanel * kPanel;
+      uint32_t* fields = reinterpret_cast<uint32_t*>(static_cast<char*>(ws) + off);
+      sdq_status st = launch_unpack_base3(S.codes[j], &Lj, fields, s);
+      if (st != SDQ_OK) return st;
+      S.codes[j] = fields;
+      off = align_up(off + fields_codes_bytes(&Lj), 256);
+    }
   }
-  return m <= 16 ? launch_decode_contract(m, codes, scales, P, y, accumulate, ws, y_ready, s)
-                 : launch_prefill_contract(m, codes, scales, P, y, accumulate, ws, s);
+  return m <= 16 ? launch_decode_contract(m, S, P, accumulate, ws, y_ready, s)
+                 : launch_prefill_contract(m, S, P, accumulate, ws, s);
+}
+
+static LinearSet single_set(const void* codes, const float* scales, const sdq_layout* L, float* y) {
+  LinearSet S;
+  S.count = 1;
+  S.codes[0] = codes;
+  S.scales[0] = scales;
+  S.y[0] = y;
+  S.n[0] = L->n;
+  return S;
 }
 
 sdq_status sdq_expand_activations(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
@@ -539,7 +573,7 @@ sdq_status sdq_linear_expanded(int64_t m, const void* codes, const float* scales
                                size_t ws_bytes, void* stream) {
   sdq_status st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK || m == 0 || L->n == 0) return st;
-  return contract_impl(m, codes, scales, L, y, accumulate != 0, ws, false, stream);
+  return contract_impl(m, single_set(codes, scales, L, y), L, accumulate != 0, ws, false, stream);
 }
 
 // Argument checks of sdq_linear that precede the workspace check.
@@ -555,6 +589,19 @@ static sdq_status linear_args(const void* x, sdq_dtype xt, int64_t m, const void
   return SDQ_OK;
 }
 
+// Expansion then contraction of a set on one workspace (sdq_linear and
+// sdq_linear_group).  Decode: the expansion also zeroes y when the GEMV
+// will add into it.
+static sdq_status run_set(const void* x, sdq_dtype xt, int64_t m, const LinearSet& S, const sdq_layout* L,
+                          int32_t accumulate, void* ws, void* stream, bool may_allocate) {
+  const sdq_layout F = fields_view(L);
+  const sdq_layout* P = needs_unpack(L, m) ? &F : L;
+  const bool zero_in_expand = !accumulate && m <= 16 && decode_needs_zero_y(P, m, set_panels(S));
+  sdq_status st = expand_impl(x, xt, m, L, ws, zero_in_expand ? &S : nullptr, stream, may_allocate);
+  if (st != SDQ_OK) return st;
+  return contract_impl(m, S, L, accumulate != 0, ws, true, stream);
+}
+
 }  // extern "C"
 
 sdq_status sdq::linear_impl(const void* x, sdq_dtype xt, int64_t m, const void* codes, const float* scales,
@@ -564,13 +611,7 @@ sdq_status sdq::linear_impl(const void* x, sdq_dtype xt, int64_t m, const void* 
   if (st != SDQ_OK || m == 0 || L->n == 0) return st;
   st = linear_common(L, m, ws_bytes, ws);
   if (st != SDQ_OK) return st;
-  // Decode: the expansion also zeroes y when the GEMV will add into it.
-  const sdq_layout F = fields_view(L);
-  const sdq_layout* P = needs_unpack(L, m) ? &F : L;
-  const bool zero_in_expand = !accumulate && m <= 16 && decode_needs_zero_y(P, m);
-  st = expand_impl(x, xt, m, L, ws, zero_in_expand ? y : nullptr, stream, may_allocate);
-  if (st != SDQ_OK) return st;
-  return contract_impl(m, codes, scales, L, y, accumulate != 0, ws, true, stream);
+  return run_set(x, xt, m, single_set(codes, scales, L, y), L, accumulate, ws, stream, may_allocate);
 }
 
 size_t sdq::linear_ws_need(const sdq_layout* L, int64_t m) {
@@ -584,6 +625,74 @@ sdq_status sdq_linear(const void* x, sdq_dtype xt, int64_t m, const void* codes,
                       const float* scales, const sdq_layout* L, float* y, int32_t accumulate,
                       void* ws, size_t ws_bytes, void* stream) {
   return linear_impl(x, xt, m, codes, scales, L, y, accumulate, ws, ws_bytes, stream, true);
+}
+
+// Layouts of one group: valid, and equal in everything the expansion and the
+// code geometry depend on (all but the row count).
+static sdq_status check_group(const sdq_layout* Ls, int32_t count) {
+  if (count < 1 || count > kMaxGroup)
+    return set_error(SDQ_ERR_ARG, "count=%d: a group holds 1 to %d linears", count, kMaxGroup);
+  if (!Ls) return set_error(SDQ_ERR_ARG, "layouts is NULL");
+  for (int j = 0; j < count; ++j) {
+    sdq_status st = check_layout(&Ls[j]);
+    if (st != SDQ_OK) return st;
+    const sdq_layout& a = Ls[0];
+    const sdq_layout& b = Ls[j];
+    if (a.k != b.k || a.block != b.block || a.m_up != b.m_up || a.levels != b.levels ||
+        a.hadamard != b.hadamard || a.packing != b.packing ||
+        !std::equal(a.had_signs, a.had_signs + 8, b.had_signs))
+      return set_error(SDQ_ERR_ARG, "linear %d differs from linear 0 in k, block, M, levels, Had or packing", j);
+  }
+  return SDQ_OK;
+}
+
+size_t sdq_linear_group_workspace_bytes(const sdq_layout* layouts, int32_t count, int64_t m) {
+  if (check_group(layouts, count) != SDQ_OK || m <= 0) return 0;
+  return group_ws_bytes(layouts, count, m);
+}
+
+// The set of a group call (empty linears left out) after its checks.
+static sdq_status group_set(int64_t m, int32_t count, const void* const* codes, const float* const* scales,
+                            const sdq_layout* layouts, float* const* y, size_t ws_bytes, const void* ws,
+                            LinearSet* S) {
+  sdq_status st = check_group(layouts, count);
+  if (st != SDQ_OK) return st;
+  if (m < 0) return set_error(SDQ_ERR_ARG, "m < 0");
+  if (!codes || !scales || !y) return set_error(SDQ_ERR_ARG, "NULL pointer array");
+  for (int j = 0; j < count; ++j) {
+    if (layouts[j].n == 0) continue;            // nothing to compute for an empty linear
+    S->codes[S->count] = codes[j];
+    S->scales[S->count] = scales[j];
+    S->y[S->count] = y[j];
+    S->n[S->count] = layouts[j].n;
+    ++S->count;
+  }
+  if (m == 0 || S->count == 0) return SDQ_OK;
+  if (m <= 16) {
+    st = decode_supported(&layouts[0]);
+    if (st != SDQ_OK) return st;
+  }
+  return workspace_ok(group_ws_bytes(layouts, count, m), ws_bytes, ws);
+}
+
+sdq_status sdq_linear_group(const void* x, sdq_dtype xt, int64_t m, int32_t count, const void* const* codes,
+                            const float* const* scales, const sdq_layout* layouts, float* const* y,
+                            int32_t accumulate, void* ws, size_t ws_bytes, void* stream) {
+  if (xt != SDQ_F16 && xt != SDQ_BF16 && xt != SDQ_F32) return set_error(SDQ_ERR_ARG, "bad dtype");
+  LinearSet S;
+  sdq_status st = group_set(m, count, codes, scales, layouts, y, ws_bytes, ws, &S);
+  if (st != SDQ_OK || m == 0 || S.count == 0) return st;
+  if (!x) return set_error(SDQ_ERR_ARG, "x is NULL");
+  return run_set(x, xt, m, S, &layouts[0], accumulate, ws, stream, true);
+}
+
+sdq_status sdq_linear_group_expanded(int64_t m, int32_t count, const void* const* codes,
+                                     const float* const* scales, const sdq_layout* layouts, float* const* y,
+                                     int32_t accumulate, void* ws, size_t ws_bytes, void* stream) {
+  LinearSet S;
+  sdq_status st = group_set(m, count, codes, scales, layouts, y, ws_bytes, ws, &S);
+  if (st != SDQ_OK || m == 0 || S.count == 0) return st;
+  return contract_impl(m, S, &layouts[0], accumulate != 0, ws, false, stream);
 }
 
 // ---------------------------------------------------------------------------

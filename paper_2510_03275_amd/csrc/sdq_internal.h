@@ -108,21 +108,43 @@ sdq_status launch_encode_blocks(const float* w, int64_t ldw, int64_t b0, int64_t
                                 const QuantWs& ws, uint32_t* rmax_acc, const uint32_t* rmax_scale,
                                 hipStream_t stream);
 
+// The linears one contraction launch covers (sdq_linear: one; sdq_linear_group:
+// up to kMaxGroup).  They share the input and the layout's k, block, M, levels,
+// Had and packing (the expansion), and have their own rows, codes, scales and
+// outputs.  Passed to the kernels by value; a workgroup finds its linear from
+// its place in the launch (the prefix sums `first` of the units -- panel
+// groups, panels or column tiles -- each linear contributes).
+constexpr int kMaxGroup = 4;
+struct LinearSet {
+  int count = 0;
+  const void* codes[kMaxGroup] = {};
+  const float* scales[kMaxGroup] = {};
+  float* y[kMaxGroup] = {};
+  int64_t n[kMaxGroup] = {};
+  int64_t first[kMaxGroup + 1] = {};   // filled by the launcher for its unit
+};
+// Rows over all linears of the set, rounded up to whole panels per linear.
+inline int64_t set_panels(const LinearSet& S) {
+  int64_t p = 0;
+  for (int j = 0; j < S.count; ++j) p += (S.n[j] + kPanel - 1) / kPanel;
+  return p;
+}
+
 // Decode path (m <= 16): expansion (fp32 x_tilde) then LUT GEMV.
 size_t decode_ws_bytes(const sdq_layout* L, int64_t m);
 sdq_status decode_supported(const sdq_layout* L);
 // When the GEMV splits K it accumulates into y atomically; y must then start
 // at zero (or hold the values to accumulate onto): the expansion zeroes it if
-// handed y (y_zero), else the GEMV launch does unless y_ready is set.
-bool decode_needs_zero_y(const sdq_layout* L, int64_t m);
+// handed the set (zero), else the GEMV launch does unless y_ready is set.
+// `panels`: the panels of the whole set (the split depends on the grid size).
+bool decode_needs_zero_y(const sdq_layout* L, int64_t m, int64_t panels);
 // Whether the decode path reads base-3 codes as stored (one activation row,
 // table GEMV); every other path reads them unpacked to fields_view(L).
 bool decode_reads_base3(const sdq_layout* L, int64_t m);
 sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
-                                const Tables* T, void* ws, float* y_zero, hipStream_t stream);
+                                const Tables* T, void* ws, const LinearSet* zero, hipStream_t stream);
 // accumulate: y += result instead of y = result.
-sdq_status launch_decode_contract(int64_t m, const void* codes, const float* scales,
-                                  const sdq_layout* L, float* y, bool accumulate, void* ws,
+sdq_status launch_decode_contract(int64_t m, LinearSet set, const sdq_layout* L, bool accumulate, void* ws,
                                   bool y_ready, hipStream_t stream);
 
 // Prefill path (m > 16): expansion (fp16 x_tilde) then MFMA GEMM.  Layouts
@@ -131,8 +153,7 @@ bool prefill_split(const sdq_layout* L);
 size_t prefill_ws_bytes(const sdq_layout* L, int64_t m);
 sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
                                  const Tables* T, void* ws, hipStream_t stream);
-sdq_status launch_prefill_contract(int64_t m, const void* codes, const float* scales,
-                                   const sdq_layout* L, float* y, bool accumulate, void* ws,
+sdq_status launch_prefill_contract(int64_t m, LinearSet set, const sdq_layout* L, bool accumulate, void* ws,
                                    hipStream_t stream);
 
 // Block compensation (Algorithm 1's block loop), fp64.

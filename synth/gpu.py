@@ -22,6 +22,9 @@ def _load():
     lib.synth_normal_f32.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int64, ctypes.c_int64,
                                      ctypes.c_uint64, ctypes.c_double, ctypes.c_int, ctypes.c_uint64,
                                      ctypes.c_void_p]
+    lib.synth_read_probe.restype = ctypes.c_int
+    lib.synth_read_probe.argtypes = [ctypes.c_void_p, ctypes.c_int64, ctypes.c_int, ctypes.c_int, ctypes.c_void_p,
+                                     ctypes.c_void_p]
     return lib
 
 
@@ -52,3 +55,12 @@ def activations_gpu(seed: int, stream: int, m: int, k: int, device="cuda"):
     import torch
     out = torch.empty((m, k), dtype=torch.float32, device=device)
     return _fill(out, m, k, 0, stream_base(seed, 2 * stream + 1), 1.0, False)
+
+
+def read_probe(buf, blocks: int, unroll: int, sink) -> None:
+    """One streaming read of the device buffer `buf` (a multiple of 16 bytes)."""
+    import torch
+    st = _lib.synth_read_probe(buf.data_ptr(), buf.numel() * buf.element_size() // 16, blocks, unroll,
+                               sink.data_ptr(), torch.cuda.current_stream().cuda_stream)
+    if st != 0:
+        raise RuntimeError(f"synth_read_probe failed ({st})")

@@ -301,3 +301,21 @@ def test_noalloc_entry_point_validates_before_gpu_work():
     # a prefill call beyond the fixed scratch is refused before anything else
     assert lib.sdq_linear_noalloc(fake, 0, 2048, fake, fake, ctypes.byref(L), fake, 0, None) == -6
     assert lib.sdq_linear_noalloc(fake, 0, 0, fake, fake, ctypes.byref(L), fake, 0, None) in (0, -7)
+
+
+def test_group_entry_point_validates_before_gpu_work():
+    lib = P.lib()
+    fake = ctypes.c_void_p(0x1000)
+    a = P.sdq_layout_init(64, 512, 2.0, 3)
+    b = P.sdq_layout_init(128, 512, 2.5, 3)
+    c = P.sdq_layout_init(128, 512, 2.0, 3)
+    ptrs = (ctypes.c_void_p * 2)(fake, fake)
+    assert P.sdq_linear_group_workspace_bytes([a, c], 1) >= P.sdq_linear_workspace_bytes(a, 1)
+    assert P.sdq_linear_group_workspace_bytes([a, b], 1) == 0           # M differs
+    assert P.sdq_linear_group_workspace_bytes([a] * 5, 1) == 0          # more than four
+    arr = (P.sdq_layout * 2)(a, b)
+    assert lib.sdq_linear_group(fake, 0, 1, 2, ptrs, ptrs, arr, ptrs, 0, fake, 1 << 30, None) == -1
+    arr = (P.sdq_layout * 2)(a, c)
+    assert lib.sdq_linear_group(fake, 0, 1, 0, ptrs, ptrs, arr, ptrs, 0, fake, 1 << 30, None) == -1
+    assert lib.sdq_linear_group(fake, 0, 1, 2, ptrs, ptrs, arr, ptrs, 0, fake, 16, None) == -6
+    assert lib.sdq_linear_group(fake, 0, 0, 2, ptrs, ptrs, arr, ptrs, 0, None, 0, None) == 0   # m = 0
