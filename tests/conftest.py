@@ -11,6 +11,11 @@ if ROOT not in sys.path:
 def pytest_configure(config):
     config.addinivalue_line("markers", "gpu: needs an MI355X (gfx950) GPU and the built HIP library")
     config.addinivalue_line("markers", "slow: longer CPU test")
+    # The oracle's process pool forks from a server started now, before any
+    # test initialises the GPU (GPU runs only).
+    if "not gpu" not in (config.getoption("markexpr") or "").replace("  ", " "):
+        from tests import oracle_pool
+        oracle_pool.start()
 
 
 @pytest.fixture(autouse=True)
