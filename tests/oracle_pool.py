@@ -111,6 +111,23 @@ def run_task(t: Task) -> Tuple:
     return packed, r.scales, ys, keep
 
 
+def submit(pool, tasks: List[Task]):
+    """Start `tasks` on `pool`; results come back in task order through `gather`."""
+    return pool.imap(run_task, tasks, chunksize=1)
+
+
+def gather(pending, count: int, label: str, task_timeout_s: float = 300.0) -> List[Tuple]:
+    """The results of `count` submitted tasks, in order; one line on stdout per
+    quarter of them done (a long oracle leg stays visibly alive)."""
+    out = []
+    step = max(1, count // 4)
+    for i in range(count):
+        out.append(pending.next(timeout=task_timeout_s))
+        if (i + 1) % step == 0 or i + 1 == count:
+            print(f"[oracle] {label}: {i + 1}/{count} tasks done", flush=True)
+    return out
+
+
 def panel_tasks(n: int, parts: int, **kw) -> List[Task]:
     """Split rows 0..n into at most `parts` tasks of whole 64-row panels."""
     panels = (n + 63) // 64

@@ -22,7 +22,6 @@ from tests.gpu_common import TOL, require_gpu, to_device_x
 
 pytestmark = pytest.mark.gpu
 
-POOL_WAIT_S = 160
 
 
 def _xspec(wl, lin, m, rows=None):
@@ -37,10 +36,10 @@ def _check_every_row(torch, wl, lin, osr, batches):
     for m in batches:
         rows = None if m <= 64 else list(range(0, m, max(1, m // 256)))[:256]
         specs.append(_xspec(wl, lin, m, rows))
-    tasks = OP.panel_tasks(lin.n, OP.workers(), seed=wl.seed, linear_id=lin.linear_id, k=lin.k,
+    tasks = OP.panel_tasks(lin.n, 4 * OP.workers(), seed=wl.seed, linear_id=lin.linear_id, k=lin.k,
                            sigma=lin.sigma, outliers=wl.outliers, osr=osr, levels=wl.levels, xs=specs)
     with OP.pool() as pool:
-        pending = pool.map_async(OP.run_task, tasks, chunksize=1)
+        pending = OP.submit(pool, tasks)
         w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
         enc = P.quantize(w, osr, wl.levels)
         del w
@@ -56,7 +55,7 @@ def _check_every_row(torch, wl, lin, osr, batches):
         scales = enc.scales.cpu().numpy()
         del enc
         torch.cuda.empty_cache()
-        results = pending.get(timeout=POOL_WAIT_S)
+        results = OP.gather(pending, len(tasks), lin.name)
     L = P.sdq_layout_init(lin.n, lin.k, osr, wl.levels)
     panel_bytes = int(L.n_chunks) * 64 * 16
     assert codes.size == int(L.n_pad) // 64 * panel_bytes
@@ -160,7 +159,7 @@ def test_llama70b_stack_64_rows_of_every_linear_kind_at_eight_depths():
                      xs=[OP.XSpec(wl.seed, 200 + m, m, lin.k, wl.x_dtype) for m in wl.batches])
              for lin, o, rows in picks]
     with OP.pool() as pool:
-        pending = pool.map_async(OP.run_task, tasks, chunksize=1)
+        pending = OP.submit(pool, tasks)
         got = []
         xs = {}
         for lin, o, rows in picks:
@@ -178,7 +177,7 @@ def test_llama70b_stack_64_rows_of_every_linear_kind_at_eight_depths():
             got.append((_rows_codes(torch, enc, rows), sc, ys))
             del enc
             torch.cuda.empty_cache()
-        results = pending.get(timeout=POOL_WAIT_S)
+        results = OP.gather(pending, len(tasks), "70B stack rows")
     for (lin, o, rows), (codes, sc, ys), (_, ref_sc, ref_ys, ref_codes) in zip(picks, got, results):
         assert np.array_equal(codes, ref_codes), (lin.name, lin.layer)
         assert np.array_equal(sc.view(np.uint32), ref_sc.view(np.uint32)), (lin.name, lin.layer)
