@@ -241,7 +241,9 @@ sdq_status sdq_quantize_compensated(const float* w_dev, const sdq_layout* layout
  *                 rows in groups of four, per block in chunk slots), then the
  *                 fp32 plane scale of every (row, block);
  *   m > 16:       fp16 x_tilde, m x k_up rounded up to whole chunks (twice,
- *                 an fp16 pair hi + lo, for layouts with SDQ_HAD_NONE);
+ *                 an fp16 pair hi + lo, for layouts with SDQ_HAD_NONE), each
+ *                 row scaled by a power of two p_i that keeps it inside
+ *                 fp16's normal range, then p_i and 1 / p_i (fp32 [m] each);
  * for a base-3 layout and m > 1 the chunks are those of 2-bit fields, and the
  * 2-bit copy of the codes follows (n_pad x ceil(k_up / 64) x 16 bytes). */
 size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
@@ -319,7 +321,8 @@ sdq_status sdq_linear_group_expanded(int64_t m, int32_t count, const void* const
  *  - Calls needing more workspace than that (sdq_linear_workspace_bytes)
  *    return SDQ_ERR_WORKSPACE; they fit for every one-to-sixteen-row call on
  *    2-bit fields up to k = 28672 at OSR 8, and prefill while
- *    m * k_up * 2 bytes (twice that without Had) stays within the limit.
+ *    m * k_up * 2 bytes (twice that without Had) plus 8 m bytes of row
+ *    factors stay within the limit.
  *  - The coefficient tables are not built here: call sdq_prepare_layout for
  *    the layout on the current device first, else SDQ_ERR_UNSUPPORTED.
  *  - All calls on one GPU share its array; nothing in it needs to start at

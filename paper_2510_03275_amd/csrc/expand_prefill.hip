@@ -4,9 +4,18 @@
 //   expand   x_tilde_b = x_b E with E = Had D^T (B x M) for every block b: a
 //            batched GEMM.  E is held as an fp16 pair hi + lo, so x E_hi + x E_lo
 //            reproduces the fp64 product to ~2^-22 relative for fp16 / bf16
-//            inputs (both exact in fp16 at these magnitudes); fp32 inputs add
-//            x_lo E_hi.  The result is rounded once to fp16 (without Had also
-//            kept as an fp16 pair, the GEMM then running over both halves).
+//            inputs; fp32 inputs add x_lo E_hi.  The result is rounded once
+//            to fp16 (without Had also kept as an fp16 pair, the GEMM then
+//            running over both halves).
+//
+//   scale    fp16 holds normal numbers from 2^-14 to 65504 only, so every
+//            activation row i is first multiplied by a power of two p_i
+//            (exact) picked from its largest magnitude a_i:
+//            a_i max(e1max, 1) p_i < 2^14.  Each x_tilde sample of the row,
+//            bounded by a_i e1max, then stays below 2^14 (no overflow in x,
+//            x_lo or x_tilde), and the row's large samples sit far above the
+//            subnormals whatever the row's magnitude.  The GEMM multiplies
+//            its sums by 1 / p_i (exact).
 //
 // Built with the matrix-core accumulators in VGPRs (the build sets the
 // compiler's MFMA VGPR form for this file): left to its heuristics the
@@ -46,6 +55,54 @@ __device__ inline int64_t xcd_tile(int64_t id, int64_t n) {
   return xcd * per + (xcd < rem ? xcd : rem) + j;
 }
 
+// Row factors: wave w of workgroup g takes activation row 4 g + w, reduces
+// max |x| over its k values (16-byte loads, 1 KB per wave load) and writes
+// p = 2^e and 1 / p with e = 14 - ceil2(a max(e1max, 1)), where ceil2(v) is
+// the exponent ex of v = f 2^ex, f in [0.5, 1) (so v < 2^ex).  A row of zeros
+// or with a non-finite maximum keeps p = 1.
+template <sdq_dtype XT>
+__global__ __launch_bounds__(256) void prefill_row_scale_kernel(const void* __restrict__ x, int64_t m,
+                                                                int64_t k, float e1, float* __restrict__ fac) {
+  const int lane = threadIdx.x % 64;
+  const int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + threadIdx.x / 64;
+  if (i >= m) return;
+  constexpr int PER = XT == SDQ_F32 ? 4 : 8;          // values per 16 bytes
+  const uint4* row = reinterpret_cast<const uint4*>(static_cast<const char*>(x) +
+                                                    i * k * (XT == SDQ_F32 ? 4 : 2));
+  float a = 0.0f;
+  for (int64_t j = lane; j < k / PER; j += 64) {
+    const uint4 u = row[j];
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int q = 0; q < 4; ++q) {
+      if (XT == SDQ_F32) {
+        a = fmaxf(a, fabsf(__uint_as_float(w[q])));
+      } else if (XT == SDQ_BF16) {
+        a = fmaxf(a, fabsf(__uint_as_float(w[q] << 16)));
+        a = fmaxf(a, fabsf(__uint_as_float(w[q] & 0xFFFF0000u)));
+      } else {
+        _Float16 h[2];
+        __builtin_memcpy(h, &w[q], 4);
+        a = fmaxf(a, fabsf(static_cast<float>(h[0])));
+        a = fmaxf(a, fabsf(static_cast<float>(h[1])));
+      }
+    }
+  }
+#pragma unroll
+  for (int off = 32; off > 0; off /= 2) a = fmaxf(a, __shfl_xor(a, off, 64));
+  if (lane == 0) {
+    const float v = a * fmaxf(e1, 1.0f);
+    int e = 0;
+    if (v > 0.0f && v <= 3.4e38f) {
+      int ex;
+      frexpf(v, &ex);
+      e = min(max(14 - ex, -126), 126);
+    }
+    fac[i] = ldexpf(1.0f, e);
+    fac[m + i] = ldexpf(1.0f, -e);
+  }
+}
+
 // Tiled expansion: workgroup tile kXTM activation rows x 128 samples of one
 // block, t in steps of 64 through LDS (x as fp16 hi (+ lo for fp32 inputs),
 // E^T as fp16 hi and lo), so each operand element fetched from memory feeds
@@ -58,7 +115,7 @@ constexpr int kXTN = 128, kXTK = 64, kXLd = kXTK + 8;
 
 template <sdq_dtype XT, int kXTM>
 __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
-    const void* __restrict__ x, int64_t m, int64_t k, int B, int m_up,
+    const void* __restrict__ x, const float* __restrict__ fac, int64_t m, int64_t k, int B, int m_up,
     int64_t k_up, int64_t k_up_pad, const uint16_t* __restrict__ et_hi,
     const uint16_t* __restrict__ et_lo, _Float16* __restrict__ xt_out,
     _Float16* __restrict__ xt_lo_out) {
@@ -105,6 +162,9 @@ __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
   // in flight together; conversion happens when the tile is stored to LDS.
   constexpr int XW = XT == SDQ_F32 ? 2 : 1;          // uint4 per 8 values
   uint4 xr[XIT][XW], eh[4], el[4];
+  float px[XIT];                                     // p_i of the rows this thread stages
+#pragma unroll
+  for (int it = 0; it < XIT; ++it) px[it] = fac[min<int64_t>(i0 + (tid + 256 * it) / 8, m - 1)];
 #define SDQ_FETCH(T0)                                                                          \
   do {                                                                                         \
     _Pragma("unroll") for (int it = 0; it < XIT; ++it) {                                       \
@@ -136,20 +196,23 @@ __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
       const int idx = tid + 256 * it;
       const int r = idx / 8, sg = idx % 8;
       const bool ok = i0 + r < m;
+      const float p = px[it];
       half8 hi, lo;
       if (XT == SDQ_F16) {
-        hi = *reinterpret_cast<const half8*>(&xr[it][0]);
+        const half8 h = *reinterpret_cast<const half8*>(&xr[it][0]);
+#pragma unroll
+        for (int q = 0; q < 8; ++q) hi[q] = static_cast<_Float16>(static_cast<float>(h[q]) * p);
       } else if (XT == SDQ_BF16) {
         const uint32_t w[4] = {xr[it][0].x, xr[it][0].y, xr[it][0].z, xr[it][0].w};
 #pragma unroll
         for (int q = 0; q < 8; ++q)
-          hi[q] = static_cast<_Float16>(__uint_as_float(((w[q / 2] >> (16 * (q % 2))) & 0xFFFFu) << 16));
+          hi[q] = static_cast<_Float16>(__uint_as_float(((w[q / 2] >> (16 * (q % 2))) & 0xFFFFu) << 16) * p);
       } else {
         const uint4 u0 = xr[it][0], u1 = xr[it][XW - 1];
         const uint32_t w[8] = {u0.x, u0.y, u0.z, u0.w, u1.x, u1.y, u1.z, u1.w};
 #pragma unroll
         for (int q = 0; q < 8; ++q) {
-          const float f = __uint_as_float(w[q]);
+          const float f = __uint_as_float(w[q]) * p;
           hi[q] = static_cast<_Float16>(f);
           lo[q] = static_cast<_Float16>(f - static_cast<float>(hi[q]));
         }
@@ -231,6 +294,11 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
                                  const Tables* T, void* ws, hipStream_t stream) {
   _Float16* xbuf = static_cast<_Float16*>(ws);
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
+  float* fac = reinterpret_cast<float*>(static_cast<char*>(ws) + prefill_planes_bytes(L, m));
+  const dim3 sgrid(static_cast<unsigned>((m + 3) / 4));
+  if (xt == SDQ_F32) prefill_row_scale_kernel<SDQ_F32><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac);
+  else if (xt == SDQ_BF16) prefill_row_scale_kernel<SDQ_BF16><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac);
+  else prefill_row_scale_kernel<SDQ_F16><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac);
   _Float16* xlo = prefill_split(L)
                       ? reinterpret_cast<_Float16*>(static_cast<char*>(ws) +
                                                     align_up(static_cast<size_t>(m) * k_up_pad * 2, 256))
@@ -241,7 +309,7 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
   const dim3 tgrid(static_cast<unsigned>(((L->m_up + kXTN - 1) / kXTN) * L->nb * ((m + tm - 1) / tm)));
 #define SDQ_XT(XT)                                                                              \
   expand_prefill_tiled_kernel<XT, tm><<<tgrid, dim3(256), 0, stream>>>(                         \
-      x, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf, xlo)
+      x, fac, m, L->k, L->block, L->m_up, L->k_up, k_up_pad, T->et_hi, T->et_lo, xbuf, xlo)
   if (xt == SDQ_F32) SDQ_XT(SDQ_F32);
   else if (xt == SDQ_BF16) SDQ_XT(SDQ_BF16);
   else SDQ_XT(SDQ_F16);

@@ -126,11 +126,14 @@ __device__ inline void prefill_tile(int64_t id, int64_t total, int64_t m_tiles, 
   *mt = 2 * p + r % rows_in_pair;
 }
 
+// row_inv: 1 / p_i of every activation row, the powers of two the expansion
+// scaled the rows by; the epilogue multiplies them back out (exact).
 template <int LEVELS>
 __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
-    const _Float16* __restrict__ xt, LinearSet S, int64_t m, int64_t n_chunks, int64_t k_up_pad,
-    int64_t m_tiles, int64_t n_tiles, int accumulate) {
+    const _Float16* __restrict__ xt, const float* __restrict__ row_inv, LinearSet S, int64_t m,
+    int64_t n_chunks, int64_t k_up_pad, int64_t m_tiles, int64_t n_tiles, int accumulate) {
   __shared__ __attribute__((aligned(1024))) _Float16 As[kABufs][kTileHalves];
+  __shared__ float rinv[kBM];
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
@@ -182,6 +185,8 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
                                        (lds_void_ptr)(dst_ + j * 8 * kBK), 16, 0, 0);            \
   } while (0)
 
+  static_assert(kBM == 256, "one row factor per thread");
+  rinv[tid] = m0 + tid < m ? row_inv[m0 + tid] : 1.0f;
   const int it1 = n_iter > 1 ? 1 : 0;
   SDQ_FILL_A(0, 0);
   SDQ_FILL_A(1, it1);
@@ -245,9 +250,10 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     for (int r = 0; r < 8; ++r)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int64_t row = m0 + r * 32 + 8 * (v / 4) + 4 * half + (v % 4);
+        const int lr = r * 32 + 8 * (v / 4) + 4 * half + (v % 4);
+        const int64_t row = m0 + lr;
         if (row < m) {
-          const float val = acc[r][c][v] * s;
+          const float val = acc[r][c][v] * s * rinv[lr];
           y[row * n + col] = accumulate ? y[row * n + col] + val : val;
         }
       }
@@ -256,9 +262,13 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
 
 }  // namespace
 
-size_t prefill_ws_bytes(const sdq_layout* L, int64_t m) {
+size_t prefill_planes_bytes(const sdq_layout* L, int64_t m) {
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   return align_up(static_cast<size_t>(m) * k_up_pad * 2, 256) * (prefill_split(L) ? 2 : 1);
+}
+
+size_t prefill_ws_bytes(const sdq_layout* L, int64_t m) {
+  return prefill_planes_bytes(L, m) + align_up(static_cast<size_t>(m) * 2 * sizeof(float), 256);
 }
 
 sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, bool accumulate, void* ws,
@@ -269,6 +279,7 @@ sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, 
   const int64_t n_tiles = S.first[S.count];
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const size_t plane = align_up(static_cast<size_t>(m) * k_up_pad * 2, 256);
+  const float* row_inv = reinterpret_cast<const float*>(static_cast<const char*>(ws) + prefill_planes_bytes(L, m)) + m;
   // The kernel addresses x_tilde with 32-bit element offsets: launch row
   // chunks of at most 2^31 elements.
   const int64_t rows_max = std::max<int64_t>(kBM, ((int64_t{1} << 31) / k_up_pad) / kBM * kBM);
@@ -284,11 +295,11 @@ sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, 
       LinearSet Sc = S;
       for (int j = 0; j < S.count; ++j) Sc.y[j] = S.y[j] + r0 * S.n[j];
       if (L->levels == 2)
-        gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(xc, Sc, mm, L->n_chunks, k_up_pad, m_tiles,
-                                                                n_tiles, acc);
+        gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks, k_up_pad,
+                                                                m_tiles, n_tiles, acc);
       else
-        gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(xc, Sc, mm, L->n_chunks, k_up_pad, m_tiles,
-                                                                n_tiles, acc);
+        gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks, k_up_pad,
+                                                                m_tiles, n_tiles, acc);
     }
   }
   hipError_t e = hipGetLastError();

@@ -148,8 +148,11 @@ sdq_status launch_decode_contract(int64_t m, LinearSet set, const sdq_layout* L,
                                   bool y_ready, hipStream_t stream);
 
 // Prefill path (m > 16): expansion (fp16 x_tilde) then MFMA GEMM.  Layouts
-// without Had keep x_tilde as an fp16 pair (prefill_split).
+// without Had keep x_tilde as an fp16 pair (prefill_split).  The workspace:
+// the fp16 x_tilde plane(s) (prefill_planes_bytes), then the per-row powers of
+// two p_i [m] and 1 / p_i [m] (fp32) that keep x_tilde inside fp16's range.
 bool prefill_split(const sdq_layout* L);
+size_t prefill_planes_bytes(const sdq_layout* L, int64_t m);
 size_t prefill_ws_bytes(const sdq_layout* L, int64_t m);
 sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const sdq_layout* L,
                                  const Tables* T, void* ws, hipStream_t stream);

@@ -6,6 +6,7 @@ import pytest
 import oracle
 import synth
 from oracle import layout as LY
+from oracle import hadamard as OH
 from oracle import linear as OL
 from tests.gpu_common import TOL, gpu_encode, host_bytes, require_gpu, to_device_x
 
@@ -250,3 +251,55 @@ def test_weight_moments_match_oracle():
         x = w.astype(np.float64)
         assert abs(got[0] - x.mean()) <= 1e-12 * max(1.0, abs(x.mean()))
         assert abs(got[1] - oracle.variance_fp64(w)) <= 1e-10 * max(oracle.variance_fp64(w), 1e-30)
+
+
+def _row_factors(kind, m):
+    """Power-of-two factors per activation row: one for every row, or a spread."""
+    if kind == "mixed":
+        return np.array([2.0 ** ((7 * i) % 81 - 40) for i in range(m)], dtype=np.float64)
+    return np.full(m, 2.0 ** kind)
+
+
+@pytest.mark.parametrize("dtype,kind", [("f16", 12), ("f16", -16), ("f16", "mixed12"),
+                                        ("bf16", 12), ("bf16", -16), ("bf16", 40), ("bf16", -40),
+                                        ("bf16", "mixed"), ("f32", 12), ("f32", -16), ("f32", 40),
+                                        ("f32", -40), ("f32", "mixed")])
+@pytest.mark.parametrize("m", [1, 8, 64])
+def test_linear_activation_magnitudes(dtype, kind, m):
+    # Activations far outside N(0, 1): every path keeps 1e-3 whatever a row's
+    # magnitude -- the prefill path stores x_tilde in fp16 (normal range
+    # 2^-14 .. 65504) and scales each row by a power of two first.  The fp16
+    # cases stay inside fp16's own range (at most 2^12 times N(0, 1)).
+    torch = require_gpu()
+    enc, r = _oracle_codes_on_device(torch, 200, 1024, 2.0, 3, seed=31)
+    if kind == "mixed12":
+        f = np.array([2.0 ** ((5 * i) % 25 - 12) for i in range(m)])
+    else:
+        f = _row_factors(kind, m)
+    x32 = (synth.activations_f32(41, 0, m, 1024).astype(np.float64) * f[:, None]).astype(np.float32)
+    x_dev, x64 = to_device_x(x32, dtype, torch)
+    y = _run_linear(torch, enc, x_dev)
+    assert np.all(np.isfinite(y))
+    err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up))
+    assert np.all(err <= TOL), (dtype, kind, m, err.max())
+
+
+@pytest.mark.parametrize("had", ["none", "sylvester"])
+def test_linear_prefill_magnitudes_fp16_pair(had):
+    # Layouts without Had keep x_tilde as an fp16 pair hi + lo: both halves
+    # are scaled by the row's power of two.  Codes from the oracle encoder.
+    torch = require_gpu()
+    import paper_2510_03275_amd as P
+    n, k, m = 130, 768, 40
+    w = synth.weight_rows(77, 2, n, k, 0.02, True)
+    hd_o = OH.HAD_NONE if had == "none" else OH.HAD_SYLVESTER
+    r = oracle.encode(w, 2.0, 3, 256, hd_o)
+    L = P.sdq_layout_init(n, k, 2.0, 3)
+    P.sdq_layout_set_hadamard(L, P.SDQ_HAD_NONE if had == "none" else P.SDQ_HAD_SYLVESTER)
+    enc = P.Encoded(L, torch.from_numpy(LY.pack(r.codes, 3)).cuda(), torch.from_numpy(r.scales).cuda())
+    f = np.array([2.0 ** ((11 * i) % 61 - 30) for i in range(m)])
+    x32 = (synth.activations_f32(5, 0, m, k).astype(np.float64) * f[:, None]).astype(np.float32)
+    x_dev, x64 = to_device_x(x32, "bf16", torch)
+    y = _run_linear(torch, enc, x_dev)
+    err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up, hd_o))
+    assert np.all(err <= TOL), err.max()
