@@ -730,7 +730,8 @@ def traffic_probe(torch, P, synth, SG) -> None:
     """A short eager run for hardware-counter passes: one 256 MiB device copy
     of known size (to scale FETCH_SIZE / WRITE_SIZE), then the contraction
     launches of one token step through the LLaMA-70B stack (m = 1, expansions
-    once before), the LLaMA-7B down_proj GEMV and the LLaMA-70B prefill GEMMs.
+    once before), the same at m = 8, the LLaMA-7B down_proj GEMV and the
+    LLaMA-70B prefill GEMMs.
     Prints what it ran and the code bytes of the stack's launches."""
     nbytes = 256 << 20
     a = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
@@ -747,6 +748,13 @@ def traffic_probe(torch, P, synth, SG) -> None:
         fn()
     torch.cuda.synchronize()
     print(f"stack m=1 contraction: {len(fns)} launches, code bytes {run.code_bytes}", flush=True)
+    del run, fns, ws
+    run = StackRun(torch, P, SG, encs, layers, 8, wl.seed)
+    fns, ws = run.contraction_fns()
+    for fn in fns:
+        fn()
+    torch.cuda.synchronize()
+    print(f"stack m=8 contraction: {len(fns)} launches, code bytes {run.code_bytes}", flush=True)
     del run, fns, ws, encs
     torch.cuda.empty_cache()
     for wl_i, lin_i, m, xdt, label in ((2, 0, 1, torch.float16, "down_proj 4096x11008 m=1"),

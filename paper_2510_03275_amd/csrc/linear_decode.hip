@@ -42,6 +42,7 @@ constexpr int kExpThreads = 256;
 constexpr int kMaxDecodeRows = 16;  // activation rows of the decode path
 constexpr int kGemvWaves = 4;
 constexpr int kGroupsPerChunk = 32; // 128 bits / 4
+constexpr int64_t kExpRowPairs = 1024; // one-row expansion: two blocks per workgroup from here
 
 __device__ inline float load_x(const void* x, sdq_dtype xt, int64_t idx) {
   if (xt == SDQ_F16) return __half2float(static_cast<const __half*>(x)[idx]);
@@ -126,6 +127,73 @@ __global__ __launch_bounds__(kExpThreads) void expand_decode_kernel(
     if (oo < m_up)
       xt_out[static_cast<int64_t>(i) * k_up_pad + b * m_up + oo] =
           (red[0][i][l] + red[1][i][l]) + (red[2][i][l] + red[3][i][l]);
+  }
+}
+
+// One activation row: one workgroup per 64 output samples and NBW (1 or 2)
+// consecutive blocks.  The 64 columns of E are loaded once into registers
+// (wave w: t in its quarter, as above) and serve every block of the
+// workgroup, and the x of all its blocks is staged in LDS by one round of
+// loads issued together, so E crosses the caches once per NBW blocks instead
+// of once per block.  Same sums in the same order as expand_decode_kernel.
+template <int B, int NBW>
+__global__ __launch_bounds__(kExpThreads) void expand_decode_row_kernel(
+    const void* __restrict__ x, sdq_dtype xt, int nb, int m_up, int m_pad, int64_t k_up, int64_t k_up_pad,
+    const float4* __restrict__ edec, float* __restrict__ xt_out, LinearSet zero) {
+  constexpr int TQ = B / 4;                 // t values per wave
+  constexpr int XPT = (NBW * B + kExpThreads - 1) / kExpThreads;  // x values staged per thread
+  __shared__ float xs[NBW][B];
+  __shared__ float red[4][NBW][64];
+  const int tid = threadIdx.x;
+  const int lane = tid % 64;
+  const int w = tid / 64;
+  const int o = blockIdx.x * 64 + lane;     // < m_pad: the table is zero there
+  const int b0 = blockIdx.y * NBW;
+  const int nbl = min(NBW, nb - b0);
+  float4 e[TQ / 4];
+  const float4* ep = edec + static_cast<int64_t>(w * (TQ / 4)) * m_pad + o;
+#pragma unroll
+  for (int q = 0; q < TQ / 4; ++q) e[q] = ep[static_cast<int64_t>(q) * m_pad];
+  float xv[XPT];
+#pragma unroll
+  for (int j = 0; j < XPT; ++j) {
+    const int idx = tid + kExpThreads * j;
+    xv[j] = idx < NBW * B && idx / B < nbl ? load_x(x, xt, static_cast<int64_t>(b0) * B + idx) : 0.0f;
+  }
+#pragma unroll
+  for (int j = 0; j < XPT; ++j) {
+    const int idx = tid + kExpThreads * j;
+    if (idx < NBW * B) xs[idx / B][idx % B] = xv[j];
+  }
+  // Side duties: zero y for a split-K GEMV, zero x_tilde's padding.
+  const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t n_wg = static_cast<int64_t>(gridDim.x) * gridDim.y;
+  zero_outputs(zero, 1, wg, n_wg, tid);
+  if (wg == 0)
+    for (int64_t i = k_up + tid; i < k_up_pad; i += kExpThreads) xt_out[i] = 0.0f;
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < NBW; ++j) {
+    if (j >= nbl) break;
+    const float4* xr = reinterpret_cast<const float4*>(&xs[j][w * TQ]);
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+    for (int q = 0; q < TQ / 4; ++q) {
+      const float4 v = xr[q];
+      a0 += e[q].x * v.x;
+      a1 += e[q].y * v.y;
+      a2 += e[q].z * v.z;
+      a3 += e[q].w * v.w;
+    }
+    red[w][j][lane] = (a0 + a1) + (a2 + a3);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < nbl * 64; idx += kExpThreads) {
+    const int j = idx / 64, l = idx % 64;
+    const int oo = blockIdx.x * 64 + l;
+    if (oo < m_up)
+      xt_out[static_cast<int64_t>(b0 + j) * m_up + oo] =
+          (red[0][j][l] + red[1][j][l]) + (red[2][j][l] + red[3][j][l]);
   }
 }
 
@@ -976,6 +1044,36 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
       }
     }
 #undef SDQ_PLANES
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_error(e, "decode expansion launch");
+    return SDQ_OK;
+  }
+  if (m == 1) {
+    // Blocks per workgroup: two once the launch has kExpRowPairs (64-sample
+    // tile, block) pairs or more, else one.  Measured on MI355X at m = 1:
+    // k = 28672 at OSR 3 (1344 pairs) 5.4 -> 4.4 us with two, no gain at
+    // k = 8192 (384 pairs) or k = 28672 at OSR 1.5 (672 pairs), and slower
+    // with four or eight (their blocks' products run one after another).
+    // SDQ_EXP_NBW=1 or 2 overrides (a tuning aid).
+    static const char* env = std::getenv("SDQ_EXP_NBW");
+    const int64_t tiles = T->m_pad / 64;
+    int nbw = tiles * L->nb >= kExpRowPairs ? 2 : 1;
+    if (env && (std::atoi(env) == 1 || std::atoi(env) == 2)) nbw = std::atoi(env);
+    const dim3 rgrid(static_cast<unsigned>(tiles), static_cast<unsigned>((L->nb + nbw - 1) / nbw));
+#define SDQ_ROW(BB, NBW_)                                                                       \
+  expand_decode_row_kernel<BB, NBW_><<<rgrid, dim3(kExpThreads), 0, stream>>>(                  \
+      x, xt, static_cast<int>(L->nb), L->m_up, T->m_pad, L->k_up, k_up_pad,                      \
+      reinterpret_cast<const float4*>(T->edec), w.xt, z)
+#define SDQ_ROW_B(BB)                                                                           \
+  if (nbw == 2) SDQ_ROW(BB, 2);                                                                 \
+  else SDQ_ROW(BB, 1)
+    switch (B) {
+      case 64: SDQ_ROW_B(64); break;
+      case 128: SDQ_ROW_B(128); break;
+      default: SDQ_ROW_B(256); break;
+    }
+#undef SDQ_ROW_B
+#undef SDQ_ROW
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_error(e, "decode expansion launch");
     return SDQ_OK;
