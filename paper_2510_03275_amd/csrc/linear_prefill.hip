@@ -133,7 +133,6 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     const _Float16* __restrict__ xt, const float* __restrict__ row_inv, LinearSet S, int64_t m,
     int64_t n_chunks, int64_t k_up_pad, int64_t m_tiles, int64_t n_tiles, int accumulate) {
   __shared__ __attribute__((aligned(1024))) _Float16 As[kABufs][kTileHalves];
-  __shared__ float rinv[kBM];
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
@@ -185,8 +184,6 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
                                        (lds_void_ptr)(dst_ + j * 8 * kBK), 16, 0, 0);            \
   } while (0)
 
-  static_assert(kBM == 256, "one row factor per thread");
-  rinv[tid] = m0 + tid < m ? row_inv[m0 + tid] : 1.0f;
   const int it1 = n_iter > 1 ? 1 : 0;
   SDQ_FILL_A(0, 0);
   SDQ_FILL_A(1, it1);
@@ -241,6 +238,15 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
   }
 #undef SDQ_FILL_A
 
+  // The row factors of the tile, staged in the first buffer of the ring once
+  // every copy has landed and every fragment read is done (a separate LDS
+  // array would make the compiler wait for all copies in every step).
+  static_assert(kBM == 256, "one row factor per thread");
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  float* rinv = reinterpret_cast<float*>(&As[0][0]);
+  rinv[tid] = m0 + tid < m ? row_inv[m0 + tid] : 1.0f;
+  __syncthreads();
 #pragma unroll
   for (int c = 0; c < 2; ++c) {
     const int64_t col = cols[c];
