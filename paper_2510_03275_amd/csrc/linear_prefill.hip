@@ -15,6 +15,7 @@
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
+#include <type_traits>
 #include <cstdlib>
 #include <hip/hip_fp16.h>
 #include <hip/hip_bf16.h>
@@ -114,11 +115,12 @@ __device__ inline uint4 load_codes(const uint4* __restrict__ codes, int64_t col,
 // of two row tiles by many column tiles and its L2 fetches each x_tilde and
 // code slice once for all of them.
 constexpr int kXcds = 8;
-__device__ inline void prefill_tile(int64_t id, int64_t total, int64_t m_tiles, int64_t n_tiles,
-                                    int64_t* mt, int64_t* nt) {
+__device__ inline int64_t xcd_index(int64_t id, int64_t total) {
   const int64_t xcd = id % kXcds, j = id / kXcds;
   const int64_t per = total / kXcds, rem = total % kXcds;
-  const int64_t t = xcd * per + (xcd < rem ? xcd : rem) + j;
+  return xcd * per + (xcd < rem ? xcd : rem) + j;
+}
+__device__ inline void prefill_tile(int64_t t, int64_t m_tiles, int64_t n_tiles, int64_t* mt, int64_t* nt) {
   const int64_t pair_tiles = 2 * n_tiles;          // tiles of one pair of row tiles
   const int64_t p = t / pair_tiles, r = t % pair_tiles;
   const int64_t rows_in_pair = min<int64_t>(2, m_tiles - 2 * p);
@@ -128,17 +130,24 @@ __device__ inline void prefill_tile(int64_t id, int64_t total, int64_t m_tiles, 
 
 // row_inv: 1 / p_i of every activation row, the powers of two the expansion
 // scaled the rows by; the epilogue multiplies them back out (exact).
-template <int LEVELS>
+// A launch covers the tiles t_base .. t_base + t_count - 1 of that order: NC =
+// 2 a whole 256 x 256 tile per workgroup, NC = 1 half of one (256 activation
+// rows x 128 weight rows, each wave 32 of them), so that a last, partly
+// filled wave of whole tiles can run as one full wave of half tiles.
+template <int LEVELS, int NC>
 __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     const _Float16* __restrict__ xt, const float* __restrict__ row_inv, LinearSet S, int64_t m,
-    int64_t n_chunks, int64_t k_up_pad, int64_t m_tiles, int64_t n_tiles, int accumulate) {
+    int64_t n_chunks, int64_t k_up_pad, int64_t m_tiles, int64_t n_tiles, int64_t t_base, int64_t t_count,
+    int accumulate) {
   __shared__ __attribute__((aligned(1024))) _Float16 As[kABufs][kTileHalves];
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
   const int half = lane / 32;
   int64_t mt, nt;
-  prefill_tile(blockIdx.x, static_cast<int64_t>(gridDim.x), m_tiles, n_tiles, &mt, &nt);
+  const int64_t u = xcd_index(blockIdx.x, static_cast<int64_t>(gridDim.x));
+  const int nh = NC == 2 ? 0 : static_cast<int>(u % 2);   // which half of the tile's weight rows
+  prefill_tile(t_base + (NC == 2 ? u : u / 2), m_tiles, n_tiles, &mt, &nt);
   const int lin = [&] {                           // units: column tiles of kBN weight rows
     int j = 0;
 #pragma unroll
@@ -152,15 +161,17 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
   const float* __restrict__ scales = S.scales[lin];
   float* __restrict__ y = S.y[lin];
   const int64_t m0 = mt * kBM;
-  const int64_t n0 = (nt - S.first[lin]) * kBN + wave * 64;
-  const int64_t cols[2] = {n0 + lane % 32, n0 + 32 + lane % 32};
+  const int64_t n0 = (nt - S.first[lin]) * kBN + (NC == 2 ? wave * 64 : nh * 128 + wave * 32);
+  int64_t cols[NC];
+#pragma unroll
+  for (int c = 0; c < NC; ++c) cols[c] = n0 + 32 * c + lane % 32;
   const int n_iter = static_cast<int>(k_up_pad / kBK);
 
-  floatx16 acc[8][2];
+  floatx16 acc[8][NC];
 #pragma unroll
   for (int r = 0; r < 8; ++r)
 #pragma unroll
-    for (int c = 0; c < 2; ++c)
+    for (int c = 0; c < NC; ++c)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[r][c][v] = 0.0f;
 
@@ -188,9 +199,9 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
   SDQ_FILL_A(0, 0);
   SDQ_FILL_A(1, it1);
   uint4 c0 = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, 0);
-  uint4 c1 = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, 0);
+  uint4 c1 = load_codes<LEVELS>(codes, cols[NC - 1], n_pad, n_chunks, 0);
   uint4 d0 = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, it1);   // the next step's
-  uint4 d1 = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, it1);
+  uint4 d1 = load_codes<LEVELS>(codes, cols[NC - 1], n_pad, n_chunks, it1);
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
 
@@ -205,19 +216,20 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     const int n2 = it + 2 < n_iter ? it + 2 : n_iter - 1;
     SDQ_FILL_A(cur ^ 2, n2);
     const uint4 e0 = load_codes<LEVELS>(codes, cols[0], n_pad, n_chunks, n2);
-    const uint4 e1 = load_codes<LEVELS>(codes, cols[1], n_pad, n_chunks, n2);
+    const uint4 e1 = NC == 2 ? load_codes<LEVELS>(codes, cols[NC - 1], n_pad, n_chunks, n2) : e0;
     const _Float16* abuf = As[cur];
 #pragma unroll
     for (int ks = 0; ks < kBK / 16; ++ks) {
-      const half8 b0 = expand8<LEVELS>(codes_at<LEVELS>(c0, ks, half));
-      const half8 b1 = expand8<LEVELS>(codes_at<LEVELS>(c1, ks, half));
+      half8 b[NC];
+      b[0] = expand8<LEVELS>(codes_at<LEVELS>(c0, ks, half));
+      if (NC == 2) b[NC - 1] = expand8<LEVELS>(codes_at<LEVELS>(c1, ks, half));
       const int g = 2 * ks + half;
 #pragma unroll
       for (int rt = 0; rt < 8; ++rt) {
         const int r = rt * 32 + fr;
         const half8 afrag = *reinterpret_cast<const half8*>(abuf + r * kBK + 8 * (g ^ swz(r)));
-        acc[rt][0] = mfma32(afrag, b0, acc[rt][0]);
-        acc[rt][1] = mfma32(afrag, b1, acc[rt][1]);
+#pragma unroll
+        for (int c = 0; c < NC; ++c) acc[rt][c] = mfma32(afrag, b[c], acc[rt][c]);
       }
     }
     c0 = d0;
@@ -248,7 +260,7 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
   rinv[tid] = m0 + tid < m ? row_inv[m0 + tid] : 1.0f;
   __syncthreads();
 #pragma unroll
-  for (int c = 0; c < 2; ++c) {
+  for (int c = 0; c < NC; ++c) {
     const int64_t col = cols[c];
     if (col >= n) continue;
     const float s = scales[col];
@@ -264,6 +276,19 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
         }
       }
   }
+}
+
+// Compute units of the current device (cached per device).
+int64_t compute_units() {
+  static int64_t cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cached[dev] = v;
+  }
+  return cached[dev];
 }
 
 }  // namespace
@@ -290,22 +315,42 @@ sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, 
   // chunks of at most 2^31 elements.
   const int64_t rows_max = std::max<int64_t>(kBM, ((int64_t{1} << 31) / k_up_pad) / kBM * kBM);
   const int passes = prefill_split(L) ? 2 : 1;   // x_tilde hi, then lo added on
+  const int64_t cus = compute_units();
   for (int pass = 0; pass < passes; ++pass) {
     const _Float16* xbuf = reinterpret_cast<const _Float16*>(static_cast<const char*>(ws) + pass * plane);
     const int acc = accumulate || pass > 0 ? 1 : 0;
     for (int64_t r0 = 0; r0 < m; r0 += rows_max) {
       const int64_t mm = std::min(rows_max, m - r0);
       const int64_t m_tiles = (mm + kBM - 1) / kBM;
-      const dim3 ggrid(static_cast<unsigned>(m_tiles * n_tiles));
       const _Float16* xc = xbuf + r0 * k_up_pad;
       LinearSet Sc = S;
       for (int j = 0; j < S.count; ++j) Sc.y[j] = S.y[j] + r0 * S.n[j];
-      if (L->levels == 2)
-        gemm_prefill_kernel<2><<<ggrid, dim3(256), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks, k_up_pad,
-                                                                m_tiles, n_tiles, acc);
-      else
-        gemm_prefill_kernel<3><<<ggrid, dim3(256), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks, k_up_pad,
-                                                                m_tiles, n_tiles, acc);
+      // One workgroup per CU: whole tiles in full waves, and a last wave that
+      // would be at most half full as twice as many half tiles (same time per
+      // wave of work, no idle half).
+      const int64_t tiles = m_tiles * n_tiles;
+      const int64_t tail = tiles % cus;
+      const int64_t t_half = tail > 0 && 2 * tail <= cus ? tail : 0;
+      const int64_t t_whole = tiles - t_half;
+      auto launch = [&](auto lv, auto nc, int64_t t_base, int64_t t_count) {
+        constexpr int LV = decltype(lv)::value, NC = decltype(nc)::value;
+        if (t_count <= 0) return;
+        const dim3 ggrid(static_cast<unsigned>(t_count * (NC == 2 ? 1 : 2)));
+        gemm_prefill_kernel<LV, NC><<<ggrid, dim3(256), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks,
+                                                                   k_up_pad, m_tiles, n_tiles, t_base, t_count,
+                                                                   acc);
+      };
+      using L2_ = std::integral_constant<int, 2>;
+      using L3_ = std::integral_constant<int, 3>;
+      using W_ = std::integral_constant<int, 2>;
+      using H_ = std::integral_constant<int, 1>;
+      if (L->levels == 2) {
+        launch(L2_{}, W_{}, 0, t_whole);
+        launch(L2_{}, H_{}, t_whole, t_half);
+      } else {
+        launch(L3_{}, W_{}, 0, t_whole);
+        launch(L3_{}, H_{}, t_whole, t_half);
+      }
     }
   }
   hipError_t e = hipGetLastError();

@@ -303,3 +303,16 @@ def test_linear_prefill_magnitudes_fp16_pair(had):
     y = _run_linear(torch, enc, x_dev)
     err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up, hd_o))
     assert np.all(err <= TOL), err.max()
+
+
+def test_linear_prefill_whole_and_half_tiles():
+    # 2 x 160 GEMM tiles of 256 x 256: on a 256-CU part the first 256 run as
+    # whole tiles and the last 64 as 128 half tiles; rows 300..511 of the
+    # second row tile are past m.  All weight rows are checked.
+    torch = require_gpu()
+    n, k, m = 40960, 256, 300
+    enc, r = _oracle_codes_on_device(torch, n, k, 2.0, 3, seed=404)
+    x_dev, x64 = to_device_x(synth.activations_f32(404, 0, m, k), "bf16", torch)
+    y = _run_linear(torch, enc, x_dev)
+    err = OL.rel_err_rows(y, OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up))
+    assert np.all(err <= TOL), err.max()
