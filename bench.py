@@ -62,8 +62,10 @@ POOL_MAX = 16                    # oracle workers: the host share of one GPU
 # were taken with: a source whose hash differs reports traffic null.
 TRAFFIC_FETCH_SCALE = 1.999749
 TRAFFIC_WRITE_SCALE = 1.000000
-TRAFFIC_SOURCES = {}
-TRAFFIC_KIB = {}   # kernel family -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB) per launch
+TRAFFIC_SOURCES = {"linear_decode.hip": "10a94cfa08e43212e979348f9d96f9c0234ddea3514588c75bbc81b8ecc4883c"}
+# kernel family -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB) per launch: the mean
+# over the 325 contraction launches of one m = 1 token step through the stack.
+TRAFFIC_KIB = {"gemv_lut_kernel<1,3,*>": ("linear_decode.hip", 64921.1, 6897.9)}
 
 
 def traffic_bytes(kernel: str):
@@ -683,8 +685,8 @@ def bench_sweep(torch, P, synth, SG):
 # The oracle beside it.
 # ---------------------------------------------------------------------------
 
-def cpu_baseline(ctx, synth, wl, osr, layer: int = 40, rows_per_kind: int = 64, chunk: int = 8):
-    """The oracle on 64 rows of each of the seven linear kinds of one stack
+def cpu_baseline(ctx, synth, wl, osr, layer: int = 40, rows_per_kind: int = 512, chunk: int = 32):
+    """The oracle on 512 rows of each of the seven linear kinds of one stack
     layer (at their MultiOSR OSRs): the encoder over a process pool, then the
     fp64 linear (Algorithm 1's reconstruction, one activation row) over the
     same pool.  value = code bytes of the sampled rows / linear wall time."""
