@@ -36,9 +36,11 @@ __device__ inline floatx16 mfma32(const half8& a, const half8& b, const floatx16
 
 // ---------------------------------------------------------------------------
 // GEMM.  Workgroup tile 256 (activation rows) x 256 (weight rows), k step 64.
-// Four waves side by side along the weight rows, each owning a 256 x 64 tile
-// (8 x 2 accumulator tiles of 32 x 32).  The x_tilde tile is double-buffered
-// in LDS and filled straight from global memory (global_load_lds_dwordx4, no
+// Eight waves, 2 (activation rows) x 4 (weight rows), each owning a 128 x 64
+// tile (4 x 2 accumulator tiles of 32 x 32), two waves per SIMD; or four
+// waves side by side along the weight rows, each owning 256 x 64.  The
+// x_tilde tile is double-buffered in LDS and filled straight from global
+// memory (global_load_lds_dwordx4, no
 // staging registers); its 16-byte groups are XOR-swizzled by row so that the
 // fragment reads of 16 consecutive rows fall on distinct banks.  A ring of
 // four buffers (128 KB): the copies for step k + 2 are issued while step k
@@ -134,15 +136,22 @@ __device__ inline void prefill_tile(int64_t t, int64_t m_tiles, int64_t n_tiles,
 // 2 a whole 256 x 256 tile per workgroup, NC = 1 half of one (256 activation
 // rows x 128 weight rows, each wave 32 of them), so that a last, partly
 // filled wave of whole tiles can run as one full wave of half tiles.
-template <int LEVELS, int NC>
-__global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
+// W waves: 4 (each 256 activation rows x 64 weight rows, 256 accumulator
+// registers, one wave per SIMD) or 8 (each 128 x 64, two waves per SIMD).
+template <int LEVELS, int NC, int W>
+__global__ __launch_bounds__(64 * W, 1) void gemm_prefill_kernel(
     const _Float16* __restrict__ xt, const float* __restrict__ row_inv, LinearSet S, int64_t m,
     int64_t n_chunks, int64_t k_up_pad, int64_t m_tiles, int64_t n_tiles, int64_t t_base, int64_t t_count,
     int accumulate) {
   __shared__ __attribute__((aligned(1024))) _Float16 As[kABufs][kTileHalves];
+  constexpr int RPW = kBM / (W / 4);          // activation rows per wave
+  constexpr int RT = RPW / 32;                 // 32-row MFMA tiles per wave
+  constexpr int FC = kBM / W / 8;              // tile-fill copies per wave and step (8 rows each)
   const int tid = threadIdx.x;
   const int lane = tid % 64;
   const int wave = tid / 64;
+  const int wq = wave % 4;                     // column quarter
+  const int row0 = (wave / 4) * RPW;           // first activation row of the wave in the tile
   const int half = lane / 32;
   int64_t mt, nt;
   const int64_t u = xcd_index(blockIdx.x, static_cast<int64_t>(gridDim.x));
@@ -161,15 +170,15 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
   const float* __restrict__ scales = S.scales[lin];
   float* __restrict__ y = S.y[lin];
   const int64_t m0 = mt * kBM;
-  const int64_t n0 = (nt - S.first[lin]) * kBN + (NC == 2 ? wave * 64 : nh * 128 + wave * 32);
+  const int64_t n0 = (nt - S.first[lin]) * kBN + (NC == 2 ? wq * 64 : nh * 128 + wq * 32);
   int64_t cols[NC];
 #pragma unroll
   for (int c = 0; c < NC; ++c) cols[c] = n0 + 32 * c + lane % 32;
   const int n_iter = static_cast<int>(k_up_pad / kBK);
 
-  floatx16 acc[8][NC];
+  floatx16 acc[RT][NC];
 #pragma unroll
-  for (int r = 0; r < 8; ++r)
+  for (int r = 0; r < RT; ++r)
 #pragma unroll
     for (int c = 0; c < NC; ++c)
 #pragma unroll
@@ -179,18 +188,18 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
   // rows each); lane l of copy j writes slot l % 8 of row 64 w + 8 j + l / 8,
   // which holds 16-byte group (l % 8) ^ swz(row).  Rows past m read row m - 1:
   // they only feed output rows that are not stored.
-  uint32_t a_off[8];                        // element offsets (m * k_up_pad < 2^31)
+  uint32_t a_off[FC];                       // element offsets (m * k_up_pad < 2^31)
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const int r = wave * 64 + 8 * j + lane / 8;
+  for (int j = 0; j < FC; ++j) {
+    const int r = wave * (kBM / W) + 8 * j + lane / 8;
     const int64_t row = m0 + r;
     a_off[j] = static_cast<uint32_t>((row < m ? row : m - 1) * k_up_pad + 8 * ((lane % 8) ^ swz(r)));
   }
 #define SDQ_FILL_A(BUF, IT)                                                                      \
   do {                                                                                           \
     const _Float16* src_ = xt + static_cast<uint32_t>((IT) * kBK);                               \
-    _Float16* dst_ = &As[(BUF)][wave * 64 * kBK];                                                \
-    _Pragma("unroll") for (int j = 0; j < 8; ++j)                                                \
+    _Float16* dst_ = &As[(BUF)][wave * (kBM / W) * kBK];                                         \
+    _Pragma("unroll") for (int j = 0; j < FC; ++j)                                               \
       __builtin_amdgcn_global_load_lds((gbl_void_ptr)(src_ + a_off[j]),                          \
                                        (lds_void_ptr)(dst_ + j * 8 * kBK), 16, 0, 0);            \
   } while (0)
@@ -225,8 +234,8 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
       if (NC == 2) b[NC - 1] = expand8<LEVELS>(codes_at<LEVELS>(c1, ks, half));
       const int g = 2 * ks + half;
 #pragma unroll
-      for (int rt = 0; rt < 8; ++rt) {
-        const int r = rt * 32 + fr;
+      for (int rt = 0; rt < RT; ++rt) {
+        const int r = row0 + rt * 32 + fr;
         const half8 afrag = *reinterpret_cast<const half8*>(abuf + r * kBK + 8 * (g ^ swz(r)));
 #pragma unroll
         for (int c = 0; c < NC; ++c) acc[rt][c] = mfma32(afrag, b[c], acc[rt][c]);
@@ -243,7 +252,7 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     // waits for every outstanding LDS copy.  The empty asm statements keep LDS
     // accesses from moving across it; every fragment read of the buffer that
     // is refilled next has returned before its MFMAs issued.
-    __builtin_amdgcn_s_waitcnt(0xF7A);
+    __builtin_amdgcn_s_waitcnt(W == 4 ? 0xF7A : 0xF70 | (FC + 2));
     asm volatile("" ::: "memory");
     __builtin_amdgcn_s_barrier();
     asm volatile("" ::: "memory");
@@ -257,7 +266,7 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
   __builtin_amdgcn_s_waitcnt(0);
   __syncthreads();
   float* rinv = reinterpret_cast<float*>(&As[0][0]);
-  rinv[tid] = m0 + tid < m ? row_inv[m0 + tid] : 1.0f;
+  if (tid < kBM) rinv[tid] = m0 + tid < m ? row_inv[m0 + tid] : 1.0f;
   __syncthreads();
 #pragma unroll
   for (int c = 0; c < NC; ++c) {
@@ -265,10 +274,10 @@ __global__ __launch_bounds__(256, 1) void gemm_prefill_kernel(
     if (col >= n) continue;
     const float s = scales[col];
 #pragma unroll
-    for (int r = 0; r < 8; ++r)
+    for (int r = 0; r < RT; ++r)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const int lr = r * 32 + 8 * (v / 4) + 4 * half + (v % 4);
+        const int lr = row0 + r * 32 + 8 * (v / 4) + 4 * half + (v % 4);
         const int64_t row = m0 + lr;
         if (row < m) {
           const float val = acc[r][c][v] * s * rinv[lr];
@@ -316,6 +325,12 @@ sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, 
   const int64_t rows_max = std::max<int64_t>(kBM, ((int64_t{1} << 31) / k_up_pad) / kBM * kBM);
   const int passes = prefill_split(L) ? 2 : 1;   // x_tilde hi, then lo added on
   const int64_t cus = compute_units();
+  // Eight waves (two per SIMD, so one wave's LDS and memory waits overlap the
+  // other's MFMAs) by default: measured 431 against 437-445 us on 8192x8192 and
+  // 1489 against 1540-1548 us on 28672x8192 at m = 2048, equal on 8192x28672.
+  // SDQ_PF_WAVES=4 selects one wave per SIMD (a tuning aid).
+  static const char* env_w = std::getenv("SDQ_PF_WAVES");
+  const int waves = env_w && std::atoi(env_w) == 4 ? 4 : 8;
   for (int pass = 0; pass < passes; ++pass) {
     const _Float16* xbuf = reinterpret_cast<const _Float16*>(static_cast<const char*>(ws) + pass * plane);
     const int acc = accumulate || pass > 0 ? 1 : 0;
@@ -336,9 +351,14 @@ sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, 
         constexpr int LV = decltype(lv)::value, NC = decltype(nc)::value;
         if (t_count <= 0) return;
         const dim3 ggrid(static_cast<unsigned>(t_count * (NC == 2 ? 1 : 2)));
-        gemm_prefill_kernel<LV, NC><<<ggrid, dim3(256), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks,
-                                                                   k_up_pad, m_tiles, n_tiles, t_base, t_count,
-                                                                   acc);
+        if (waves == 8)
+          gemm_prefill_kernel<LV, NC, 8><<<ggrid, dim3(512), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks,
+                                                                        k_up_pad, m_tiles, n_tiles, t_base,
+                                                                        t_count, acc);
+        else
+          gemm_prefill_kernel<LV, NC, 4><<<ggrid, dim3(256), 0, stream>>>(xc, row_inv + r0, Sc, mm, L->n_chunks,
+                                                                        k_up_pad, m_tiles, n_tiles, t_base,
+                                                                        t_count, acc);
       };
       using L2_ = std::integral_constant<int, 2>;
       using L3_ = std::integral_constant<int, 3>;
