@@ -21,8 +21,10 @@
 // All of it is dense fp64 linear algebra: one GEMM on the fp64 matrix cores
 // with general strides (64 x 64 tile per workgroup, 16-deep k slices through
 // LDS) serves the Hessian, the panel solves, the trailing updates, the
-// triangular inverses and the block corrections; a 64 x 64 Cholesky-and-
-// inverse kernel works on diagonal blocks in LDS.
+// triangular inverses and the block corrections.  The 64 x 64 diagonal
+// blocks of the Cholesky factor are factored and inverted in registers by one
+// workgroup, fused into the trailing update that produces them; another small
+// kernel inverts given triangular 64-blocks in LDS.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -35,6 +37,133 @@ namespace {
 constexpr int kT = 64;     // factorisation panel / GEMM tile
 constexpr int kTK = 16;    // GEMM k step
 constexpr int kStage = kT * kTK / 256;   // operand elements staged per thread and k step
+
+// Cholesky factor and inverse of one 64 x 64 block in place: the lower part
+// of A (row stride lda, unit column stride) is read, A = L L^T is written back
+// with the upper part zeroed and X = L^-1 (lower) is written.  Symmetric
+// elimination without square roots: step j takes column j of the reduced
+// matrix (pivot d_j), forms the multipliers m_i = c_i / d_j of the rows below
+// it and subtracts m_i times row j from row i, in the reduced matrix and in a
+// copy of the identity, which becomes L'^-1 for the unit lower factor of
+// A = L' D L'^T.  Then column j of L is c / sqrt(d_j) and L^-1 = D^-1/2 L'^-1
+// (row i divided by sqrt(d_i)).  Thread t keeps a 4 x 4 tile of the reduced
+// matrix and of the inverse in registers (rows 4 (t / 16) .., columns
+// 4 (t % 16) ..; a finished column stays in place).  Per step, the owners of
+// the next column and of the next row of the inverse update those first and
+// publish them in a two-slot LDS ring, with the next-but-one diagonal entry;
+// from that entry every thread forms the next pivot and its reciprocal while
+// the rest of the tile is updated, so only a multiply and an FMA lie between
+// two barriers on the column-to-column path (one barrier per column).  Upper
+// entries of the tiles are updated too and never read.  A pivot that is not
+// positive sets *info and is taken as 1.  Needs 256 threads and 322 doubles of
+// LDS at lds.
+__device__ __forceinline__ void chol64_tile(double* A, int64_t lda, double* X, int64_t ldx, int* info,
+                                            double* lds) {
+  double(*ct)[kT] = reinterpret_cast<double(*)[kT]>(lds);            // column j in slot j % 2
+  double(*xr)[kT] = reinterpret_cast<double(*)[kT]>(lds + 2 * kT);   // row j of L'^-1, slot j % 2
+  double* ev = lds + 4 * kT;                                          // diagonal entry j in slot j % 2
+  double* dv = lds + 4 * kT + 2;                                      // pivots
+  const int tid = threadIdx.x;
+  const int ti = tid / 16, tk = tid % 16;
+  const int i0 = 4 * ti, k0 = 4 * tk;
+  double a[4][4], x[4][4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      a[r][c] = k0 + c <= i0 + r ? A[(i0 + r) * lda + k0 + c] : 0.0;
+      x[r][c] = i0 + r == k0 + c ? 1.0 : 0.0;
+    }
+  }
+  if (tk == 0) {
+#pragma unroll
+    for (int r = 0; r < 4; ++r) ct[0][i0 + r] = a[r][0];
+  }
+  if (ti == 0) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) xr[0][k0 + c] = x[0][c];
+  }
+  if (tid == 0) ev[1] = a[1][1];
+  __syncthreads();
+  double d = ct[0][0];
+  if (!(d > 0.0)) {
+    if (tid == 0) info[0] = 1;
+    d = 1.0;
+  }
+  if (tid == 0) dv[0] = d;
+  double rd = 1.0 / d;
+  for (int jb = 0; jb < kT; jb += 4) {
+#pragma unroll
+    for (int jj = 0; jj < 4; ++jj) {
+      const int j = jb + jj, sl = jj & 1, sn = sl ^ 1;
+      const int jn = j + 1, cn = (jj + 1) & 3, c2 = (jj + 2) & 3;
+      // All of the step's LDS reads first, unconditionally (a select after
+      // the load keeps them out of branches).
+      const double2 cr0 = *reinterpret_cast<const double2*>(&ct[sl][i0]);
+      const double2 cr1 = *reinterpret_cast<const double2*>(&ct[sl][i0 + 2]);
+      const double2 cc0 = *reinterpret_cast<const double2*>(&ct[sl][k0]);
+      const double2 cc1 = *reinterpret_cast<const double2*>(&ct[sl][k0 + 2]);
+      const double2 xx0 = *reinterpret_cast<const double2*>(&xr[sl][k0]);
+      const double2 xx1 = *reinterpret_cast<const double2*>(&xr[sl][k0 + 2]);
+      const double cj = ct[sl][jn < kT ? jn : j];
+      const double en = ev[sn];
+      const double crv[4] = {cr0.x, cr0.y, cr1.x, cr1.y};
+      const double ccv[4] = {cc0.x, cc0.y, cc1.x, cc1.y};
+      double m[4], ck[4];
+      const double xk[4] = {xx0.x, xx0.y, xx1.x, xx1.y};
+#pragma unroll
+      for (int r = 0; r < 4; ++r) m[r] = crv[r] * (i0 + r > j ? rd : 0.0);   // (entries above j are finite)
+#pragma unroll
+      for (int c = 0; c < 4; ++c) ck[c] = k0 + c > j ? ccv[c] : 0.0;
+      if (jn < kT) {
+        if (tk == jn / 4) {
+#pragma unroll
+          for (int r = 0; r < 4; ++r) ct[sn][i0 + r] = a[r][cn] - m[r] * ck[cn];
+        }
+        if (ti == jn / 4) {
+#pragma unroll
+          for (int c = 0; c < 4; ++c) xr[sn][k0 + c] = x[cn][c] - m[cn] * xk[c];
+        }
+        if (jn + 1 < kT && ti == (jn + 1) / 4 && tk == (jn + 1) / 4) ev[sl] = a[c2][c2] - m[c2] * ck[c2];
+        // next pivot: entry (j + 1, j + 1) after this step's update
+        double dn = en - (cj * rd) * cj;
+        if (!(dn > 0.0)) {
+          if (tid == 0) info[0] = 1;
+          dn = 1.0;
+        }
+        if (tid == 0) dv[jn] = dn;
+        rd = 1.0 / dn;
+      }
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+#pragma unroll
+        for (int c = 0; c < 4; ++c) {
+          a[r][c] -= m[r] * ck[c];
+          x[r][c] -= m[r] * xk[c];
+        }
+      }
+      __syncthreads();
+    }
+  }
+  double* sq = ct[0];   // square roots of the pivots (the ring is free now)
+  if (tid < kT) sq[tid] = sqrt(dv[tid]);
+  __syncthreads();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+#pragma unroll
+    for (int c = 0; c < 4; ++c) {
+      const int i = i0 + r, k = k0 + c;
+      A[i * lda + k] = k < i ? a[r][c] / sq[k] : (k == i ? sq[i] : 0.0);
+      X[i * ldx + k] = k <= i ? x[r][c] / sq[i] : 0.0;
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void chol64_kernel(double* A, int64_t lda, double* X, int64_t ldx,
+                                                     int* info) {
+  __shared__ double lds[4 * kT + 2 + kT];
+  chol64_tile(A, lda, X, ldx, info, lds);
+}
 
 // C = beta C + alpha A B; element (i, p) of A at A[i * rsa + p * csa], likewise
 // B and C; blockIdx.z selects a batch (strides bsa, bsb, bsc).  lower_only = 1
@@ -54,11 +183,11 @@ constexpr int kStage = kT * kTK / 256;   // operand elements staged per thread a
 // B[l / 16][l % 16] and receives D[l / 16 + 4 v][l % 16] in item v.
 typedef double double4_t __attribute__((ext_vector_type(4)));
 
-template <typename TA, typename TB>
+template <typename TA, typename TB, bool kChol = false>
 __global__ __launch_bounds__(256) void gemm64_kernel(
     int64_t M, int64_t N, int64_t K, double alpha, const TA* A, int64_t rsa, int64_t csa,
     int64_t bsa, const TB* B, int64_t rsb, int64_t csb, int64_t bsb, double beta, double* C,
-    int64_t rsc, int64_t csc, int64_t bsc, int lower_only) {
+    int64_t rsc, int64_t csc, int64_t bsc, int lower_only, double* cx, int64_t ldx, int* info) {
   __shared__ double As[kTK][kT + 2];
   __shared__ double Bs[kTK][kT + 2];
   const int tid = threadIdx.x;
@@ -151,20 +280,24 @@ __global__ __launch_bounds__(256) void gemm64_kernel(
           }
         }
       }
+  if constexpr (kChol) {
+    // The first tile goes on to its Cholesky factor and inverse (the tile's
+    // stores above are visible to the whole workgroup after the barrier).
+    if (blockIdx.x == 0 && blockIdx.y == 0 && blockIdx.z == 0) {
+      __syncthreads();
+      chol64_tile(C, rsc, cx, ldx, info, &As[0][0]);
+    }
+  }
 }
 
-// One 64 x 64 diagonal block per workgroup (grid x: blocks along a diagonal,
-// stride sa1 / sx1; grid y: batches, stride sa2 / sx2).  factor = 1: Cholesky
-// of the block's lower part in place (A = L L^T, the upper part zeroed); a
-// pivot that is not positive sets *info and is replaced by 1.  Then X = L^-1
-// (lower) in three levels: the four 16 x 16 diagonal blocks by forward
-// substitution (one column per thread), then pairs of diagonal blocks are
-// joined as X21 = -X22 (L21 X11), 16 -> 32 and 32 -> 64, every output of a
-// product on its own thread.
-__global__ __launch_bounds__(256) void potrf64_kernel(double* A, int64_t lda, int64_t sa1,
-                                                      int64_t sa2, double* X, int64_t ldx,
-                                                      int64_t sx1, int64_t sx2, int factor,
-                                                      int* info) {
+// Inverse X = L^-1 of lower-triangular 64 x 64 diagonal blocks, one per
+// workgroup (grid x: blocks along a diagonal, stride sa1 / sx1; grid y:
+// batches, stride sa2 / sx2), in three levels: the four 16 x 16 diagonal
+// blocks by forward substitution (one column per thread), then pairs of
+// diagonal blocks are joined as X21 = -X22 (L21 X11), 16 -> 32 and 32 -> 64,
+// every output of a product on its own thread.
+__global__ __launch_bounds__(256) void trinv64_kernel(const double* A, int64_t lda, int64_t sa1, int64_t sa2,
+                                                      double* X, int64_t ldx, int64_t sx1, int64_t sx2) {
   __shared__ double a[kT][kT + 1];
   __shared__ double x[kT][kT + 1];
   A += blockIdx.x * sa1 + blockIdx.y * sa2;
@@ -175,37 +308,6 @@ __global__ __launch_bounds__(256) void potrf64_kernel(double* A, int64_t lda, in
     a[i][k] = k <= i ? A[i * lda + k] : 0.0;
   }
   __syncthreads();
-  if (factor) {
-    // Column j: lanes j .. 63 of wave 0 read the pivot before lane j writes
-    // its square root (one instruction stream).  Update: thread t owns column
-    // t % 64, rows t / 64 + 4 q, of the trailing part.
-    const int kk = tid % kT;
-    for (int j = 0; j < kT; ++j) {
-      if (tid >= j && tid < kT) {
-        double d = a[j][j];
-        if (!(d > 0.0)) {
-          if (tid == j) info[0] = 1;
-          d = 1.0;
-        }
-        const double sd = sqrt(d);
-        a[tid][j] = tid == j ? sd : a[tid][j] / sd;
-      }
-      __syncthreads();
-      if (kk > j) {
-        const double akj = a[kk][j];
-#pragma unroll
-        for (int q = 0; q < kT / 4; ++q) {
-          const int i = tid / kT + 4 * q;
-          if (i >= kk) a[i][kk] -= a[i][j] * akj;
-        }
-      }
-      __syncthreads();
-    }
-    for (int e = tid; e < kT * kT; e += 256) {
-      const int i = e / kT, k = e % kT;
-      A[i * lda + k] = k <= i ? a[i][k] : 0.0;
-    }
-  }
   __shared__ double rd[kT];          // 1 / L[i][i]
   __shared__ double tt[32 * 32];     // L21 X11 of the current level
   if (tid < kT) rd[tid] = 1.0 / a[tid][tid];
@@ -328,7 +430,20 @@ void gemm64(int64_t M, int64_t N, int64_t K, double alpha, const TA* A, int64_t 
   const dim3 grid(static_cast<unsigned>((N + kT - 1) / kT), static_cast<unsigned>((M + kT - 1) / kT),
                   static_cast<unsigned>(batch));
   gemm64_kernel<TA, TB><<<grid, dim3(256), 0, stream>>>(M, N, K, alpha, A, rsa, csa, bsa, B, rsb, csb,
-                                                        bsb, beta, C, rsc, csc, bsc, lower_only);
+                                                        bsb, beta, C, rsc, csc, bsc, lower_only, nullptr, 0,
+                                                        nullptr);
+}
+
+// Trailing update of a right-looking Cholesky step, C -= P P^T on the tiles
+// on or below the diagonal (P: n x 64, row stride ld; C: n x n, row stride
+// ld), whose first tile then factors and inverts the next diagonal block
+// (L into C's first tile, its inverse into X).
+void trailing_update_chol(int64_t n, const double* P, double* C, int64_t ld, double* X, int64_t ldx, int* info,
+                          hipStream_t stream) {
+  const unsigned tiles = static_cast<unsigned>((n + kT - 1) / kT);
+  gemm64_kernel<double, double, true><<<dim3(tiles, tiles, 1), dim3(256), 0, stream>>>(
+      n, n, int64_t{kT}, -1.0, P, ld, int64_t{1}, 0, P, int64_t{1}, ld, 0, 1.0, C, ld, int64_t{1}, 0, 1, X,
+      ldx, info);
 }
 
 // Lower-triangular inverse X = L^-1 of a batch of n x n matrices (n a multiple
@@ -403,18 +518,18 @@ sdq_status launch_hessian_factor(const double* h, int64_t k, double lam, double*
   clear_info_kernel<<<1, 64, 0, stream>>>(info);
   fill_f64_kernel<<<grid1(kk), 256, 0, stream>>>(X, kk, 0.0);
   reverse_tri_kernel<<<dim3(grid1(kk), 1), 256, 0, stream>>>(h, k, 0, k, A, k, 0, 1, lam);
+  // Right-looking blocked Cholesky in 64-column steps: the panel below the
+  // diagonal block is solved with the block's inverse, then the trailing lower
+  // part is updated, and the same launch factors the next diagonal block.
   const int64_t t = k / kT;
-  for (int64_t j = 0; j < t; ++j) {
-    const int64_t d = j * kT;
-    potrf64_kernel<<<dim3(1, 1), 256, 0, stream>>>(A + d * k + d, k, 0, 0, X + d * k + d, k, 0, 0, 1, info);
-    const int64_t r0 = d + kT, rows = k - r0;
-    if (rows <= 0) break;
-    // panel: L[r0:, d] = A[r0:, d] L_dd^-T (in place; one 64-wide column of tiles)
+  chol64_kernel<<<1, 256, 0, stream>>>(A, k, X, k, info);
+  for (int64_t j = 0; j + 1 < t; ++j) {
+    const int64_t d = j * kT, r0 = d + kT, rows = k - r0;
+    // L[r0:, d] = A[r0:, d] L_dd^-T, in place
     gemm64(rows, int64_t{kT}, int64_t{kT}, 1.0, A + r0 * k + d, k, int64_t{1}, X + d * k + d, int64_t{1}, k,
            0.0, A + r0 * k + d, k, int64_t{1}, stream);
-    // trailing lower part: A[r0:, r0:] -= L[r0:, d] L[r0:, d]^T
-    gemm64(rows, rows, int64_t{kT}, -1.0, A + r0 * k + d, k, int64_t{1}, A + r0 * k + d, int64_t{1}, k, 1.0,
-           A + r0 * k + r0, k, int64_t{1}, stream, 1);
+    // A[r0:, r0:] -= L[r0:, d] L[r0:, d]^T (lower), then block r0 factored
+    trailing_update_chol(rows, A + r0 * k + d, A + r0 * k + r0, k, X + r0 * k + r0, k, info, stream);
   }
   trtri_lower(A, X, k, k, 0, 1, tmp, stream);
   reverse_tri_kernel<<<dim3(grid1(kk), 1), 256, 0, stream>>>(X, k, 0, k, u, k, 0, 0, 0.0);
@@ -492,8 +607,8 @@ sdq_status launch_quantize_compensated(const float* w, const sdq_layout* L, cons
     fill_f64_kernel<<<grid1(nb * bb), 256, 0, stream>>>(cw.xb, nb * bb, 0.0);
     reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
         u, k, B * k + B, B, cw.lb, B, bb, 1, 0.0);
-    potrf64_kernel<<<dim3(static_cast<unsigned>(B / kT), static_cast<unsigned>(nb)), 256, 0, stream>>>(
-        cw.lb, B, kT * B + kT, bb, cw.xb, B, kT * B + kT, bb, 0, reinterpret_cast<int*>(cw.q.flag) + 1);
+    trinv64_kernel<<<dim3(static_cast<unsigned>(B / kT), static_cast<unsigned>(nb)), 256, 0, stream>>>(
+        cw.lb, B, kT * B + kT, bb, cw.xb, B, kT * B + kT, bb);
     trtri_lower(cw.lb, cw.xb, B, B, bb, static_cast<int>(nb), cw.tmp, stream);
     reverse_tri_kernel<<<dim3(grid1(bb), static_cast<unsigned>(nb)), 256, 0, stream>>>(
         cw.xb, B, bb, B, cw.vb, B, bb, 0, 0.0);

@@ -67,13 +67,26 @@ def test_factor_matches_oracle(k):
     assert np.max(np.abs(u.T @ u @ (h + lam * np.eye(k)) - np.eye(k))) < 1e-8
 
 
-def test_factor_reports_an_indefinite_matrix():
+@pytest.mark.parametrize("bad", [None, 0, 70, 130])
+def test_factor_reports_an_indefinite_matrix(bad):
+    # The pivot that fails lies in the first diagonal block (factored on its
+    # own) or in a later one (factored by the trailing update producing it).
+    # The factor works on the index-reversed matrix, so entry bad of the
+    # reversed diagonal is entry k - 1 - bad of H.
     torch = require_gpu()
     import paper_2510_03275_amd as P
-    h = -torch.eye(128, dtype=torch.float64, device="cuda")
+    k = 192
+    if bad is None:
+        h = -torch.eye(k, dtype=torch.float64, device="cuda")
+    else:
+        h = torch.eye(k, dtype=torch.float64, device="cuda")
+        h[k - 1 - bad, k - 1 - bad] = -1.0
     with pytest.raises(P.SdqError) as ei:
         P.hessian_factor(h, 0.0)
     assert ei.value.status == -10
+    ok = torch.eye(k, dtype=torch.float64, device="cuda")
+    u = P.hessian_factor(ok, 0.0).cpu().numpy()   # the flag does not stick
+    assert np.array_equal(u, np.eye(k))
 
 
 CASES = [
