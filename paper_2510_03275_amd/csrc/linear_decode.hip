@@ -468,6 +468,127 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
   }
 }
 
+// The same contraction with the planes shared through LDS: one workgroup owns
+// four consecutive 64-row panels of one linear (one per wave) and bpg
+// consecutive blocks; per block it copies the block's planes (cpb * NPG KB)
+// into LDS once, and every wave contracts its own panel's codes against them,
+// so each plane byte crosses L2 once per four panels instead of once per
+// panel.  A wave adds its outputs into y itself (one atomic per output and
+// workgroup when K is split).
+template <int LEVELS, int NPG, int CH>
+__global__ __launch_bounds__(256) void gemv_mfma_lds_kernel(
+    LinearSet S, const uint4* __restrict__ planes, const float* __restrict__ sx, int m,
+    int64_t n_chunks, int64_t nb, int m_up, int cpb, int bpg, int n_split, int accumulate) {
+  extern __shared__ uint4 pls[];
+  typedef int v4i __attribute__((ext_vector_type(4)));
+  constexpr uint32_t kTable = LEVELS == 2 ? 0x000001FFu : 0xFF000100u;   // code -> int8
+  constexpr uint32_t kMask = LEVELS == 2 ? 0x01010101u : 0x03030303u;
+  constexpr int kBits = LEVELS == 2 ? 1 : 2;
+  constexpr int SPC = LEVELS == 2 ? 2 : 1;
+  constexpr int kCpc = LEVELS == 2 ? 128 : 64;
+  const int lane = threadIdx.x % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+  const int lin = linear_of(S, blockIdx.y);            // units: groups of four panels
+  const int64_t n = S.n[lin];
+  const int64_t n_panels = (n + kPanel - 1) / kPanel;
+  const int64_t panel = (blockIdx.y - S.first[lin]) * 4 + wave;
+  const bool live = panel < n_panels;
+  const float* __restrict__ scales = S.scales[lin];
+  float* __restrict__ y = S.y[lin];
+  const int kg = lane / 16;
+  // A wave past the linear's last panel reads panel 0 (in bounds) and writes nothing.
+  const uint4* __restrict__ cpanel =
+      static_cast<const uint4*>(S.codes[lin]) + (live ? panel : 0) * n_chunks * kPanel;
+  const int per_block = cpb * SPC * NPG * 64;           // uint4 of one block's planes
+  float accf[NPG][4];
+#pragma unroll
+  for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) accf[pg][cg] = 0.0f;
+  const int64_t b_begin = static_cast<int64_t>(blockIdx.x) * bpg;
+  const int64_t b_end = min<int64_t>(nb, b_begin + bpg);
+  for (int64_t b = b_begin; b < b_end; ++b) {
+    const uint4* __restrict__ src = planes + b * per_block;
+    for (int i = threadIdx.x; i < per_block; i += 256) pls[i] = src[i];
+    float sxv[NPG];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      const int a = pg * 4 + kg;
+      const float v = sx[static_cast<int64_t>(min(a, m - 1)) * nb + b];
+      sxv[pg] = a < m ? v : 0.0f;
+    }
+    __syncthreads();
+    v4i acc[NPG][4];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+      for (int cg = 0; cg < 4; ++cg) acc[pg][cg] = v4i{0, 0, 0, 0};
+    const int64_t c_first = b * m_up / kCpc;
+    for (int c0 = 0; c0 < cpb; c0 += CH) {
+      uint4 q[CH];
+#pragma unroll
+      for (int j = 0; j < CH; ++j) q[j] = cpanel[min<int64_t>(c_first + c0 + j, n_chunks - 1) * kPanel + lane];
+#pragma unroll
+      for (int j = 0; j < CH; ++j) {
+        uint32_t r0 = q[j].x, r1 = q[j].y, r2 = q[j].z, r3 = q[j].w;
+        {
+          const auto s02 = __builtin_amdgcn_permlane32_swap(r0, r2, false, false);
+          const auto s13 = __builtin_amdgcn_permlane32_swap(r1, r3, false, false);
+          r0 = s02[0]; r2 = s02[1]; r1 = s13[0]; r3 = s13[1];
+          const auto s01 = __builtin_amdgcn_permlane16_swap(r0, r1, false, false);
+          const auto s23 = __builtin_amdgcn_permlane16_swap(r2, r3, false, false);
+          r0 = s01[0]; r1 = s01[1]; r2 = s23[0]; r3 = s23[1];
+        }
+        const uint32_t wcg[4] = {r0, r1, r2, r3};
+#pragma unroll
+        for (int s = 0; s < SPC; ++s)
+#pragma unroll
+          for (int cg = 0; cg < 4; ++cg) {
+            const uint32_t wv = wcg[cg];
+            v4i bop;
+#pragma unroll
+            for (int di = 0; di < 4; ++di) {
+              const int d = LEVELS == 2 ? 4 * s + di : di;
+              bop[di] = static_cast<int>(__builtin_amdgcn_perm(0u, kTable, (wv >> (kBits * d)) & kMask));
+            }
+#pragma unroll
+            for (int pg = 0; pg < NPG; ++pg) {
+              const uint4 a4 = pls[(((c0 + j) * SPC + s) * NPG + pg) * 64 + lane];
+              const v4i aop = {static_cast<int>(a4.x), static_cast<int>(a4.y), static_cast<int>(a4.z),
+                               static_cast<int>(a4.w)};
+              acc[pg][cg] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop, bop, acc[pg][cg], 0, 0, 0);
+            }
+          }
+      }
+    }
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+#pragma unroll
+      for (int cg = 0; cg < 4; ++cg) {
+        const float v = (static_cast<float>(acc[pg][cg][0]) * 65536.0f +
+                         static_cast<float>(acc[pg][cg][1]) * 256.0f) +
+                        static_cast<float>(acc[pg][cg][2]);
+        accf[pg][cg] += sxv[pg] * v;
+      }
+    }
+    __syncthreads();   // before the next block's planes overwrite these
+  }
+  if (!live) return;
+  // output (pg, cg, lane): activation row 4 pg + lane / 16, weight row 16 cg + lane % 16
+#pragma unroll
+  for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) {
+      const int a = pg * 4 + kg;
+      const int64_t r = panel * kPanel + 16 * cg + lane % 16;
+      if (a >= m || r >= n) continue;
+      const float val = accf[pg][cg] * scales[r];
+      float* yp = &y[static_cast<int64_t>(a) * n + r];
+      if (n_split > 1) unsafeAtomicAdd(yp, val);
+      else *yp = accumulate ? *yp + val : val;
+    }
+}
+
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
   for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < count;
        i += static_cast<int64_t>(gridDim.x) * blockDim.x)
@@ -901,6 +1022,7 @@ int64_t fill_first(LinearSet& S, F per) {
 }
 
 int64_t panels_of(int64_t n) { return (n + kPanel - 1) / kPanel; }
+constexpr int64_t kLdsPlanesWgs = 768;
 int64_t pgroups_of(int64_t n) { return (panels_of(n) + kGemvWaves - 1) / kGemvWaves; }
 
 template <int LEVELS, int NPG, int CH>
@@ -911,6 +1033,32 @@ void launch_mfma_ch(const DecodeWs& w, LinearSet S, const sdq_layout* L, int64_t
   const int splits = mfma_splits(L, m);
   // K groups fastest: consecutive workgroups sweep one panel's chunks.
   const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(panels));
+  // Planes shared through LDS by four panels: for two plane groups (5-8 rows)
+  // on launches of at least kLdsPlanesWgs workgroups, when the chunks go in
+  // batches of four or the rows are long (64 blocks or more).  Measured on
+  // MI355X at m = 8 (70B shapes): gate/up 93 -> 87 us at OSR 3 and 65 -> 62 us
+  // at OSR 2 (batches of four), but 78 -> 80 at OSR 2.5 and 51 -> 53 at 1.5
+  // (batches of two); down 2-6 % faster at OSR 1.5-3; the smaller q/k/v and
+  // o launches (256-320 workgroups of four panels) ran 21 -> 31 and
+  // 17 -> 27 us, and one or four plane groups were slower at every size
+  // (m = 2 gate/up 66 -> 72 us, m = 16 140 -> 188 us).
+  // SDQ_MFMA_LDS=0 or 1 forces the choice (a tuning and test aid, read on
+  // every launch so that a test can take both paths in one process).
+  LinearSet S4 = S;
+  const int64_t pgroups = fill_first(S4, pgroups_of);
+  const size_t lds_bytes = static_cast<size_t>(mfma_cpb(L)) * (LEVELS == 2 ? 2 : 1) * NPG * 1024;
+  const char* lds_env = std::getenv("SDQ_MFMA_LDS");
+  bool lds = NPG == 2 && static_cast<int64_t>(splits) * pgroups >= kLdsPlanesWgs && (CH >= 4 || L->nb >= 64);
+  if (lds_env && (std::atoi(lds_env) == 0 || std::atoi(lds_env) == 1)) lds = std::atoi(lds_env) == 1;
+  if constexpr (NPG == 2) {
+    if (lds && lds_bytes <= 65536) {
+      const dim3 grid4(static_cast<unsigned>(splits), static_cast<unsigned>(pgroups));
+      gemv_mfma_lds_kernel<LEVELS, NPG, CH><<<grid4, dim3(256), lds_bytes, stream>>>(
+          S4, reinterpret_cast<const uint4*>(w.planes), w.sx, static_cast<int>(m), L->n_chunks, L->nb,
+          L->m_up, mfma_cpb(L), 4 * bpw, splits, accumulate ? 1 : 0);
+      return;
+    }
+  }
   gemv_mfma_kernel<LEVELS, NPG, CH><<<grid, dim3(256), 0, stream>>>(
       S, reinterpret_cast<const uint4*>(w.planes), w.sx, static_cast<int>(m), L->n_chunks, L->nb, L->m_up,
       mfma_cpb(L), bpw, splits, accumulate ? 1 : 0);

@@ -46,6 +46,23 @@ def test_linear_small_f16(n, k, osr, levels, m):
     assert np.all(err <= TOL), err.max()
 
 
+@pytest.mark.parametrize("lds", ["0", "1"])
+@pytest.mark.parametrize("m", [5, 8])
+@pytest.mark.parametrize("n,k,osr,levels", SHAPES)
+def test_linear_mfma_planes_from_lds_or_l2(n, k, osr, levels, m, lds, monkeypatch):
+    # The 5-8-row contraction has two kernels: planes read per panel from L2,
+    # or staged in LDS once per four panels (chosen by launch size; forced
+    # here so that both run on every shape).
+    torch = require_gpu()
+    monkeypatch.setenv("SDQ_MFMA_LDS", lds)
+    enc, r = _oracle_codes_on_device(torch, n, k, osr, levels, seed=3 * n + m)
+    x_dev, x64 = to_device_x(synth.activations_f32(m + 1, 0, m, k), "f16", torch)
+    y = _run_linear(torch, enc, x_dev)
+    y_ref = OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up)
+    err = OL.rel_err_rows(y, y_ref)
+    assert np.all(err <= TOL), err.max()
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("m", [1, 5, 16, 40])
 def test_linear_small_other_dtypes(dtype, m):
