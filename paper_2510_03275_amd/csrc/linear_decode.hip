@@ -237,6 +237,20 @@ __device__ inline uint32_t plane_byte(int q, int t) {
   return static_cast<uint32_t>(v) & 255u;
 }
 
+// Max over the 64 lanes of a wave of non-negative floats (compared as their
+// bit patterns, which order them alike): DPP steps within each row of 16
+// lanes, then the row broadcasts carry rows 0-2 into row 3; read from lane 63.
+__device__ inline float wave_max_nonneg(float v) {
+  int x = __float_as_int(v);
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0xB1, 0xF, 0xF, false));    // quad_perm [1, 0, 3, 2]
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x4E, 0xF, 0xF, false));    // quad_perm [2, 3, 0, 1]
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x141, 0xF, 0xF, false));   // row_half_mirror
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x140, 0xF, 0xF, false));   // row_mirror
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x142, 0xA, 0xF, false));   // row_bcast:15 -> rows 1, 3
+  x = max(x, __builtin_amdgcn_update_dpp(x, x, 0x143, 0xC, 0xF, false));   // row_bcast:31 -> rows 2, 3
+  return __int_as_float(__builtin_amdgcn_readlane(x, 63));
+}
+
 // One workgroup: one 64-code segment u of block b's chunk slots (code
 // positions floor(b M / chunk) * chunk + 64 u + [0, 64)), all m rows; the
 // samples of block b among them by the fp32 expansion, the rest zero; then
@@ -260,13 +274,45 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   const int64_t g0 = c_first * kCpc + static_cast<int64_t>(blockIdx.x) * 64;
   const int o = static_cast<int>(g0 + lane - b * m_up);    // this lane's sample within block b
   const bool in_block = o >= 0 && o < m_up;
+  // The activation block goes to LDS with every load issued before any
+  // store (converted afterwards: a conversion next to its load waits for it,
+  // one global round trip per element), and before the E columns, so that
+  // the stores and the max below wait for x alone.
+  constexpr int XPT = kMaxDecodeRows * B / kExpThreads;   // elements per thread, at most
+  const int mb = m * B;
+  uint32_t xr[XPT];
+  const int k32 = static_cast<int>(k);   // m k < 2^31 on the decode path
+  if (xt == SDQ_F32) {
+    const uint32_t* __restrict__ xp = static_cast<const uint32_t*>(x) + b * B;
+#pragma unroll
+    for (int r = 0; r < XPT; ++r) {
+      if (kExpThreads * r >= mb) break;
+      const int idx = tid + kExpThreads * r;
+      xr[r] = idx < mb ? xp[(idx / B) * k32 + idx % B] : 0u;
+    }
+  } else {
+    const uint16_t* __restrict__ xp = static_cast<const uint16_t*>(x) + b * B;
+#pragma unroll
+    for (int r = 0; r < XPT; ++r) {
+      if (kExpThreads * r >= mb) break;
+      const int idx = tid + kExpThreads * r;
+      xr[r] = idx < mb ? xp[(idx / B) * k32 + idx % B] : 0u;
+    }
+  }
   float4 e[TQ / 4];
   const float4* ep = edec + static_cast<int64_t>(w * (TQ / 4)) * m_pad + (in_block ? o : 0);
 #pragma unroll
   for (int q = 0; q < TQ / 4; ++q) e[q] = ep[static_cast<int64_t>(q) * m_pad];
-  for (int idx = tid; idx < m * B; idx += kExpThreads) {
-    const int i = idx / B, t = idx % B;
-    xs[i][t] = load_x(x, xt, static_cast<int64_t>(i) * k + b * B + t);
+#pragma unroll
+  for (int r = 0; r < XPT; ++r) {
+    if (kExpThreads * r >= mb) break;
+    const int idx = tid + kExpThreads * r;
+    if (idx < mb) {
+      const float v = xt == SDQ_F32    ? __uint_as_float(xr[r])
+                      : xt == SDQ_BF16 ? __uint_as_float(xr[r] << 16)
+                                       : __half2float(__ushort_as_half(static_cast<unsigned short>(xr[r])));
+      xs[idx / B][idx % B] = v;
+    }
   }
   const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
   const int64_t n_wg = static_cast<int64_t>(gridDim.x) * gridDim.y;
@@ -276,8 +322,7 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   for (int i = w; i < m; i += 4) {
     float mx = 0.0f;
     for (int t = lane; t < B; t += 64) mx = fmaxf(mx, fabsf(xs[i][t]));
-#pragma unroll
-    for (int off = 32; off > 0; off >>= 1) mx = fmaxf(mx, __shfl_xor(mx, off));
+    mx = wave_max_nonneg(mx);
     if (lane == 0) xmax[i] = mx;
   }
   for (int i = 0; i < m; ++i) {
