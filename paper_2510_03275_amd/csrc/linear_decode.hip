@@ -377,6 +377,127 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   }
 }
 
+// Base-3 codes on the integer-MFMA path (read as stored, no unpack pass).
+// A base-3 chunk holds 80 codes of a row, five per byte (first code the most
+// significant digit).  The k order of the contraction follows the digits:
+// block b owns cpb3 chunk slots (rounded up to whole groups of four), slot j
+// starting at chunk floor(b M / 80) + j; each group of four slots gives five
+// 64-code k-steps: one per slot with digits 0-3 of its 16 bytes (k-group kg,
+// dword di, byte beta <-> digit di of byte 4 kg + beta), and one with digit 4
+// of all four slots (dword di <-> slot 4 G + di, byte beta <-> byte
+// 4 kg + beta).  The planes are laid out per (block, step, plane group) as for
+// the 2-bit codes.
+constexpr int kB3Group = 4;    // slots per group of steps
+constexpr int kB3Steps = 5;    // k-steps per group
+
+// One workgroup: 64 consecutive code positions of block b's slots (segment u
+// of the block's 5 * groups segments), all m rows: the same fp32 expansion
+// and 24-bit quantisation as expand_planes_kernel, then every plane byte of
+// those codes (all 16 MFMA rows of each plane group, zero where no activation
+// row or plane) written to its place in the digit order.
+template <int B>
+__global__ __launch_bounds__(kExpThreads) void expand_planes_b3_kernel(
+    const void* __restrict__ x, sdq_dtype xt, int m, int npg, int64_t k, int64_t nb, int m_up,
+    int m_pad, int steps3, const float4* __restrict__ edec, float e1max, uint8_t* __restrict__ planes,
+    float* __restrict__ sx, LinearSet zero) {
+  constexpr int TQ = B / 4;
+  __shared__ float xs[kMaxDecodeRows][B];
+  __shared__ float red[4][kMaxDecodeRows][64];
+  __shared__ int qv[kMaxDecodeRows][64];
+  __shared__ float xmax[kMaxDecodeRows];
+  const int tid = threadIdx.x;
+  const int lane = tid % 64;
+  const int w = tid / 64;
+  const int64_t b = blockIdx.y;
+  const int64_t c_first = b * m_up / kBase3PerChunk;       // block b's first base-3 chunk
+  const int64_t g0 = c_first * kBase3PerChunk + static_cast<int64_t>(blockIdx.x) * 64;
+  const int o = static_cast<int>(g0 + lane - b * m_up);    // this lane's sample within block b
+  const bool in_block = o >= 0 && o < m_up;
+  constexpr int XPT = kMaxDecodeRows * B / kExpThreads;
+  const int mb = m * B;
+  uint32_t xr[XPT];
+  const int k32 = static_cast<int>(k);
+  if (xt == SDQ_F32) {
+    const uint32_t* __restrict__ xp = static_cast<const uint32_t*>(x) + b * B;
+#pragma unroll
+    for (int r = 0; r < XPT; ++r) {
+      if (kExpThreads * r >= mb) break;
+      const int idx = tid + kExpThreads * r;
+      xr[r] = idx < mb ? xp[(idx / B) * k32 + idx % B] : 0u;
+    }
+  } else {
+    const uint16_t* __restrict__ xp = static_cast<const uint16_t*>(x) + b * B;
+#pragma unroll
+    for (int r = 0; r < XPT; ++r) {
+      if (kExpThreads * r >= mb) break;
+      const int idx = tid + kExpThreads * r;
+      xr[r] = idx < mb ? xp[(idx / B) * k32 + idx % B] : 0u;
+    }
+  }
+  float4 e[TQ / 4];
+  const float4* ep = edec + static_cast<int64_t>(w * (TQ / 4)) * m_pad + (in_block ? o : 0);
+#pragma unroll
+  for (int q = 0; q < TQ / 4; ++q) e[q] = ep[static_cast<int64_t>(q) * m_pad];
+#pragma unroll
+  for (int r = 0; r < XPT; ++r) {
+    if (kExpThreads * r >= mb) break;
+    const int idx = tid + kExpThreads * r;
+    if (idx < mb) {
+      const float v = xt == SDQ_F32    ? __uint_as_float(xr[r])
+                      : xt == SDQ_BF16 ? __uint_as_float(xr[r] << 16)
+                                       : __half2float(__ushort_as_half(static_cast<unsigned short>(xr[r])));
+      xs[idx / B][idx % B] = v;
+    }
+  }
+  const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  const int64_t n_wg = static_cast<int64_t>(gridDim.x) * gridDim.y;
+  zero_outputs(zero, m, wg, n_wg, tid);
+  __syncthreads();
+  for (int i = w; i < m; i += 4) {
+    float mx = 0.0f;
+    for (int t = lane; t < B; t += 64) mx = fmaxf(mx, fabsf(xs[i][t]));
+    mx = wave_max_nonneg(mx);
+    if (lane == 0) xmax[i] = mx;
+  }
+  for (int i = 0; i < m; ++i) {
+    const float4* xrow = reinterpret_cast<const float4*>(&xs[i][w * TQ]);
+    float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
+#pragma unroll
+    for (int q = 0; q < TQ / 4; ++q) {
+      const float4 v = xrow[q];
+      a0 += e[q].x * v.x;
+      a1 += e[q].y * v.y;
+      a2 += e[q].z * v.z;
+      a3 += e[q].w * v.w;
+    }
+    red[w][i][lane] = (a0 + a1) + (a2 + a3);
+  }
+  __syncthreads();
+  for (int idx = tid; idx < m * 64; idx += kExpThreads) {
+    const int i = idx / 64, l = idx % 64;
+    const float val = (red[0][i][l] + red[1][i][l]) + (red[2][i][l] + red[3][i][l]);
+    const float bound = xmax[i] * e1max;
+    const int ol = static_cast<int>(g0 + l - b * m_up);
+    qv[i][l] = bound > 0.0f && ol >= 0 && ol < m_up ? __float2int_rn(val * (kQ / bound)) : 0;
+    if (blockIdx.x == 0 && l == 0) sx[static_cast<int64_t>(i) * nb + b] = bound / kQ;
+  }
+  __syncthreads();
+  // Plane bytes: entry idx = code l of the segment (fastest), MFMA row p, plane group pg.
+  for (int idx = tid; idx < 64 * 16 * npg; idx += kExpThreads) {
+    const int l = idx % 64, p = (idx / 64) % 16, pg = idx / 1024;
+    const int64_t g = g0 + l;
+    const int j = static_cast<int>(g / kBase3PerChunk - c_first);
+    const int pos = static_cast<int>(g % kBase3PerChunk);
+    const int byte = pos / 5, digit = pos % 5;
+    const int kg = byte / 4, beta = byte % 4;
+    const int step = (j / kB3Group) * kB3Steps + (digit < 4 ? j % kB3Group : 4);
+    const int di = digit < 4 ? digit : j % kB3Group;
+    const int a = pg * 4 + p / 4, t = p % 4;
+    const uint32_t val = a < m && t < 3 ? plane_byte(qv[a][l], t) : 0u;
+    planes[((((b * steps3 + step) * npg + pg) * 64 + kg * 16 + p) * 16) + 4 * di + beta] = static_cast<uint8_t>(val);
+  }
+}
+
 // One workgroup: one 64-row panel and 4 * bpw consecutive blocks, wave w
 // taking blocks w * bpw .. w * bpw + bpw - 1 of them (the workgroup reads one
 // contiguous stretch of the panel's chunks; consecutive workgroups continue
@@ -632,6 +753,172 @@ __global__ __launch_bounds__(256) void gemv_mfma_lds_kernel(
       if (n_split > 1) unsafeAtomicAdd(yp, val);
       else *yp = accumulate ? *yp + val : val;
     }
+}
+
+// The five base-3 digits d = code + 1 of each byte of w, as five words of
+// four bytes (word j: digit j of bytes 0..3).  A byte q stores
+// ceil(256 v / 243) for its digits' value v (first code most significant), so
+// digit j is the integer part of 3 r, r the fraction left by the digits
+// before it (r = q / 256 to begin with).  Bytes 0, 2 and 1, 3 travel as two
+// 16-bit fractions per word; 3 r < 768 keeps each product inside its half,
+// with the digit in the half's high byte: one v_perm gathers the four.
+__device__ inline void base3_digits(uint32_t w, uint32_t d[5]) {
+  uint32_t P = w & 0x00FF00FFu;           // bytes 0, 2
+  uint32_t Q = (w >> 8) & 0x00FF00FFu;    // bytes 1, 3
+#pragma unroll
+  for (int j = 0; j < 5; ++j) {
+    // 3 P as (P << 1) + P in one full-rate instruction (left to itself the
+    // compiler turns it into a 24-bit multiply)
+    asm("v_lshl_add_u32 %0, %1, 1, %1" : "=v"(P) : "v"(P));
+    asm("v_lshl_add_u32 %0, %1, 1, %1" : "=v"(Q) : "v"(Q));
+    d[j] = __builtin_amdgcn_perm(Q, P, 0x07030501u);   // P.b1 Q.b1 P.b3 Q.b3
+    if (j < 4) {
+      P &= 0x00FF00FFu;
+      Q &= 0x00FF00FFu;
+    }
+  }
+}
+
+// gemv_mfma_kernel for base-3 codes: per group of four chunk slots, each
+// slot's chunk is loaded lane = row and transposed as for 2-bit codes, its
+// four bytes per lane give the digit bytes d = code + 1 of the slot's k-step
+// and one word of the group's digit-4 k-step; the sums of d x less the sums
+// of x (one more product per k-step against a B operand of ones) are the
+// sums of code x.
+template <int NPG>
+__global__ __launch_bounds__(256) void gemv_mfma_b3_kernel(
+    LinearSet S, const uint4* __restrict__ planes, const float* __restrict__ sx, int m,
+    int64_t n_chunks, int64_t nb, int m_up, int cpb3, int steps3, int bpw, int n_split, int accumulate) {
+  typedef int v4i __attribute__((ext_vector_type(4)));
+  __shared__ float red[4][NPG * 4][64];
+  const int lane = threadIdx.x % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / 64);
+  const int lin = linear_of(S, blockIdx.y);            // units: panels
+  const int64_t panel = blockIdx.y - S.first[lin];
+  const int64_t n = S.n[lin];
+  const float* __restrict__ scales = S.scales[lin];
+  float* __restrict__ y = S.y[lin];
+  const int kg = lane / 16;
+  const uint4* __restrict__ cpanel = static_cast<const uint4*>(S.codes[lin]) + panel * n_chunks * kPanel;
+  const v4i ones = {0x01010101, 0x01010101, 0x01010101, 0x01010101};
+  float accf[NPG][4];
+#pragma unroll
+  for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) accf[pg][cg] = 0.0f;
+  const int64_t b_begin = (static_cast<int64_t>(blockIdx.x) * 4 + wave) * bpw;
+  const int64_t b_end = min<int64_t>(nb, b_begin + bpw);
+  const int groups = steps3 / kB3Steps;
+  for (int64_t b = b_begin; b < b_end; ++b) {
+    v4i acc[NPG][4], acc1[NPG];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      acc1[pg] = v4i{0, 0, 0, 0};
+#pragma unroll
+      for (int cg = 0; cg < 4; ++cg) acc[pg][cg] = v4i{0, 0, 0, 0};
+    }
+    const int64_t c_first = b * m_up / kBase3PerChunk;
+    float sxv[NPG];
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+      const int a = pg * 4 + kg;
+      const float v = sx[static_cast<int64_t>(min(a, m - 1)) * nb + b];
+      sxv[pg] = a < m ? v : 0.0f;
+    }
+    for (int G = 0; G < groups; ++G) {
+      uint4 q[kB3Group];
+      uint4 av[kB3Steps][NPG];
+#pragma unroll
+      for (int jj = 0; jj < kB3Group; ++jj)
+        q[jj] = cpanel[min<int64_t>(c_first + G * kB3Group + jj, n_chunks - 1) * kPanel + lane];
+#pragma unroll
+      for (int st = 0; st < kB3Steps; ++st)
+#pragma unroll
+        for (int pg = 0; pg < NPG; ++pg)
+          av[st][pg] = planes[((((b * steps3) + G * kB3Steps + st) * NPG + pg) * 64) + lane];
+      uint32_t d4[4][kB3Group];
+#pragma unroll
+      for (int jj = 0; jj < kB3Group; ++jj) {
+        // A slot past the block's last holds zero planes: its products are skipped.
+        const bool live = G * kB3Group + jj < cpb3;
+        uint32_t r0 = q[jj].x, r1 = q[jj].y, r2 = q[jj].z, r3 = q[jj].w;
+        {
+          const auto s02 = __builtin_amdgcn_permlane32_swap(r0, r2, false, false);
+          const auto s13 = __builtin_amdgcn_permlane32_swap(r1, r3, false, false);
+          r0 = s02[0]; r2 = s02[1]; r1 = s13[0]; r3 = s13[1];
+          const auto s01 = __builtin_amdgcn_permlane16_swap(r0, r1, false, false);
+          const auto s23 = __builtin_amdgcn_permlane16_swap(r2, r3, false, false);
+          r0 = s01[0]; r1 = s01[1]; r2 = s23[0]; r3 = s23[1];
+        }
+        const uint32_t wcg[4] = {r0, r1, r2, r3};
+#pragma unroll
+        for (int cg = 0; cg < 4; ++cg) {
+          uint32_t d[5];
+          base3_digits(wcg[cg], d);
+          d4[cg][jj] = d[4];
+          if (live) {
+            const v4i bop = {static_cast<int>(d[0]), static_cast<int>(d[1]), static_cast<int>(d[2]),
+                             static_cast<int>(d[3])};
+#pragma unroll
+            for (int pg = 0; pg < NPG; ++pg) {
+              const uint4 a4 = av[jj][pg];
+              const v4i aop = {static_cast<int>(a4.x), static_cast<int>(a4.y), static_cast<int>(a4.z),
+                               static_cast<int>(a4.w)};
+              acc[pg][cg] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop, bop, acc[pg][cg], 0, 0, 0);
+            }
+          }
+        }
+        if (live) {
+#pragma unroll
+          for (int pg = 0; pg < NPG; ++pg) {
+            const uint4 a4 = av[jj][pg];
+            const v4i aop = {static_cast<int>(a4.x), static_cast<int>(a4.y), static_cast<int>(a4.z),
+                             static_cast<int>(a4.w)};
+            acc1[pg] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop, ones, acc1[pg], 0, 0, 0);
+          }
+        }
+      }
+      // the group's digit-4 step (a dead slot's word meets zero planes)
+#pragma unroll
+      for (int pg = 0; pg < NPG; ++pg) {
+        const uint4 a4 = av[kB3Group][pg];
+        const v4i aop = {static_cast<int>(a4.x), static_cast<int>(a4.y), static_cast<int>(a4.z),
+                         static_cast<int>(a4.w)};
+#pragma unroll
+        for (int cg = 0; cg < 4; ++cg) {
+          const v4i bop = {static_cast<int>(d4[cg][0]), static_cast<int>(d4[cg][1]), static_cast<int>(d4[cg][2]),
+                           static_cast<int>(d4[cg][3])};
+          acc[pg][cg] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop, bop, acc[pg][cg], 0, 0, 0);
+        }
+        acc1[pg] = __builtin_amdgcn_mfma_i32_16x16x64_i8(aop, ones, acc1[pg], 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int pg = 0; pg < NPG; ++pg) {
+#pragma unroll
+      for (int cg = 0; cg < 4; ++cg) {
+        const v4i t = acc[pg][cg] - acc1[pg];
+        const float v = (static_cast<float>(t[0]) * 65536.0f + static_cast<float>(t[1]) * 256.0f) +
+                        static_cast<float>(t[2]);
+        accf[pg][cg] += sxv[pg] * v;
+      }
+    }
+  }
+#pragma unroll
+  for (int pg = 0; pg < NPG; ++pg)
+#pragma unroll
+    for (int cg = 0; cg < 4; ++cg) red[wave][pg * 4 + cg][lane] = accf[pg][cg];
+  __syncthreads();
+  for (int idx = threadIdx.x; idx < NPG * 4 * 64; idx += 256) {
+    const int pc = idx / 64, l = idx % 64;
+    const int a = (pc / 4) * 4 + l / 16;
+    const int64_t r = panel * kPanel + 16 * (pc % 4) + l % 16;
+    if (a >= m || r >= n) continue;
+    const float val = ((red[0][pc][l] + red[1][pc][l]) + (red[2][pc][l] + red[3][pc][l])) * scales[r];
+    float* yp = &y[static_cast<int64_t>(a) * n + r];
+    if (n_split > 1) unsafeAtomicAdd(yp, val);
+    else *yp = accumulate ? *yp + val : val;
+  }
 }
 
 __global__ void fill_zero_kernel(float* __restrict__ p, int64_t count) {
@@ -995,6 +1282,21 @@ int mfma_cpb(const sdq_layout* L) {
   return static_cast<int>(most);
 }
 
+// Base-3 chunk slots per block on the MFMA path (the most 80-code chunks any
+// block touches, rounded up to whole groups of four) and k-steps per block.
+int mfma_cpb3(const sdq_layout* L) {
+  int64_t most = 0;
+  for (int64_t b = 0; b < L->nb; ++b) {
+    const int64_t first = b * L->m_up / kBase3PerChunk;
+    const int64_t end = ((b + 1) * L->m_up + kBase3PerChunk - 1) / kBase3PerChunk;
+    most = std::max(most, end - first);
+    if (L->m_up % kBase3PerChunk == 0) break;
+  }
+  return static_cast<int>(most);
+}
+int mfma_steps3(const sdq_layout* L) { return (mfma_cpb3(L) + kB3Group - 1) / kB3Group * kB3Steps; }
+bool mfma_base3(const sdq_layout* L, int64_t m) { return L->packing == SDQ_PACK_BASE3 && use_mfma(L, m); }
+
 // Blocks per wave of the MFMA GEMV (each split over K costs one atomic add per
 // output); SDQ_MFMA_BPW overrides.  Measured on MI355X (70B shapes and
 // 8192 x 8192, OSR 2): one block per wave is best up to two plane groups
@@ -1029,7 +1331,8 @@ DecodeWs carve(const sdq_layout* L, int64_t m, void* base) {
   DecodeWs w{};
   char* p = static_cast<char*>(base);
   if (use_mfma(L, m)) {
-    const size_t steps = static_cast<size_t>(L->nb) * mfma_cpb(L) * (L->levels == 2 ? 2 : 1);
+    const size_t steps = mfma_base3(L, m) ? static_cast<size_t>(L->nb) * mfma_steps3(L)
+                                          : static_cast<size_t>(L->nb) * mfma_cpb(L) * (L->levels == 2 ? 2 : 1);
     const size_t pl = align_up(steps * npg_for(m) * 1024, 256);
     w.planes = reinterpret_cast<uint32_t*>(p);
     w.sx = reinterpret_cast<float*>(p + pl);
@@ -1200,7 +1503,7 @@ sdq_status decode_supported(const sdq_layout* L) {
 }
 
 bool decode_reads_base3(const sdq_layout* L, int64_t m) {
-  return L->packing == SDQ_PACK_BASE3 && m == 1 && !use_mfma(L, m);
+  return L->packing == SDQ_PACK_BASE3 && (m == 1 || use_mfma(L, m));
 }
 
 bool decode_needs_zero_y(const sdq_layout* L, int64_t m, int64_t panels) {
@@ -1215,6 +1518,24 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const LinearSet z = zero ? *zero : LinearSet{};
   const dim3 egrid(static_cast<unsigned>(T->m_pad / 64), static_cast<unsigned>(L->nb));
+  if (mfma_base3(L, m)) {
+    const int steps3 = mfma_steps3(L);
+    const dim3 pgrid(static_cast<unsigned>(steps3), static_cast<unsigned>(L->nb));
+#define SDQ_PLANES3(BB)                                                                          \
+  expand_planes_b3_kernel<BB><<<pgrid, dim3(kExpThreads), 0, stream>>>(                          \
+      x, xt, static_cast<int>(m), npg_for(m), L->k, L->nb, L->m_up, T->m_pad, steps3,            \
+      reinterpret_cast<const float4*>(T->edec), T->e1max, reinterpret_cast<uint8_t*>(w.planes),  \
+      w.sx, z)
+    switch (B) {
+      case 64: SDQ_PLANES3(64); break;
+      case 128: SDQ_PLANES3(128); break;
+      default: SDQ_PLANES3(256); break;
+    }
+#undef SDQ_PLANES3
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_error(e, "decode expansion launch");
+    return SDQ_OK;
+  }
   if (use_mfma(L, m)) {
     const int npg = npg_for(m);
     const int cpb = mfma_cpb(L);
@@ -1296,7 +1617,23 @@ sdq_status launch_decode_contract(int64_t m, LinearSet S, const sdq_layout* L, b
       fill_zero_kernel<<<dim3(blocks), dim3(256), 0, stream>>>(S.y[j], count);
     }
   }
-  if (L->packing == SDQ_PACK_BASE3) {
+  if (mfma_base3(L, m)) {
+    const int64_t panels = fill_first(S, panels_of);
+    const int bpw = mfma_bpw(L, m);
+    const int splits = mfma_splits(L, m);
+    const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(panels));
+#define SDQ_B3(NPG_)                                                                                  \
+  gemv_mfma_b3_kernel<NPG_><<<grid, dim3(256), 0, stream>>>(                                          \
+      S, reinterpret_cast<const uint4*>(w.planes), w.sx, static_cast<int>(m), L->n_chunks, L->nb, L->m_up, \
+      mfma_cpb3(L), mfma_steps3(L), bpw, splits, accumulate ? 1 : 0)
+    switch (npg_for(m)) {
+      case 1: SDQ_B3(1); break;
+      case 2: SDQ_B3(2); break;
+      case 3: SDQ_B3(3); break;
+      default: SDQ_B3(4); break;
+    }
+#undef SDQ_B3
+  } else if (L->packing == SDQ_PACK_BASE3) {
     if (!decode_reads_base3(L, m)) return set_error(SDQ_ERR_ARG, "base-3 codes need unpacking on this path");
     switch (pick_seg(L, 1, set_panels(S))) {
       case 8: launch_gemv_base3_seg<8>(w, S, L, accumulate, stream); break;
