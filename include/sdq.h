@@ -142,9 +142,9 @@ sdq_status sdq_layout_set_hadamard(sdq_layout* layout, int32_t mode, const int8_
 
 /* Select the code storage of a ternary layout (sdq_packing); recomputes
  * codes_per_chunk (80 for SDQ_PACK_BASE3, 64 otherwise) and n_chunks.
- * Decode of one activation row reads base-3 codes directly; other row counts
- * first unpack them to 2-bit fields in the workspace (one extra pass over the
- * codes per call, see sdq_linear_workspace_bytes).
+ * Decode (m <= 16 activation rows) reads base-3 codes directly; prefill
+ * (m > 16) first unpacks them to 2-bit fields in the workspace (one extra
+ * pass over the codes per call, see sdq_linear_workspace_bytes).
  * Errors: SDQ_ERR_ARG (layout NULL or not from sdq_layout_init, bad value),
  * SDQ_ERR_LEVELS (base-3 for binary codes). */
 sdq_status sdq_layout_set_packing(sdq_layout* layout, int32_t packing);
@@ -238,13 +238,15 @@ sdq_status sdq_quantize_compensated(const float* w_dev, const sdq_layout* layout
  * expanded activations, at offset 0 --
  *   m = 1:        fp32 x_tilde, k_up rounded up to whole chunks;
  *   2 <= m <= 16: x_tilde as 24-bit fixed point (three signed-byte planes,
- *                 rows in groups of four, per block in chunk slots), then the
- *                 fp32 plane scale of every (row, block);
+ *                 rows in groups of four, per block in chunk slots; for
+ *                 base-3 codes in the order of their digits: per group of
+ *                 four 80-code chunks, five 64-code steps), then the fp32
+ *                 plane scale of every (row, block);
  *   m > 16:       fp16 x_tilde, m x k_up rounded up to whole chunks (twice,
  *                 an fp16 pair hi + lo, for layouts with SDQ_HAD_NONE), each
  *                 row scaled by a power of two p_i that keeps it inside
  *                 fp16's normal range, then p_i and 1 / p_i (fp32 [m] each);
- * for a base-3 layout and m > 1 the chunks are those of 2-bit fields, and the
+ * for a base-3 layout and m > 16 the chunks are those of 2-bit fields, and the
  * 2-bit copy of the codes follows (n_pad x ceil(k_up / 64) x 16 bytes). */
 size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
 
