@@ -29,6 +29,8 @@
 
 #include <algorithm>
 #include <cstdlib>
+#include <string>
+#include <type_traits>
 #include <hip/hip_fp16.h>
 #include <hip/hip_bf16.h>
 
@@ -282,6 +284,176 @@ __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
 
 #undef SDQ_FETCH
 
+// E-stationary form of the same product, for fp16 and bf16 activations with
+// B = 128 or 256 and a single fp16 x_tilde (the layouts with Had): E^T is the
+// same for every block, so a workgroup keeps one 128-sample slice of it in
+// registers, as MFMA B fragments (each wave 32 samples x B taps, hi and lo),
+// loaded once, and walks a range of (128-row tile, block) items.  Each item's
+// x tile goes straight from global memory to LDS (global_load_lds, 16-byte
+// groups XOR-swizzled by row as in the GEMM) in two buffers, the next item's
+// copies in flight during this item's MFMAs, with the tile's row factors p_i
+// copied beside it.  The products run on the activation's own type: fp16 x
+// against the fp16 pair hi + lo of E, bf16 x against a bf16 pair of E formed
+// in registers (hi = bf16(E), lo = bf16(E - hi), E to ~2^-17).  E^T is the
+// A operand, so a lane's accumulators hold four consecutive samples of one
+// x_tilde row: the sums are multiplied by p_i in fp32, rounded once to fp16
+// and stored 8 bytes at a time.  Workgroups sharing an item (the slices) are
+// placed on one XCD.  Barriers are plain s_barrier with explicit counter
+// waits (a __syncthreads() fence would wait for the copies in flight).
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef __attribute__((address_space(3))) void* est_lds_ptr;
+typedef __attribute__((address_space(1))) const void* est_gbl_ptr;
+
+__device__ inline int est_swz(int r) { return (r >> 1) & 7; }
+constexpr int kEstWaitLgkm = 0xC07F;   // lgkmcnt(0) only
+
+template <sdq_dtype XT, int B>
+__global__ __launch_bounds__(256, 1) void expand_prefill_estat_kernel(
+    const void* __restrict__ x, const float* __restrict__ fac, int64_t m, int64_t k, int m_up,
+    int64_t k_up, int64_t k_up_pad, int64_t nb, int n_ss, int64_t ipg, int64_t n_items,
+    const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo, _Float16* __restrict__ xt_out) {
+  constexpr int G = B / 8;            // 16-byte groups per x row
+  constexpr int KS = B / 16;          // 16-deep k steps
+  constexpr int TILE = 128 * B;       // halves per x tile
+  constexpr int RPC = 64 / G;         // rows per 1 KB copy
+  constexpr int FC = 32 / RPC;        // copies per wave per tile (a wave fills 32 rows)
+  constexpr bool BF = XT == SDQ_BF16;
+  typedef typename std::conditional<BF, bf16x8, half8>::type frag8;
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * TILE + 2 * 2 * 128];
+  float* const pvb = reinterpret_cast<float*>(lds + 2 * TILE);   // [2][128] row factors
+  const int tid = threadIdx.x, lane = tid % 64;
+  const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
+  const int id = blockIdx.x, xcd = id % kXcds, jx = id / kXcds;
+  const int s = jx % n_ss;
+  const int64_t g = static_cast<int64_t>(jx / n_ss) * kXcds + xcd;
+  const int64_t it_begin = g * ipg, it_end = min<int64_t>(n_items, it_begin + ipg);
+  if (it_begin >= it_end) return;
+  const int64_t n_rt = (m + 127) / 128;
+  (void)n_rt;
+  // E^T fragments of this lane's sample, k = 16 ks + 8 (lane / 32) .. + 7.
+  const int col = 128 * s + 32 * wave + lane % 32;
+  const bool cok = col < m_up;
+  frag8 eh[KS], el[KS];
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    const int64_t off = static_cast<int64_t>(cok ? col : 0) * B + 16 * ks + 8 * (lane / 32);
+    uint4 h = *reinterpret_cast<const uint4*>(et_hi + off);
+    uint4 l = *reinterpret_cast<const uint4*>(et_lo + off);
+    if (!cok) h = l = make_uint4(0u, 0u, 0u, 0u);
+    const half8 hh = __builtin_bit_cast(half8, h), ll = __builtin_bit_cast(half8, l);
+    if constexpr (BF) {
+#pragma unroll
+      for (int q = 0; q < 8; ++q) {
+        const float e = static_cast<float>(hh[q]) + static_cast<float>(ll[q]);
+        const __bf16 bh = static_cast<__bf16>(e);
+        eh[ks][q] = bh;
+        el[ks][q] = static_cast<__bf16>(e - static_cast<float>(bh));
+      }
+    } else {
+      eh[ks] = hh;
+      el[ks] = ll;
+    }
+  }
+  const uint16_t* __restrict__ xg = static_cast<const uint16_t*>(x);
+  // Copy of item `item`'s x tile and row factors into buffer `buf`: copy j of
+  // wave w writes rows 32 w + RPC j .. (lane l: row + l / G, slot l % G, which
+  // holds group (l % G) ^ swz(row)); rows past m read row m - 1.
+  auto fill = [&](int buf, int64_t item) {
+    const int64_t rt = item / nb, b = item % nb;
+    const int64_t i0 = rt * 128;
+#pragma unroll
+    for (int j = 0; j < FC; ++j) {
+      const int r = 32 * wave + RPC * j + lane / G;
+      const int64_t row = min<int64_t>(i0 + r, m - 1);
+      const uint16_t* src = xg + row * k + b * B + 8 * ((lane % G) ^ est_swz(r));
+      __builtin_amdgcn_global_load_lds((est_gbl_ptr)src, (est_lds_ptr)(lds + buf * TILE + (32 * wave + RPC * j) * B),
+                                       16, 0, 0);
+    }
+    if (wave < 2) {
+      const float* src = fac + min<int64_t>(i0 + 64 * wave + lane, m - 1);
+      __builtin_amdgcn_global_load_lds((est_gbl_ptr)src, (est_lds_ptr)(pvb + buf * 128 + 64 * wave), 4, 0, 0);
+    }
+  };
+  // Pipeline: buffer cur holds item it (landed), buffer cur ^ 1 item it + 1
+  // (copies in flight).  After item it's products every wave waits for all of
+  // its own vm operations (the next item's copies, issued an item ago, and
+  // the previous item's stores), and the barrier makes that hold for all.
+  fill(0, it_begin);
+  fill(1, min<int64_t>(it_begin + 1, it_end - 1));
+  __builtin_amdgcn_s_waitcnt(0);
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+  for (int64_t it = it_begin; it < it_end; ++it) {
+    const int cur = static_cast<int>((it - it_begin) & 1);
+    const int64_t rt = it / nb, b = it % nb;
+    const int64_t i0 = rt * 128;
+    const uint16_t* abuf = lds + cur * TILE;
+    floatx16 acc[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[r][v] = 0.0f;
+#pragma unroll
+    for (int ks = 0; ks < KS; ++ks) {
+      const int gk = 2 * ks + lane / 32;
+#pragma unroll
+      for (int r = 0; r < 4; ++r) {
+        const int row = 32 * r + lane % 32;
+        const frag8 a = *reinterpret_cast<const frag8*>(abuf + row * B + 8 * (gk ^ est_swz(row)));
+        if constexpr (BF) {
+          acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(eh[ks], a, acc[r], 0, 0, 0);
+          acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(el[ks], a, acc[r], 0, 0, 0);
+        } else {
+          acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_f16(eh[ks], a, acc[r], 0, 0, 0);
+          acc[r] = __builtin_amdgcn_mfma_f32_32x32x16_f16(el[ks], a, acc[r], 0, 0, 0);
+        }
+      }
+    }
+    // item it + 1 has landed, every wave is done with buffer cur's tile and
+    // the previous item's stores have drained
+    __builtin_amdgcn_s_waitcnt(0);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    // this lane's rows: 32 r + lane % 32 (factors read before the refill)
+    float pr[4];
+#pragma unroll
+    for (int r = 0; r < 4; ++r) pr[r] = pvb[cur * 128 + 32 * r + lane % 32];
+    __builtin_amdgcn_s_waitcnt(kEstWaitLgkm);
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    fill(cur, min<int64_t>(it + 2, it_end - 1));
+    if (b == 0 && s == 0) {
+      // zero the padding columns of these rows (written by nobody else)
+      const int64_t pad = k_up_pad - k_up;
+      for (int64_t idx = tid; idx < 128 * pad; idx += 256) {
+        const int64_t i = i0 + idx / pad;
+        if (i < m) xt_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
+      }
+    }
+    // acc[r][v] = x_tilde of row i0 + 32 r + lane % 32, sample
+    // 128 s + 32 w + 8 (v / 4) + 4 (lane / 32) + v % 4: four consecutive
+    // samples per 8-byte store
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int64_t i = i0 + 32 * r + lane % 32;
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        const int c = 128 * s + 32 * wave + 8 * q + 4 * (lane / 32);
+        typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+        half4 h;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) h[u] = static_cast<_Float16>(acc[r][4 * q + u] * pr[r]);
+        if (i < m && c < m_up) *reinterpret_cast<half4*>(xt_out + i * k_up_pad + b * m_up + c) = h;
+      }
+    }
+  }
+  // the last copies (never read) land before the workgroup's LDS is released
+  __builtin_amdgcn_s_waitcnt(0);
+}
+
 }  // namespace
 
 // Without Had the row scales follow the weights' outliers and the layer
@@ -303,6 +475,34 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
                       ? reinterpret_cast<_Float16*>(static_cast<char*>(ws) +
                                                     align_up(static_cast<size_t>(m) * k_up_pad * 2, 256))
                       : nullptr;
+  // fp16 / bf16 activations, B = 128 or 256, one fp16 x_tilde: the
+  // E-stationary kernel (SDQ_PREFILL_EXPAND=tiled keeps the tiled one, a
+  // tuning aid).  Workgroups: one per compute unit, spread over the 128-sample
+  // slices of M; each walks an even share of the (row tile, block) items.
+  static const char* env = std::getenv("SDQ_PREFILL_EXPAND");
+  const bool tiled_forced = env && std::string(env) == "tiled";
+  if (!tiled_forced && xt != SDQ_F32 && !xlo && (L->block == 128 || L->block == 256)) {
+    const int n_ss = (L->m_up + 127) / 128;
+    const int64_t n_items = ((m + 127) / 128) * L->nb;
+    const int64_t cus = device_compute_units();
+    const int64_t groups = ((cus + n_ss - 1) / n_ss + kXcds - 1) / kXcds * kXcds;
+    const int64_t ipg = (n_items + groups - 1) / groups;
+    const dim3 egrid(static_cast<unsigned>(n_ss * groups));
+#define SDQ_EST(XT, BB)                                                                          \
+  expand_prefill_estat_kernel<XT, BB><<<egrid, dim3(256), 0, stream>>>(                           \
+      x, fac, m, L->k, L->m_up, L->k_up, k_up_pad, L->nb, n_ss, ipg, n_items, T->et_hi, T->et_lo, xbuf)
+    if (xt == SDQ_BF16) {
+      if (L->block == 256) SDQ_EST(SDQ_BF16, 256);
+      else SDQ_EST(SDQ_BF16, 128);
+    } else {
+      if (L->block == 256) SDQ_EST(SDQ_F16, 256);
+      else SDQ_EST(SDQ_F16, 128);
+    }
+#undef SDQ_EST
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return hip_error(e, "prefill expansion launch");
+    return SDQ_OK;
+  }
   // Sample tiles fastest: neighbouring workgroups share the x tile.  B is a
   // multiple of the 64-wide t step for every supported block.
   constexpr int tm = 128;

@@ -287,18 +287,6 @@ __global__ __launch_bounds__(64 * W, 1) void gemm_prefill_kernel(
   }
 }
 
-// Compute units of the current device (cached per device).
-int64_t compute_units() {
-  static int64_t cached[64] = {};
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
-  if (cached[dev] == 0) {
-    int v = 0;
-    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
-    cached[dev] = v;
-  }
-  return cached[dev];
-}
 
 }  // namespace
 
@@ -324,7 +312,7 @@ sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, 
   // chunks of at most 2^31 elements.
   const int64_t rows_max = std::max<int64_t>(kBM, ((int64_t{1} << 31) / k_up_pad) / kBM * kBM);
   const int passes = prefill_split(L) ? 2 : 1;   // x_tilde hi, then lo added on
-  const int64_t cus = compute_units();
+  const int64_t cus = device_compute_units();
   // Eight waves (two per SIMD, so one wave's LDS and memory waits overlap the
   // other's MFMAs) by default: measured 431 against 437-445 us on 8192x8192 and
   // 1489 against 1540-1548 us on 28672x8192 at m = 2048, equal on 8192x28672.
@@ -376,6 +364,19 @@ sdq_status launch_prefill_contract(int64_t m, LinearSet S, const sdq_layout* L, 
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return hip_error(e, "prefill GEMM launch");
   return SDQ_OK;
+}
+
+// Compute units of the current device (cached per device).
+int64_t device_compute_units() {
+  static int64_t cached[64] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cached[dev] == 0) {
+    int v = 0;
+    if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || v <= 0) v = 256;
+    cached[dev] = v;
+  }
+  return cached[dev];
 }
 
 }  // namespace sdq

@@ -130,6 +130,9 @@ inline int64_t set_panels(const LinearSet& S) {
   return p;
 }
 
+// Compute units of the current device (cached per device; 256 if unknown).
+int64_t device_compute_units();
+
 // Decode path (m <= 16): expansion (fp32 x_tilde) then LUT GEMV.
 size_t decode_ws_bytes(const sdq_layout* L, int64_t m);
 sdq_status decode_supported(const sdq_layout* L);
