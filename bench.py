@@ -733,7 +733,7 @@ def traffic_probe(torch, P, synth, SG) -> None:
     of known size (to scale FETCH_SIZE / WRITE_SIZE), then the contraction
     launches of one token step through the LLaMA-70B stack (m = 1, expansions
     once before), the same at m = 8, the LLaMA-7B down_proj GEMV and the
-    LLaMA-70B prefill GEMMs.
+    LLaMA-70B prefill GEMMs, and the 28672x8192 layer with base-3 codes at m = 8.
     Prints what it ran and the code bytes of the stack's launches."""
     nbytes = 256 << 20
     a = torch.ones(nbytes, dtype=torch.uint8, device="cuda")
@@ -759,14 +759,16 @@ def traffic_probe(torch, P, synth, SG) -> None:
     print(f"stack m=8 contraction: {len(fns)} launches, code bytes {run.code_bytes}", flush=True)
     del run, fns, ws, encs
     torch.cuda.empty_cache()
-    for wl_i, lin_i, m, xdt, label in ((2, 0, 1, torch.float16, "down_proj 4096x11008 m=1"),
-                                       (4, 0, 2048, torch.bfloat16, "70B 8192x8192 m=2048"),
-                                       (4, 1, 2048, torch.bfloat16, "70B 28672x8192 m=2048"),
-                                       (4, 2, 2048, torch.bfloat16, "70B 8192x28672 m=2048")):
+    for wl_i, lin_i, m, xdt, pack, label in (
+            (2, 0, 1, torch.float16, P.SDQ_PACK_FIELDS, "down_proj 4096x11008 m=1"),
+            (4, 0, 2048, torch.bfloat16, P.SDQ_PACK_FIELDS, "70B 8192x8192 m=2048"),
+            (4, 1, 2048, torch.bfloat16, P.SDQ_PACK_FIELDS, "70B 28672x8192 m=2048"),
+            (4, 2, 2048, torch.bfloat16, P.SDQ_PACK_FIELDS, "70B 8192x28672 m=2048"),
+            (4, 1, 8, torch.float16, P.SDQ_PACK_BASE3, "70B 28672x8192 m=8 base-3")):
         wl = synth.workload(wl_i)
         lin = wl.linears[lin_i]
         w = SG.weight_rows_gpu(wl.seed, lin.linear_id, lin.n, lin.k, lin.sigma, wl.outliers)
-        enc = P.quantize(w, wl.osr, wl.levels)
+        enc = P.quantize(w, wl.osr, wl.levels, packing=pack)
         del w
         L = enc.layout
         x = SG.activations_gpu(wl.seed, 5, m, lin.k).to(xdt)

@@ -44,6 +44,16 @@ constexpr int kGemvWaves = 4;
 constexpr int kGroupsPerChunk = 32; // 128 bits / 4
 constexpr int64_t kExpRowPairs = 1024; // one-row expansion: two blocks per workgroup from here
 
+// A 16-byte load of packed codes, marked non-temporal: each code byte is read
+// once per call, and the streaming hint keeps the code stream from evicting
+// the expansion tables and x_tilde from L2 (measured on MI355X: the 70B stack
+// at m = 1 9.94 -> 9.47 ms per token, at m = 8 16.08 -> 15.55 ms).
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+__device__ inline uint4 load_code_chunk(const uint4* p) {
+  const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+
 __device__ inline float load_x(const void* x, sdq_dtype xt, int64_t idx) {
   if (xt == SDQ_F16) return __half2float(static_cast<const __half*>(x)[idx]);
   if (xt == SDQ_BF16) return __bfloat162float(static_cast<const __hip_bfloat16*>(x)[idx]);
@@ -560,7 +570,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
         // reach hold zero planes; their code loads stay inside the layer.
         const bool live = c0 + j < cpb;
         const int jj = min(c0 + j, cpb - 1);
-        q[j] = cbase[min<int64_t>(c_first + jj, n_chunks - 1) * kPanel];
+        q[j] = load_code_chunk(&cbase[min<int64_t>(c_first + jj, n_chunks - 1) * kPanel]);
         const int64_t slot = b * cpb + jj;
 #pragma unroll
         for (int s = 0; s < SPC; ++s)
@@ -693,7 +703,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_lds_kernel(
     for (int c0 = 0; c0 < cpb; c0 += CH) {
       uint4 q[CH];
 #pragma unroll
-      for (int j = 0; j < CH; ++j) q[j] = cpanel[min<int64_t>(c_first + c0 + j, n_chunks - 1) * kPanel + lane];
+      for (int j = 0; j < CH; ++j) q[j] = load_code_chunk(&cpanel[min<int64_t>(c_first + c0 + j, n_chunks - 1) * kPanel + lane]);
 #pragma unroll
       for (int j = 0; j < CH; ++j) {
         uint32_t r0 = q[j].x, r1 = q[j].y, r2 = q[j].z, r3 = q[j].w;
@@ -830,7 +840,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_b3_kernel(
       uint4 av[kB3Steps][NPG];
 #pragma unroll
       for (int jj = 0; jj < kB3Group; ++jj)
-        q[jj] = cpanel[min<int64_t>(c_first + G * kB3Group + jj, n_chunks - 1) * kPanel + lane];
+        q[jj] = load_code_chunk(&cpanel[min<int64_t>(c_first + G * kB3Group + jj, n_chunks - 1) * kPanel + lane]);
 #pragma unroll
       for (int st = 0; st < kB3Steps; ++st)
 #pragma unroll
@@ -1031,7 +1041,7 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_kernel(
   {
     const uint4* src = codes + ((panel_ok ? panel : n_panels - 1) * n_chunks + c0) * kPanel + lane;
 #pragma unroll
-    for (int j = 0; j < SEG; ++j) q[j] = src[static_cast<int64_t>(min(j, nch - 1)) * kPanel];
+    for (int j = 0; j < SEG; ++j) q[j] = load_code_chunk(&src[static_cast<int64_t>(min(j, nch - 1)) * kPanel]);
   }
   __builtin_amdgcn_sched_barrier(0);
 
@@ -1163,7 +1173,7 @@ __global__ __launch_bounds__(64 * kGemvWaves) void gemv_lut_base3_kernel(
   {
     const uint4* src = codes + ((panel_ok ? panel : n_panels - 1) * n_chunks + c0) * kPanel + lane;
 #pragma unroll
-    for (int j = 0; j < SEG; ++j) q[j] = src[static_cast<int64_t>(min(j, nch - 1)) * kPanel];
+    for (int j = 0; j < SEG; ++j) q[j] = load_code_chunk(&src[static_cast<int64_t>(min(j, nch - 1)) * kPanel]);
   }
   __builtin_amdgcn_sched_barrier(0);
 
