@@ -14,8 +14,9 @@
 //            4-bit group of codes (4 binary codes or 2 ternary codes), and each
 //            lane adds one table entry per 4 bits.
 // Two to sixteen rows (integer matrix cores):
-//   expand   the same x_tilde, quantised per (row, block) to 24-bit fixed
-//            point and written as three signed-byte planes;
+//   expand   the same x_tilde (for fp16 and bf16 x on the matrix cores, with
+//            E as an fp16 pair hi + lo), quantised per (row, block) to
+//            24-bit fixed point and written as three signed-byte planes;
 //   gemv     codes expanded to int8 {-1, 0, +1} by a byte permute and
 //            contracted against the planes with v_mfma_i32_16x16x64_i8 (exact
 //            int32 sums), dequantised per block.  The cost barely grows with
@@ -261,6 +262,139 @@ __device__ inline float wave_max_nonneg(float v) {
   return __int_as_float(__builtin_amdgcn_readlane(x, 63));
 }
 
+// The plane words of one workgroup's 64 code positions (2-bit fields):
+// chunk slot `slot`, and (binary) half `half` of the chunk, from the
+// quantised samples qv[row][position] of all m rows (rows >= m and plane 3
+// zero); 256 * npg dwords, every thread of the workgroup taking a share.
+template <int LEVELS>
+__device__ inline void store_planes(const int (*qv)[64], int m, int npg, int64_t slot, int half,
+                                    uint32_t* __restrict__ planes) {
+  for (int idx = threadIdx.x; idx < 256 * npg; idx += kExpThreads) {
+    const int di = idx % 4;
+    const int p = (idx / 4) % 16;
+    int s, kg, pg;
+    if (LEVELS == 2) {          // kg in {2 half, 2 half + 1}, both steps of the chunk
+      kg = 2 * half + (idx / 64) % 2;
+      pg = (idx / 128) % npg;
+      s = idx / (128 * npg);
+    } else {                    // all four kg, the chunk's one step
+      kg = (idx / 64) % 4;
+      pg = idx / 256;
+      s = 0;
+    }
+    const int a = pg * 4 + p / 4;
+    const int t = p % 4;
+    uint32_t word = 0;
+    if (a < m && t < 3) {
+#pragma unroll
+      for (int beta = 0; beta < 4; ++beta)
+        word |= plane_byte(qv[a][chunk_code<LEVELS>(s, kg, di, beta) - 64 * half], t) << (8 * beta);
+    }
+    const int64_t step = LEVELS == 2 ? 2 * slot + s : slot;
+    planes[((step * npg + pg) * 64 + kg * 16 + p) * 4 + di] = word;
+  }
+}
+
+typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
+typedef float float4_t __attribute__((ext_vector_type(4)));
+
+// Matrix-core front end of the plane expansions for fp16 and bf16
+// activations: the quantised x_tilde of code positions g0 + [0, 64) of block
+// b for all rows, into qv[row][position] (zero outside the block), and (when
+// write_sx) the block's plane scales.  Wave w takes positions 16 w + [0, 16):
+// x_b (rows as the A operand, zero past m) times the columns of E as the
+// fp16 pair hi + lo of the transposed tables (the B operand), 2 B / 32
+// v_mfma_f32_16x16x32_f16 with fp32 accumulation.  bf16 x is scaled per
+// (row, block) by a power of two that brings its max into [2^14, 2^15), so it
+// converts to fp16 exactly (values below 2^-24 of the max round); the scale
+// cancels in the quantisation, whose bound max |x_b| * e1max is the fp32
+// path's.  E hi + lo carries ~22 bits, against 24 for the fixed point.
+template <int B, bool BF16>
+__device__ inline void planes_qv_mfma(const uint16_t* __restrict__ x, int m, int k32, int64_t b,
+                                      int64_t g0, int m_up, int64_t nb, bool write_sx,
+                                      const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo,
+                                      float e1max, float* __restrict__ sx, int (*qv)[64]) {
+  constexpr int S = B / 32;                  // k-steps of 32 samples of t
+  const int lane = threadIdx.x % 64;
+  const int w = threadIdx.x / 64;
+  const int r = lane % 16, grp = lane / 16;  // operand row / column, k group
+  const int pos = 16 * w + r;                // this lane's B column: code position
+  const int o = static_cast<int>(g0 + pos - b * m_up);
+  const bool in_block = o >= 0 && o < m_up;
+  // Loads from clamped (in-bounds) addresses, zeroed by selects.
+  const uint4* __restrict__ xp =
+      reinterpret_cast<const uint4*>(x + static_cast<int64_t>(min(r, m - 1)) * k32 + b * B) + grp;
+  const uint4* __restrict__ hp = reinterpret_cast<const uint4*>(et_hi + static_cast<int64_t>(in_block ? o : 0) * B) + grp;
+  const uint4* __restrict__ lp = reinterpret_cast<const uint4*>(et_lo + static_cast<int64_t>(in_block ? o : 0) * B) + grp;
+  uint4 xq[S], eh[S], el[S];
+#pragma unroll
+  for (int st = 0; st < S; ++st) xq[st] = xp[4 * st];
+#pragma unroll
+  for (int st = 0; st < S; ++st) eh[st] = hp[4 * st];
+#pragma unroll
+  for (int st = 0; st < S; ++st) el[st] = lp[4 * st];
+  // max |x| of row r over the lane's 8 S samples, then over the four k groups
+  float mx = 0.0f;
+#pragma unroll
+  for (int st = 0; st < S; ++st) {
+    const uint32_t wv[4] = {xq[st].x, xq[st].y, xq[st].z, xq[st].w};
+#pragma unroll
+    for (int j = 0; j < 4; ++j) {
+      const float lo = BF16 ? __uint_as_float(wv[j] << 16) : __half2float(__ushort_as_half(static_cast<unsigned short>(wv[j])));
+      const float hi = BF16 ? __uint_as_float(wv[j] & 0xFFFF0000u)
+                            : __half2float(__ushort_as_half(static_cast<unsigned short>(wv[j] >> 16)));
+      mx = fmaxf(mx, fmaxf(fabsf(lo), fabsf(hi)));
+    }
+  }
+  mx = fmaxf(mx, __shfl_xor(mx, 16));
+  mx = fmaxf(mx, __shfl_xor(mx, 32));
+  if (r >= m) mx = 0.0f;
+  int ex = 0;
+  (void)frexpf(mx, &ex);                     // mx < 2^ex
+  const int sh = mx > 0.0f ? 15 - ex : 0;    // bf16 scale 2^sh
+  float4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+#pragma unroll
+  for (int st = 0; st < S; ++st) {
+    half8_t a;
+    if constexpr (BF16) {
+      const uint32_t wv[4] = {xq[st].x, xq[st].y, xq[st].z, xq[st].w};
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        a[2 * j] = static_cast<_Float16>(ldexpf(__uint_as_float(wv[j] << 16), sh));
+        a[2 * j + 1] = static_cast<_Float16>(ldexpf(__uint_as_float(wv[j] & 0xFFFF0000u), sh));
+      }
+    } else {
+      a = *reinterpret_cast<const half8_t*>(&xq[st]);
+    }
+    if (r >= m) a = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+    half8_t h = *reinterpret_cast<const half8_t*>(&eh[st]);
+    half8_t l = *reinterpret_cast<const half8_t*>(&el[st]);
+    if (!in_block) {
+      h = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      l = h;
+    }
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, h, acc, 0, 0, 0);
+    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, l, acc, 0, 0, 0);
+  }
+  // Output v of this lane: row a = 4 grp + v, position pos.  The row's max
+  // sits in lane a (lane a holds row a % 16 = a).
+#pragma unroll
+  for (int v = 0; v < 4; ++v) {
+    const int a = 4 * grp + v;
+    const float mxa = __shfl(mx, a);
+    const float bound = mxa * e1max;
+    int q = 0;
+    if (bound > 0.0f && in_block) {
+      int exa = 0;
+      (void)frexpf(mxa, &exa);
+      const float sc = BF16 ? ldexpf(bound, 15 - exa) : bound;   // the bound in acc's scale
+      q = __float2int_rn(acc[v] * (kQ / sc));
+    }
+    qv[a][pos] = q;
+  }
+  if (write_sx && w == 0 && grp == 0 && r < m) sx[static_cast<int64_t>(r) * nb + b] = mx * e1max / kQ;
+}
+
 // One workgroup: one 64-code segment u of block b's chunk slots (code
 // positions floor(b M / chunk) * chunk + 64 u + [0, 64)), all m rows; the
 // samples of block b among them by the fp32 expansion, the rest zero; then
@@ -358,33 +492,8 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
     if (blockIdx.x == 0 && l == 0) sx[static_cast<int64_t>(i) * nb + b] = bound / kQ;
   }
   __syncthreads();
-  // Chunk slot of these 64 codes, and (binary) which half of the chunk they are.
-  const int64_t slot = b * cpb + static_cast<int64_t>(blockIdx.x) / (kCpc / 64);
-  const int half = static_cast<int>(blockIdx.x % (kCpc / 64));
-  for (int idx = tid; idx < 256 * npg; idx += kExpThreads) {
-    const int di = idx % 4;
-    const int p = (idx / 4) % 16;
-    int s, kg, pg;
-    if (LEVELS == 2) {          // kg in {2 half, 2 half + 1}, both steps of the chunk
-      kg = 2 * half + (idx / 64) % 2;
-      pg = (idx / 128) % npg;
-      s = idx / (128 * npg);
-    } else {                    // all four kg, the chunk's one step
-      kg = (idx / 64) % 4;
-      pg = idx / 256;
-      s = 0;
-    }
-    const int a = pg * 4 + p / 4;
-    const int t = p % 4;
-    uint32_t word = 0;
-    if (a < m && t < 3) {
-#pragma unroll
-      for (int beta = 0; beta < 4; ++beta)
-        word |= plane_byte(qv[a][chunk_code<LEVELS>(s, kg, di, beta) - 64 * half], t) << (8 * beta);
-    }
-    const int64_t step = LEVELS == 2 ? 2 * slot + s : slot;
-    planes[((step * npg + pg) * 64 + kg * 16 + p) * 4 + di] = word;
-  }
+  store_planes<LEVELS>(qv, m, npg, b * cpb + static_cast<int64_t>(blockIdx.x) / (kCpc / 64),
+                       static_cast<int>(blockIdx.x % (kCpc / 64)), planes);
 }
 
 // Base-3 codes on the integer-MFMA path (read as stored, no unpack pass).
@@ -399,6 +508,26 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
 // the 2-bit codes.
 constexpr int kB3Group = 4;    // slots per group of steps
 constexpr int kB3Steps = 5;    // k-steps per group
+
+// The plane bytes of one workgroup's 64 base-3 code positions g0 + [0, 64)
+// of block b (whose first chunk is c_first) in the digit order, from
+// qv[row][position]: entry idx = position (fastest), MFMA row p, plane group.
+__device__ inline void store_planes_b3(const int (*qv)[64], int m, int npg, int64_t b, int64_t g0, int64_t c_first,
+                                       int steps3, uint8_t* __restrict__ planes) {
+  for (int idx = threadIdx.x; idx < 64 * 16 * npg; idx += kExpThreads) {
+    const int l = idx % 64, p = (idx / 64) % 16, pg = idx / 1024;
+    const int64_t g = g0 + l;
+    const int j = static_cast<int>(g / kBase3PerChunk - c_first);
+    const int pos = static_cast<int>(g % kBase3PerChunk);
+    const int byte = pos / 5, digit = pos % 5;
+    const int kg = byte / 4, beta = byte % 4;
+    const int step = (j / kB3Group) * kB3Steps + (digit < 4 ? j % kB3Group : 4);
+    const int di = digit < 4 ? digit : j % kB3Group;
+    const int a = pg * 4 + p / 4, t = p % 4;
+    const uint32_t val = a < m && t < 3 ? plane_byte(qv[a][l], t) : 0u;
+    planes[((((b * steps3 + step) * npg + pg) * 64 + kg * 16 + p) * 16) + 4 * di + beta] = static_cast<uint8_t>(val);
+  }
+}
 
 // One workgroup: 64 consecutive code positions of block b's slots (segment u
 // of the block's 5 * groups segments), all m rows: the same fp32 expansion
@@ -492,20 +621,46 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_b3_kernel(
     if (blockIdx.x == 0 && l == 0) sx[static_cast<int64_t>(i) * nb + b] = bound / kQ;
   }
   __syncthreads();
-  // Plane bytes: entry idx = code l of the segment (fastest), MFMA row p, plane group pg.
-  for (int idx = tid; idx < 64 * 16 * npg; idx += kExpThreads) {
-    const int l = idx % 64, p = (idx / 64) % 16, pg = idx / 1024;
-    const int64_t g = g0 + l;
-    const int j = static_cast<int>(g / kBase3PerChunk - c_first);
-    const int pos = static_cast<int>(g % kBase3PerChunk);
-    const int byte = pos / 5, digit = pos % 5;
-    const int kg = byte / 4, beta = byte % 4;
-    const int step = (j / kB3Group) * kB3Steps + (digit < 4 ? j % kB3Group : 4);
-    const int di = digit < 4 ? digit : j % kB3Group;
-    const int a = pg * 4 + p / 4, t = p % 4;
-    const uint32_t val = a < m && t < 3 ? plane_byte(qv[a][l], t) : 0u;
-    planes[((((b * steps3 + step) * npg + pg) * 64 + kg * 16 + p) * 16) + 4 * di + beta] = static_cast<uint8_t>(val);
-  }
+  store_planes_b3(qv, m, npg, b, g0, c_first, steps3, planes);
+}
+
+// The plane expansions for fp16 and bf16 activations (the same grids, plane
+// layouts and side duties as expand_planes_kernel / expand_planes_b3_kernel),
+// with the dot products on the matrix cores (planes_qv_mfma).
+template <int B, int LEVELS, bool BF16>
+__global__ __launch_bounds__(kExpThreads) void expand_planes_mfma_kernel(
+    const void* __restrict__ x, int m, int npg, int64_t k, int64_t nb, int m_up, int cpb,
+    const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo, float e1max,
+    uint32_t* __restrict__ planes, float* __restrict__ sx, LinearSet zero) {
+  __shared__ int qv[kMaxDecodeRows][64];
+  constexpr int kCpc = LEVELS == 2 ? 128 : 64;
+  const int64_t b = blockIdx.y;
+  const int64_t c_first = b * m_up / kCpc;
+  const int64_t g0 = c_first * kCpc + static_cast<int64_t>(blockIdx.x) * 64;
+  planes_qv_mfma<B, BF16>(static_cast<const uint16_t*>(x), m, static_cast<int>(k), b, g0, m_up, nb,
+                    blockIdx.x == 0, et_hi, et_lo, e1max, sx, qv);
+  const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  zero_outputs(zero, m, wg, static_cast<int64_t>(gridDim.x) * gridDim.y, threadIdx.x);
+  __syncthreads();
+  store_planes<LEVELS>(qv, m, npg, b * cpb + static_cast<int64_t>(blockIdx.x) / (kCpc / 64),
+                       static_cast<int>(blockIdx.x % (kCpc / 64)), planes);
+}
+
+template <int B, bool BF16>
+__global__ __launch_bounds__(kExpThreads) void expand_planes_b3_mfma_kernel(
+    const void* __restrict__ x, int m, int npg, int64_t k, int64_t nb, int m_up, int steps3,
+    const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo, float e1max,
+    uint8_t* __restrict__ planes, float* __restrict__ sx, LinearSet zero) {
+  __shared__ int qv[kMaxDecodeRows][64];
+  const int64_t b = blockIdx.y;
+  const int64_t c_first = b * m_up / kBase3PerChunk;
+  const int64_t g0 = c_first * kBase3PerChunk + static_cast<int64_t>(blockIdx.x) * 64;
+  planes_qv_mfma<B, BF16>(static_cast<const uint16_t*>(x), m, static_cast<int>(k), b, g0, m_up, nb,
+                    blockIdx.x == 0, et_hi, et_lo, e1max, sx, qv);
+  const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
+  zero_outputs(zero, m, wg, static_cast<int64_t>(gridDim.x) * gridDim.y, threadIdx.x);
+  __syncthreads();
+  store_planes_b3(qv, m, npg, b, g0, c_first, steps3, planes);
 }
 
 // One workgroup: one 64-row panel and 4 * bpw consecutive blocks, wave w
@@ -1528,14 +1683,29 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   const LinearSet z = zero ? *zero : LinearSet{};
   const dim3 egrid(static_cast<unsigned>(T->m_pad / 64), static_cast<unsigned>(L->nb));
+  // Plane expansions: the matrix-core front end for fp16 and bf16 x (the fp32
+  // VALU one for fp32 x).  Measured on MI355X: the 70B stack at m = 8 (fp16 x)
+  // 15.56 -> 15.05 ms per token.  SDQ_PLANES_MFMA=0 forces the VALU kernels
+  // (a test aid, read on every launch).
+  const char* pm_env = std::getenv("SDQ_PLANES_MFMA");
+  const bool planes_mfma = xt != SDQ_F32 && !(pm_env && std::atoi(pm_env) == 0);
   if (mfma_base3(L, m)) {
     const int steps3 = mfma_steps3(L);
     const dim3 pgrid(static_cast<unsigned>(steps3), static_cast<unsigned>(L->nb));
 #define SDQ_PLANES3(BB)                                                                          \
-  expand_planes_b3_kernel<BB><<<pgrid, dim3(kExpThreads), 0, stream>>>(                          \
-      x, xt, static_cast<int>(m), npg_for(m), L->k, L->nb, L->m_up, T->m_pad, steps3,            \
-      reinterpret_cast<const float4*>(T->edec), T->e1max, reinterpret_cast<uint8_t*>(w.planes),  \
-      w.sx, z)
+  if (planes_mfma && xt == SDQ_BF16)                                                             \
+    expand_planes_b3_mfma_kernel<BB, true><<<pgrid, dim3(kExpThreads), 0, stream>>>(             \
+        x, static_cast<int>(m), npg_for(m), L->k, L->nb, L->m_up, steps3, T->et_hi, T->et_lo,      \
+        T->e1max, reinterpret_cast<uint8_t*>(w.planes), w.sx, z);                                \
+  else if (planes_mfma)                                                                          \
+    expand_planes_b3_mfma_kernel<BB, false><<<pgrid, dim3(kExpThreads), 0, stream>>>(            \
+        x, static_cast<int>(m), npg_for(m), L->k, L->nb, L->m_up, steps3, T->et_hi, T->et_lo,      \
+        T->e1max, reinterpret_cast<uint8_t*>(w.planes), w.sx, z);                                \
+  else                                                                                           \
+    expand_planes_b3_kernel<BB><<<pgrid, dim3(kExpThreads), 0, stream>>>(                        \
+        x, xt, static_cast<int>(m), npg_for(m), L->k, L->nb, L->m_up, T->m_pad, steps3,          \
+        reinterpret_cast<const float4*>(T->edec), T->e1max, reinterpret_cast<uint8_t*>(w.planes),\
+        w.sx, z)
     switch (B) {
       case 64: SDQ_PLANES3(64); break;
       case 128: SDQ_PLANES3(128); break;
@@ -1551,9 +1721,18 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
     const int cpb = mfma_cpb(L);
     const dim3 pgrid(static_cast<unsigned>(cpb * (L->levels == 2 ? 2 : 1)), static_cast<unsigned>(L->nb));
 #define SDQ_PLANES(BB, LV)                                                                       \
-  expand_planes_kernel<BB, LV><<<pgrid, dim3(kExpThreads), 0, stream>>>(                         \
-      x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad, cpb,                      \
-      reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, z)
+  if (planes_mfma && xt == SDQ_BF16)                                                             \
+    expand_planes_mfma_kernel<BB, LV, true><<<pgrid, dim3(kExpThreads), 0, stream>>>(            \
+        x, static_cast<int>(m), npg, L->k, L->nb, L->m_up, cpb, T->et_hi, T->et_lo, T->e1max,      \
+        w.planes, w.sx, z);                                                                      \
+  else if (planes_mfma)                                                                          \
+    expand_planes_mfma_kernel<BB, LV, false><<<pgrid, dim3(kExpThreads), 0, stream>>>(           \
+        x, static_cast<int>(m), npg, L->k, L->nb, L->m_up, cpb, T->et_hi, T->et_lo, T->e1max,      \
+        w.planes, w.sx, z);                                                                      \
+  else                                                                                           \
+    expand_planes_kernel<BB, LV><<<pgrid, dim3(kExpThreads), 0, stream>>>(                       \
+        x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad, cpb,                    \
+        reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, z)
     if (L->levels == 2) {
       switch (B) {
         case 64: SDQ_PLANES(64, 2); break;
