@@ -62,10 +62,10 @@ POOL_MAX = 16                    # oracle workers: the host share of one GPU
 # were taken with: a source whose hash differs reports traffic null.
 TRAFFIC_FETCH_SCALE = 1.999749
 TRAFFIC_WRITE_SCALE = 1.000000
-TRAFFIC_SOURCES = {"linear_decode.hip": "f9239b8fc81e9131d00d6a29cfc24d514e00d0ff35d6c4c4b7c27d3d33f29c92"}
+TRAFFIC_SOURCES = {"linear_decode.hip": "c7dc13d0288a24b9228e67eca35e58d49c8b00ba1446bcd92e190ca11fc3b9a6"}
 # kernel family -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB) per launch: the mean
 # over the 325 contraction launches of one m = 1 token step through the stack.
-TRAFFIC_KIB = {"gemv_lut_kernel<1,3,*>": ("linear_decode.hip", 64928.5, 6897.9)}
+TRAFFIC_KIB = {"gemv_lut_kernel<1,3,*>": ("linear_decode.hip", 64802.0, 6897.9)}
 
 
 def traffic_bytes(kernel: str):
