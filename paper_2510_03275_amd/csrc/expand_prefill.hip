@@ -64,10 +64,14 @@ __device__ inline int64_t xcd_tile(int64_t id, int64_t n) {
 // or with a non-finite maximum keeps p = 1.
 template <sdq_dtype XT>
 __global__ __launch_bounds__(256) void prefill_row_scale_kernel(const void* __restrict__ x, int64_t m,
-                                                                int64_t k, float e1, float* __restrict__ fac) {
+                                                                int64_t k, float e1, float* __restrict__ fac,
+                                                                _Float16* __restrict__ pad_out, int64_t k_up,
+                                                                int64_t k_up_pad) {
   const int lane = threadIdx.x % 64;
   const int64_t i = static_cast<int64_t>(blockIdx.x) * 4 + threadIdx.x / 64;
   if (i >= m) return;
+  if (pad_out)   // the padding columns of this row of x_tilde
+    for (int64_t j = k_up + lane; j < k_up_pad; j += 64) pad_out[i * k_up_pad + j] = static_cast<_Float16>(0.0f);
   constexpr int PER = XT == SDQ_F32 ? 4 : 8;          // values per 16 bytes
   const uint4* row = reinterpret_cast<const uint4*>(static_cast<const char*>(x) +
                                                     i * k * (XT == SDQ_F32 ? 4 : 2));
@@ -288,11 +292,11 @@ __global__ __launch_bounds__(256) void expand_prefill_tiled_kernel(
 // B = 128 or 256 and a single fp16 x_tilde (the layouts with Had): E^T is the
 // same for every block, so a workgroup keeps one 128-sample slice of it in
 // registers, as MFMA B fragments (each wave 32 samples x B taps, hi and lo),
-// loaded once, and walks a range of (128-row tile, block) items.  Each item's
+// loaded once, and walks a range of (64-row tile, block) items.  Each item's
 // x tile goes straight from global memory to LDS (global_load_lds, 16-byte
-// groups XOR-swizzled by row as in the GEMM) in two buffers, the next item's
-// copies in flight during this item's MFMAs, with the tile's row factors p_i
-// copied beside it.  The products run on the activation's own type: fp16 x
+// groups XOR-swizzled by row as in the GEMM) in a ring of four buffers, the
+// next three items' copies in flight during this item's MFMAs, with the
+// tile's row factors p_i copied beside it.  The products run on the activation's own type: fp16 x
 // against the fp16 pair hi + lo of E, bf16 x against a bf16 pair of E formed
 // in registers (hi = bf16(E), lo = bf16(E - hi), E to ~2^-17).  E^T is the
 // A operand, so a lane's accumulators hold four consecutive samples of one
@@ -306,6 +310,12 @@ typedef __attribute__((address_space(1))) const void* est_gbl_ptr;
 
 __device__ inline int est_swz(int r) { return (r >> 1) & 7; }
 constexpr int kEstWaitLgkm = 0xC07F;   // lgkmcnt(0) only
+constexpr int kEstRows = 64;          // x rows per item of the E-stationary expansion
+constexpr int kEstBufs = 4;           // x tiles in its LDS ring
+constexpr int kEstRsrcWord3 = 0x00020000;   // raw buffer resource, dword 3
+
+// vmcnt(n) with lgkmcnt(0) (expcnt not waited on).
+constexpr int est_wait_vm_lgkm0(int n) { return (n & 15) | ((n >> 4) << 14) | (7 << 4); }
 
 template <sdq_dtype XT, int B>
 __global__ __launch_bounds__(256, 1) void expand_prefill_estat_kernel(
@@ -314,13 +324,18 @@ __global__ __launch_bounds__(256, 1) void expand_prefill_estat_kernel(
     const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo, _Float16* __restrict__ xt_out) {
   constexpr int G = B / 8;            // 16-byte groups per x row
   constexpr int KS = B / 16;          // 16-deep k steps
-  constexpr int TILE = 128 * B;       // halves per x tile
+  constexpr int TR = kEstRows;        // x rows per item
+  constexpr int NBUF = kEstBufs;      // ring of x tiles
+  constexpr int TILE = TR * B;        // halves per x tile
   constexpr int RPC = 64 / G;         // rows per 1 KB copy
-  constexpr int FC = 32 / RPC;        // copies per wave per tile (a wave fills 32 rows)
+  constexpr int FC = (TR / 4) / RPC;  // copies per wave per tile (a wave fills TR / 4 rows)
+  constexpr int F = FC + 1;           // copies per wave per item (x and the row factors)
+  constexpr int SPI = (TR / 32) * 4;  // 8-byte stores per lane per item
+  static_assert(2 * F + 3 * SPI <= 63, "vmcnt range");
   constexpr bool BF = XT == SDQ_BF16;
   typedef typename std::conditional<BF, bf16x8, half8>::type frag8;
-  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * TILE + 2 * 2 * 128];
-  float* const pvb = reinterpret_cast<float*>(lds + 2 * TILE);   // [2][128] row factors
+  __shared__ __attribute__((aligned(16))) uint16_t lds[NBUF * TILE + NBUF * 4 * 2 * TR];
+  float* const pvb = reinterpret_cast<float*>(lds + NBUF * TILE);   // [NBUF][wave][TR] row factors
   const int tid = threadIdx.x, lane = tid % 64;
   const int wave = __builtin_amdgcn_readfirstlane(tid / 64);
   const int id = blockIdx.x, xcd = id % kXcds, jx = id / kXcds;
@@ -328,8 +343,6 @@ __global__ __launch_bounds__(256, 1) void expand_prefill_estat_kernel(
   const int64_t g = static_cast<int64_t>(jx / n_ss) * kXcds + xcd;
   const int64_t it_begin = g * ipg, it_end = min<int64_t>(n_items, it_begin + ipg);
   if (it_begin >= it_end) return;
-  const int64_t n_rt = (m + 127) / 128;
-  (void)n_rt;
   // E^T fragments of this lane's sample, k = 16 ks + 8 (lane / 32) .. + 7.
   const int col = 128 * s + 32 * wave + lane % 32;
   const bool cok = col < m_up;
@@ -356,49 +369,60 @@ __global__ __launch_bounds__(256, 1) void expand_prefill_estat_kernel(
   }
   const uint16_t* __restrict__ xg = static_cast<const uint16_t*>(x);
   // Copy of item `item`'s x tile and row factors into buffer `buf`: copy j of
-  // wave w writes rows 32 w + RPC j .. (lane l: row + l / G, slot l % G, which
-  // holds group (l % G) ^ swz(row)); rows past m read row m - 1.
+  // wave w writes rows TR/4 w + RPC j .. (lane l: row + l / G, slot l % G,
+  // which holds group (l % G) ^ swz(row)); rows past m read row m - 1.  FC
+  // copies per wave, and one more (the factors) on wave 0.
+  const int nb32 = static_cast<int>(nb);   // items and blocks fit 32 bits
   auto fill = [&](int buf, int64_t item) {
-    const int64_t rt = item / nb, b = item % nb;
-    const int64_t i0 = rt * 128;
+    const int rt = static_cast<int>(item) / nb32, b = static_cast<int>(item) - rt * nb32;
+    const int64_t i0 = static_cast<int64_t>(rt) * TR;
 #pragma unroll
     for (int j = 0; j < FC; ++j) {
-      const int r = 32 * wave + RPC * j + lane / G;
+      const int r = (TR / 4) * wave + RPC * j + lane / G;
       const int64_t row = min<int64_t>(i0 + r, m - 1);
       const uint16_t* src = xg + row * k + b * B + 8 * ((lane % G) ^ est_swz(r));
-      __builtin_amdgcn_global_load_lds((est_gbl_ptr)src, (est_lds_ptr)(lds + buf * TILE + (32 * wave + RPC * j) * B),
-                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds((est_gbl_ptr)src,
+                                       (est_lds_ptr)(lds + buf * TILE + ((TR / 4) * wave + RPC * j) * B), 16, 0, 0);
     }
-    if (wave < 2) {
-      const float* src = fac + min<int64_t>(i0 + 64 * wave + lane, m - 1);
-      __builtin_amdgcn_global_load_lds((est_gbl_ptr)src, (est_lds_ptr)(pvb + buf * 128 + 64 * wave), 4, 0, 0);
-    }
+    const float* src = fac + min<int64_t>(i0 + lane, m - 1);   // every wave its own copy
+    __builtin_amdgcn_global_load_lds((est_gbl_ptr)src, (est_lds_ptr)(pvb + (buf * 4 + wave) * TR), 4, 0, 0);
   };
-  // Pipeline: buffer cur holds item it (landed), buffer cur ^ 1 item it + 1
-  // (copies in flight).  After item it's products every wave waits for all of
-  // its own vm operations (the next item's copies, issued an item ago, and
-  // the previous item's stores), and the barrier makes that hold for all.
-  fill(0, it_begin);
-  fill(1, min<int64_t>(it_begin + 1, it_end - 1));
-  __builtin_amdgcn_s_waitcnt(0);
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
+  // Ring of NBUF buffers, NBUF - 1 items in flight: item it sits in buffer
+  // (it - it_begin) % NBUF.  Per item: wait for its copies (every wave its
+  // own, counted: the copies and stores issued after them stay in flight),
+  // barrier, refill the buffer the previous item used with item it + NBUF - 1,
+  // then the products and the stores.  Vector memory operations complete in
+  // issue order for the counter, and the counts below leave out the
+  // conditional operations (wave 0's factor copy, the padding stores), so
+  // each wait covers at least the item's own copies.
+  for (int p = 0; p < NBUF - 1; ++p) fill(p, min<int64_t>(it_begin + p, it_end - 1));
   for (int64_t it = it_begin; it < it_end; ++it) {
-    const int cur = static_cast<int>((it - it_begin) & 1);
-    const int64_t rt = it / nb, b = it % nb;
-    const int64_t i0 = rt * 128;
+    const int64_t t = it - it_begin;
+    const int cur = static_cast<int>(t % NBUF);
+    if (t == 0) __builtin_amdgcn_s_waitcnt(est_wait_vm_lgkm0(2 * F));
+    else if (t == 1) __builtin_amdgcn_s_waitcnt(est_wait_vm_lgkm0(2 * F + SPI));
+    else if (t == 2) __builtin_amdgcn_s_waitcnt(est_wait_vm_lgkm0(2 * F + 2 * SPI));
+    else __builtin_amdgcn_s_waitcnt(est_wait_vm_lgkm0(2 * F + 3 * SPI));
+    asm volatile("" ::: "memory");
+    __builtin_amdgcn_s_barrier();
+    asm volatile("" ::: "memory");
+    fill(static_cast<int>((t + NBUF - 1) % NBUF), min<int64_t>(it + NBUF - 1, it_end - 1));
+    const int rt = static_cast<int>(it) / nb32, b = static_cast<int>(it) - rt * nb32;
+    const int64_t i0 = static_cast<int64_t>(rt) * TR;
     const uint16_t* abuf = lds + cur * TILE;
-    floatx16 acc[4];
+    float pr[TR / 32];
 #pragma unroll
-    for (int r = 0; r < 4; ++r)
+    for (int r = 0; r < TR / 32; ++r) pr[r] = pvb[(cur * 4 + wave) * TR + 32 * r + lane % 32];
+    floatx16 acc[TR / 32];
+#pragma unroll
+    for (int r = 0; r < TR / 32; ++r)
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[r][v] = 0.0f;
 #pragma unroll
     for (int ks = 0; ks < KS; ++ks) {
       const int gk = 2 * ks + lane / 32;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
+      for (int r = 0; r < TR / 32; ++r) {
         const int row = 32 * r + lane % 32;
         const frag8 a = *reinterpret_cast<const frag8*>(abuf + row * B + 8 * (gk ^ est_swz(row)));
         if constexpr (BF) {
@@ -410,43 +434,29 @@ __global__ __launch_bounds__(256, 1) void expand_prefill_estat_kernel(
         }
       }
     }
-    // item it + 1 has landed, every wave is done with buffer cur's tile and
-    // the previous item's stores have drained
-    __builtin_amdgcn_s_waitcnt(0);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    // this lane's rows: 32 r + lane % 32 (factors read before the refill)
-    float pr[4];
-#pragma unroll
-    for (int r = 0; r < 4; ++r) pr[r] = pvb[cur * 128 + 32 * r + lane % 32];
-    __builtin_amdgcn_s_waitcnt(kEstWaitLgkm);
-    asm volatile("" ::: "memory");
-    __builtin_amdgcn_s_barrier();
-    asm volatile("" ::: "memory");
-    fill(cur, min<int64_t>(it + 2, it_end - 1));
-    if (b == 0 && s == 0) {
-      // zero the padding columns of these rows (written by nobody else)
-      const int64_t pad = k_up_pad - k_up;
-      for (int64_t idx = tid; idx < 128 * pad; idx += 256) {
-        const int64_t i = i0 + idx / pad;
-        if (i < m) xt_out[i * k_up_pad + k_up + idx % pad] = static_cast<_Float16>(0.0f);
-      }
-    }
     // acc[r][v] = x_tilde of row i0 + 32 r + lane % 32, sample
     // 128 s + 32 w + 8 (v / 4) + 4 (lane / 32) + v % 4: four consecutive
-    // samples per 8-byte store
+    // samples per 8-byte store.  Buffer stores over this row tile's rows
+    // below m: a row past m, or a sample past M (offset ~0), falls outside the
+    // range and is dropped, so every lane issues all SPI stores (the counts
+    // above rely on it).  The padding columns are zeroed by the row-scale
+    // kernel.
+    const int64_t rows_here = min<int64_t>(TR, m - i0);
+    const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
+        xt_out + i0 * k_up_pad, static_cast<short>(0), static_cast<int>(rows_here * k_up_pad * 2), kEstRsrcWord3);
 #pragma unroll
-    for (int r = 0; r < 4; ++r) {
-      const int64_t i = i0 + 32 * r + lane % 32;
+    for (int r = 0; r < TR / 32; ++r) {
+      const int ri = 32 * r + lane % 32;
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
         const int c = 128 * s + 32 * wave + 8 * q + 4 * (lane / 32);
         typedef _Float16 half4 __attribute__((ext_vector_type(4)));
+        typedef unsigned u32x2 __attribute__((ext_vector_type(2)));
         half4 h;
 #pragma unroll
         for (int u = 0; u < 4; ++u) h[u] = static_cast<_Float16>(acc[r][4 * q + u] * pr[r]);
-        if (i < m && c < m_up) *reinterpret_cast<half4*>(xt_out + i * k_up_pad + b * m_up + c) = h;
+        const uint32_t off = c < m_up ? static_cast<uint32_t>((ri * k_up_pad + b * m_up + c) * 2) : 0xFFFFFFFFu;
+        __builtin_amdgcn_raw_buffer_store_b64(__builtin_bit_cast(u32x2, h), rs, off, 0, 0);
       }
     }
   }
@@ -468,9 +478,6 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
   const int64_t k_up_pad = L->n_chunks * L->codes_per_chunk;
   float* fac = reinterpret_cast<float*>(static_cast<char*>(ws) + prefill_planes_bytes(L, m));
   const dim3 sgrid(static_cast<unsigned>((m + 3) / 4));
-  if (xt == SDQ_F32) prefill_row_scale_kernel<SDQ_F32><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac);
-  else if (xt == SDQ_BF16) prefill_row_scale_kernel<SDQ_BF16><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac);
-  else prefill_row_scale_kernel<SDQ_F16><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac);
   _Float16* xlo = prefill_split(L)
                       ? reinterpret_cast<_Float16*>(static_cast<char*>(ws) +
                                                     align_up(static_cast<size_t>(m) * k_up_pad * 2, 256))
@@ -481,9 +488,17 @@ sdq_status launch_prefill_expand(const void* x, sdq_dtype xt, int64_t m, const s
   // slices of M; each walks an even share of the (row tile, block) items.
   static const char* env = std::getenv("SDQ_PREFILL_EXPAND");
   const bool tiled_forced = env && std::string(env) == "tiled";
-  if (!tiled_forced && xt != SDQ_F32 && !xlo && (L->block == 128 || L->block == 256)) {
+  const bool estat = !tiled_forced && xt != SDQ_F32 && !xlo && (L->block == 128 || L->block == 256);
+  _Float16* pad_out = estat ? xbuf : nullptr;   // the E-stationary kernel leaves the padding to this one
+  if (xt == SDQ_F32)
+    prefill_row_scale_kernel<SDQ_F32><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac, pad_out, L->k_up, k_up_pad);
+  else if (xt == SDQ_BF16)
+    prefill_row_scale_kernel<SDQ_BF16><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac, pad_out, L->k_up, k_up_pad);
+  else
+    prefill_row_scale_kernel<SDQ_F16><<<sgrid, dim3(256), 0, stream>>>(x, m, L->k, T->e1max, fac, pad_out, L->k_up, k_up_pad);
+  if (estat) {
     const int n_ss = (L->m_up + 127) / 128;
-    const int64_t n_items = ((m + 127) / 128) * L->nb;
+    const int64_t n_items = ((m + kEstRows - 1) / kEstRows) * L->nb;
     const int64_t cus = device_compute_units();
     const int64_t groups = ((cus + n_ss - 1) / n_ss + kXcds - 1) / kXcds * kXcds;
     const int64_t ipg = (n_items + groups - 1) / groups;
