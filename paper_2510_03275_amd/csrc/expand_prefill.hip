@@ -309,7 +309,6 @@ typedef __attribute__((address_space(3))) void* est_lds_ptr;
 typedef __attribute__((address_space(1))) const void* est_gbl_ptr;
 
 __device__ inline int est_swz(int r) { return (r >> 1) & 7; }
-constexpr int kEstWaitLgkm = 0xC07F;   // lgkmcnt(0) only
 constexpr int kEstRows = 64;          // x rows per item of the E-stationary expansion
 constexpr int kEstBufs = 4;           // x tiles in its LDS ring
 constexpr int kEstRsrcWord3 = 0x00020000;   // raw buffer resource, dword 3
