@@ -44,6 +44,7 @@ constexpr int kMaxDecodeRows = 16;  // activation rows of the decode path
 constexpr int kGemvWaves = 4;
 constexpr int kGroupsPerChunk = 32; // 128 bits / 4
 constexpr int64_t kExpRowPairs = 1024; // one-row expansion: two blocks per workgroup from here
+constexpr int64_t kPlanePairs = 768;   // plane expansion: two blocks per workgroup from here
 
 // A 16-byte load of packed codes, marked non-temporal: each code byte is read
 // once per call, and the streaming hint keeps the code stream from evicting
@@ -299,100 +300,112 @@ typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
 // Matrix-core front end of the plane expansions for fp16 and bf16
-// activations: the quantised x_tilde of code positions g0 + [0, 64) of block
-// b for all rows, into qv[row][position] (zero outside the block), and (when
-// write_sx) the block's plane scales.  Wave w takes positions 16 w + [0, 16):
-// x_b (rows as the A operand, zero past m) times the columns of E as the
-// fp16 pair hi + lo of the transposed tables (the B operand), 2 B / 32
-// v_mfma_f32_16x16x32_f16 with fp32 accumulation.  bf16 x is scaled per
-// (row, block) by a power of two that brings its max into [2^14, 2^15), so it
-// converts to fp16 exactly (values below 2^-24 of the max round); the scale
+// activations: the quantised x_tilde of code positions g0 + [0, 64) of blocks
+// b0 .. b0 + nbl - 1 (nbl <= NB) for all rows, into qv[j][row][position] (zero
+// outside the block), and (when write_sx) the blocks' plane scales.  The
+// blocks share the columns of E: with M a multiple of the code chunk, code
+// position p of slot u is sample 64 u + p of every block, so E is loaded once
+// per workgroup whatever NB.  Wave w takes positions 16 w + [0, 16): x_b (rows
+// as the A operand, zero past m) times the columns of E as the fp16 pair hi +
+// lo of the transposed tables (the B operand), 2 B / 32
+// v_mfma_f32_16x16x32_f16 per block with fp32 accumulation.  bf16 x is scaled
+// per (row, block) by a power of two that brings its max into [2^14, 2^15), so
+// it converts to fp16 exactly (values below 2^-24 of the max round); the scale
 // cancels in the quantisation, whose bound max |x_b| * e1max is the fp32
 // path's.  E hi + lo carries ~22 bits, against 24 for the fixed point.
-template <int B, bool BF16>
-__device__ inline void planes_qv_mfma(const uint16_t* __restrict__ x, int m, int k32, int64_t b,
+template <int B, bool BF16, int NB>
+__device__ inline void planes_qv_mfma(const uint16_t* __restrict__ x, int m, int k32, int64_t b0, int nbl,
                                       int64_t g0, int m_up, int64_t nb, bool write_sx,
                                       const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo,
-                                      float e1max, float* __restrict__ sx, int (*qv)[64]) {
+                                      float e1max, float* __restrict__ sx, int (*qv)[kMaxDecodeRows][64]) {
   constexpr int S = B / 32;                  // k-steps of 32 samples of t
   const int lane = threadIdx.x % 64;
   const int w = threadIdx.x / 64;
   const int r = lane % 16, grp = lane / 16;  // operand row / column, k group
   const int pos = 16 * w + r;                // this lane's B column: code position
-  const int o = static_cast<int>(g0 + pos - b * m_up);
+  const int o = static_cast<int>(g0 + pos - b0 * m_up);
   const bool in_block = o >= 0 && o < m_up;
   // Loads from clamped (in-bounds) addresses, zeroed by selects.
-  const uint4* __restrict__ xp =
-      reinterpret_cast<const uint4*>(x + static_cast<int64_t>(min(r, m - 1)) * k32 + b * B) + grp;
   const uint4* __restrict__ hp = reinterpret_cast<const uint4*>(et_hi + static_cast<int64_t>(in_block ? o : 0) * B) + grp;
   const uint4* __restrict__ lp = reinterpret_cast<const uint4*>(et_lo + static_cast<int64_t>(in_block ? o : 0) * B) + grp;
-  uint4 xq[S], eh[S], el[S];
+  uint4 xq[NB][S], eh[S], el[S];
 #pragma unroll
-  for (int st = 0; st < S; ++st) xq[st] = xp[4 * st];
+  for (int j = 0; j < NB; ++j) {
+    const int64_t bj = b0 + min(j, nbl - 1);
+    const uint4* __restrict__ xp =
+        reinterpret_cast<const uint4*>(x + static_cast<int64_t>(min(r, m - 1)) * k32 + bj * B) + grp;
+#pragma unroll
+    for (int st = 0; st < S; ++st) xq[j][st] = xp[4 * st];
+  }
 #pragma unroll
   for (int st = 0; st < S; ++st) eh[st] = hp[4 * st];
 #pragma unroll
   for (int st = 0; st < S; ++st) el[st] = lp[4 * st];
-  // max |x| of row r over the lane's 8 S samples, then over the four k groups
-  float mx = 0.0f;
 #pragma unroll
-  for (int st = 0; st < S; ++st) {
-    const uint32_t wv[4] = {xq[st].x, xq[st].y, xq[st].z, xq[st].w};
+  for (int j = 0; j < NB; ++j) {
+    if (j >= nbl) break;
+    // max |x| of row r over the lane's 8 S samples, then over the four k groups
+    float mx = 0.0f;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) {
-      const float lo = BF16 ? __uint_as_float(wv[j] << 16) : __half2float(__ushort_as_half(static_cast<unsigned short>(wv[j])));
-      const float hi = BF16 ? __uint_as_float(wv[j] & 0xFFFF0000u)
-                            : __half2float(__ushort_as_half(static_cast<unsigned short>(wv[j] >> 16)));
-      mx = fmaxf(mx, fmaxf(fabsf(lo), fabsf(hi)));
-    }
-  }
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  if (r >= m) mx = 0.0f;
-  int ex = 0;
-  (void)frexpf(mx, &ex);                     // mx < 2^ex
-  const int sh = mx > 0.0f ? 15 - ex : 0;    // bf16 scale 2^sh
-  float4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
+    for (int st = 0; st < S; ++st) {
+      const uint32_t wv[4] = {xq[j][st].x, xq[j][st].y, xq[j][st].z, xq[j][st].w};
 #pragma unroll
-  for (int st = 0; st < S; ++st) {
-    half8_t a;
-    if constexpr (BF16) {
-      const uint32_t wv[4] = {xq[st].x, xq[st].y, xq[st].z, xq[st].w};
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        a[2 * j] = static_cast<_Float16>(ldexpf(__uint_as_float(wv[j] << 16), sh));
-        a[2 * j + 1] = static_cast<_Float16>(ldexpf(__uint_as_float(wv[j] & 0xFFFF0000u), sh));
+      for (int q = 0; q < 4; ++q) {
+        const float lo = BF16 ? __uint_as_float(wv[q] << 16)
+                              : __half2float(__ushort_as_half(static_cast<unsigned short>(wv[q])));
+        const float hi = BF16 ? __uint_as_float(wv[q] & 0xFFFF0000u)
+                              : __half2float(__ushort_as_half(static_cast<unsigned short>(wv[q] >> 16)));
+        mx = fmaxf(mx, fmaxf(fabsf(lo), fabsf(hi)));
       }
-    } else {
-      a = *reinterpret_cast<const half8_t*>(&xq[st]);
     }
-    if (r >= m) a = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
-    half8_t h = *reinterpret_cast<const half8_t*>(&eh[st]);
-    half8_t l = *reinterpret_cast<const half8_t*>(&el[st]);
-    if (!in_block) {
-      h = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
-      l = h;
-    }
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, h, acc, 0, 0, 0);
-    acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, l, acc, 0, 0, 0);
-  }
-  // Output v of this lane: row a = 4 grp + v, position pos.  The row's max
-  // sits in lane a (lane a holds row a % 16 = a).
+    mx = fmaxf(mx, __shfl_xor(mx, 16));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    if (r >= m) mx = 0.0f;
+    int ex = 0;
+    (void)frexpf(mx, &ex);                     // mx < 2^ex
+    const int sh = mx > 0.0f ? 15 - ex : 0;    // bf16 scale 2^sh
+    float4_t acc = {0.0f, 0.0f, 0.0f, 0.0f};
 #pragma unroll
-  for (int v = 0; v < 4; ++v) {
-    const int a = 4 * grp + v;
-    const float mxa = __shfl(mx, a);
-    const float bound = mxa * e1max;
-    int q = 0;
-    if (bound > 0.0f && in_block) {
-      int exa = 0;
-      (void)frexpf(mxa, &exa);
-      const float sc = BF16 ? ldexpf(bound, 15 - exa) : bound;   // the bound in acc's scale
-      q = __float2int_rn(acc[v] * (kQ / sc));
+    for (int st = 0; st < S; ++st) {
+      half8_t a;
+      if constexpr (BF16) {
+        const uint32_t wv[4] = {xq[j][st].x, xq[j][st].y, xq[j][st].z, xq[j][st].w};
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+          a[2 * q] = static_cast<_Float16>(ldexpf(__uint_as_float(wv[q] << 16), sh));
+          a[2 * q + 1] = static_cast<_Float16>(ldexpf(__uint_as_float(wv[q] & 0xFFFF0000u), sh));
+        }
+      } else {
+        a = *reinterpret_cast<const half8_t*>(&xq[j][st]);
+      }
+      if (r >= m) a = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+      half8_t h = *reinterpret_cast<const half8_t*>(&eh[st]);
+      half8_t l = *reinterpret_cast<const half8_t*>(&el[st]);
+      if (!in_block) {
+        h = half8_t{0, 0, 0, 0, 0, 0, 0, 0};
+        l = h;
+      }
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, h, acc, 0, 0, 0);
+      acc = __builtin_amdgcn_mfma_f32_16x16x32_f16(a, l, acc, 0, 0, 0);
     }
-    qv[a][pos] = q;
+    // Output v of this lane: row a = 4 grp + v, position pos.  The row's max
+    // sits in lane a (lane a holds row a % 16 = a).
+#pragma unroll
+    for (int v = 0; v < 4; ++v) {
+      const int a = 4 * grp + v;
+      const float mxa = __shfl(mx, a);
+      const float bound = mxa * e1max;
+      int q = 0;
+      if (bound > 0.0f && in_block) {
+        int exa = 0;
+        (void)frexpf(mxa, &exa);
+        const float sc = BF16 ? ldexpf(bound, 15 - exa) : bound;   // the bound in acc's scale
+        q = __float2int_rn(acc[v] * (kQ / sc));
+      }
+      qv[j][a][pos] = q;
+    }
+    if (write_sx && w == 0 && grp == 0 && r < m) sx[static_cast<int64_t>(r) * nb + b0 + j] = mx * e1max / kQ;
   }
-  if (write_sx && w == 0 && grp == 0 && r < m) sx[static_cast<int64_t>(r) * nb + b] = mx * e1max / kQ;
 }
 
 // One workgroup: one 64-code segment u of block b's chunk slots (code
@@ -624,26 +637,32 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_b3_kernel(
   store_planes_b3(qv, m, npg, b, g0, c_first, steps3, planes);
 }
 
-// The plane expansions for fp16 and bf16 activations (the same grids, plane
-// layouts and side duties as expand_planes_kernel / expand_planes_b3_kernel),
-// with the dot products on the matrix cores (planes_qv_mfma).
-template <int B, int LEVELS, bool BF16>
+// The plane expansions for fp16 and bf16 activations (the same plane layouts
+// and side duties as expand_planes_kernel / expand_planes_b3_kernel), with the
+// dot products on the matrix cores (planes_qv_mfma).  Grid: (slots, blocks /
+// NB); NB = 2 only when M is a multiple of the code chunk (the blocks of a
+// workgroup then use the same columns of E).
+template <int B, int LEVELS, bool BF16, int NB>
 __global__ __launch_bounds__(kExpThreads) void expand_planes_mfma_kernel(
     const void* __restrict__ x, int m, int npg, int64_t k, int64_t nb, int m_up, int cpb,
     const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo, float e1max,
     uint32_t* __restrict__ planes, float* __restrict__ sx, LinearSet zero) {
-  __shared__ int qv[kMaxDecodeRows][64];
+  __shared__ int qv[NB][kMaxDecodeRows][64];
   constexpr int kCpc = LEVELS == 2 ? 128 : 64;
-  const int64_t b = blockIdx.y;
-  const int64_t c_first = b * m_up / kCpc;
-  const int64_t g0 = c_first * kCpc + static_cast<int64_t>(blockIdx.x) * 64;
-  planes_qv_mfma<B, BF16>(static_cast<const uint16_t*>(x), m, static_cast<int>(k), b, g0, m_up, nb,
-                    blockIdx.x == 0, et_hi, et_lo, e1max, sx, qv);
+  const int64_t b0 = static_cast<int64_t>(blockIdx.y) * NB;
+  const int nbl = static_cast<int>(min<int64_t>(NB, nb - b0));
+  const int64_t g0 = b0 * m_up / kCpc * kCpc + static_cast<int64_t>(blockIdx.x) * 64;
+  planes_qv_mfma<B, BF16, NB>(static_cast<const uint16_t*>(x), m, static_cast<int>(k), b0, nbl, g0, m_up, nb,
+                              blockIdx.x == 0, et_hi, et_lo, e1max, sx, qv);
   const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
   zero_outputs(zero, m, wg, static_cast<int64_t>(gridDim.x) * gridDim.y, threadIdx.x);
   __syncthreads();
-  store_planes<LEVELS>(qv, m, npg, b * cpb + static_cast<int64_t>(blockIdx.x) / (kCpc / 64),
-                       static_cast<int>(blockIdx.x % (kCpc / 64)), planes);
+#pragma unroll
+  for (int j = 0; j < NB; ++j) {
+    if (j >= nbl) break;
+    store_planes<LEVELS>(qv[j], m, npg, (b0 + j) * cpb + static_cast<int64_t>(blockIdx.x) / (kCpc / 64),
+                         static_cast<int>(blockIdx.x % (kCpc / 64)), planes);
+  }
 }
 
 template <int B, bool BF16>
@@ -651,16 +670,16 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_b3_mfma_kernel(
     const void* __restrict__ x, int m, int npg, int64_t k, int64_t nb, int m_up, int steps3,
     const uint16_t* __restrict__ et_hi, const uint16_t* __restrict__ et_lo, float e1max,
     uint8_t* __restrict__ planes, float* __restrict__ sx, LinearSet zero) {
-  __shared__ int qv[kMaxDecodeRows][64];
+  __shared__ int qv[1][kMaxDecodeRows][64];
   const int64_t b = blockIdx.y;
   const int64_t c_first = b * m_up / kBase3PerChunk;
   const int64_t g0 = c_first * kBase3PerChunk + static_cast<int64_t>(blockIdx.x) * 64;
-  planes_qv_mfma<B, BF16>(static_cast<const uint16_t*>(x), m, static_cast<int>(k), b, g0, m_up, nb,
-                    blockIdx.x == 0, et_hi, et_lo, e1max, sx, qv);
+  planes_qv_mfma<B, BF16, 1>(static_cast<const uint16_t*>(x), m, static_cast<int>(k), b, 1, g0, m_up, nb,
+                             blockIdx.x == 0, et_hi, et_lo, e1max, sx, qv);
   const int64_t wg = static_cast<int64_t>(blockIdx.y) * gridDim.x + blockIdx.x;
   zero_outputs(zero, m, wg, static_cast<int64_t>(gridDim.x) * gridDim.y, threadIdx.x);
   __syncthreads();
-  store_planes_b3(qv, m, npg, b, g0, c_first, steps3, planes);
+  store_planes_b3(qv[0], m, npg, b, g0, c_first, steps3, planes);
 }
 
 // One workgroup: one 64-row panel and 4 * bpw consecutive blocks, wave w
@@ -1720,16 +1739,33 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
     const int npg = npg_for(m);
     const int cpb = mfma_cpb(L);
     const dim3 pgrid(static_cast<unsigned>(cpb * (L->levels == 2 ? 2 : 1)), static_cast<unsigned>(L->nb));
-#define SDQ_PLANES(BB, LV)                                                                       \
-  if (planes_mfma && xt == SDQ_BF16)                                                             \
-    expand_planes_mfma_kernel<BB, LV, true><<<pgrid, dim3(kExpThreads), 0, stream>>>(            \
-        x, static_cast<int>(m), npg, L->k, L->nb, L->m_up, cpb, T->et_hi, T->et_lo, T->e1max,      \
-        w.planes, w.sx, z);                                                                      \
-  else if (planes_mfma)                                                                          \
-    expand_planes_mfma_kernel<BB, LV, false><<<pgrid, dim3(kExpThreads), 0, stream>>>(           \
+    // Two blocks per workgroup (E loaded once for both) for fp16 x when M is a
+    // multiple of the code chunk and one block per workgroup would take
+    // kPlanePairs workgroups or more (bf16 x: 248 VGPRs with two blocks).
+    // Measured on MI355X at m = 8, k = 28672 (graph replay): OSR 3 16.7 ->
+    // 13.0 us, OSR 2 12.2 -> 10.2 us, OSR 1.5 (672 workgroups) 9.5 -> 9.9 us.  SDQ_PLANES_NBW=1 or 2 overrides (a tuning aid,
+    // read on every launch; 2 only where M allows it).
+    const int64_t cpc = L->levels == 2 ? 128 : 64;
+    const char* nbw_env = std::getenv("SDQ_PLANES_NBW");
+    int pnb = xt == SDQ_F16 && L->m_up % cpc == 0 && static_cast<int64_t>(pgrid.x) * L->nb >= kPlanePairs ? 2 : 1;
+    if (nbw_env && (std::atoi(nbw_env) == 1 || std::atoi(nbw_env) == 2)) pnb = std::atoi(nbw_env);
+    if (L->m_up % cpc != 0) pnb = 1;
+    const dim3 pgrid2(pgrid.x, static_cast<unsigned>((L->nb + 1) / 2));
+#define SDQ_PLANES_M(BB, LV, BF)                                                                 \
+  if (pnb == 2)                                                                                  \
+    expand_planes_mfma_kernel<BB, LV, BF, 2><<<pgrid2, dim3(kExpThreads), 0, stream>>>(          \
         x, static_cast<int>(m), npg, L->k, L->nb, L->m_up, cpb, T->et_hi, T->et_lo, T->e1max,      \
         w.planes, w.sx, z);                                                                      \
   else                                                                                           \
+    expand_planes_mfma_kernel<BB, LV, BF, 1><<<pgrid, dim3(kExpThreads), 0, stream>>>(           \
+        x, static_cast<int>(m), npg, L->k, L->nb, L->m_up, cpb, T->et_hi, T->et_lo, T->e1max,      \
+        w.planes, w.sx, z)
+#define SDQ_PLANES(BB, LV)                                                                       \
+  if (planes_mfma && xt == SDQ_BF16) {                                                           \
+    SDQ_PLANES_M(BB, LV, true);                                                                  \
+  } else if (planes_mfma) {                                                                      \
+    SDQ_PLANES_M(BB, LV, false);                                                                 \
+  } else                                                                                         \
     expand_planes_kernel<BB, LV><<<pgrid, dim3(kExpThreads), 0, stream>>>(                       \
         x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad, cpb,                    \
         reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, z)
@@ -1747,6 +1783,7 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
       }
     }
 #undef SDQ_PLANES
+#undef SDQ_PLANES_M
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_error(e, "decode expansion launch");
     return SDQ_OK;

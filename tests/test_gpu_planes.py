@@ -3,7 +3,8 @@ VALU dot products (every activation dtype) and the matrix-core ones (fp16 and
 bf16 x: x_b times E as the fp16 pair hi + lo).  Both must meet the 1e-3
 budget against the fp64 oracle on every layout kind, including binary codes
 without the Hadamard (the layout most sensitive to noise in x_tilde), base-3
-codes and blocks of 64 and 128; the matrix-core one is also held to 1e-4."""
+codes and blocks of 64 and 128; the matrix-core one (one block per workgroup,
+or two sharing the columns of E) is also held to 1e-4."""
 import numpy as np
 import pytest
 
@@ -51,11 +52,14 @@ def test_plane_front_ends(n, k, osr, levels, block, had, packing, m, dtype, monk
     x_dev, x64 = to_device_x(synth.activations_f32(n + m, 2, m, k), dtype, torch)
     ref = OL.linear_fp64(x64, r.codes, r.scales, block, r.m_up, had, None)
     errs = {}
-    for front in ("0", "1"):
-        monkeypatch.setenv("SDQ_PLANES_MFMA", front)
+    # VALU front end; matrix-core front end with one block per workgroup, and
+    # with two blocks sharing E (taken where M is a multiple of the chunk).
+    for front, mfma, nbw in (("valu", "0", "1"), ("mfma", "1", "1"), ("mfma2", "1", "2")):
+        monkeypatch.setenv("SDQ_PLANES_MFMA", mfma)
+        monkeypatch.setenv("SDQ_PLANES_NBW", nbw)
         y = P.linear(x_dev, enc)
         torch.cuda.synchronize()
         errs[front] = OL.rel_err_rows(y.cpu().numpy().astype(np.float64), ref).max()
-    print(f"valu {errs['0']:.3e} mfma {errs['1']:.3e}")
-    assert errs["0"] <= TOL and errs["1"] <= TOL, errs
-    assert errs["1"] <= 1e-4, errs
+    print(" ".join(f"{f} {e:.3e}" for f, e in errs.items()))
+    assert all(e <= TOL for e in errs.values()), errs
+    assert errs["mfma"] <= 1e-4 and errs["mfma2"] <= 1e-4, errs
