@@ -259,9 +259,10 @@ size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
  *   x_dev        [m x k] activations of type xt (F16, BF16 or F32), row-major.
  *   m            activation rows, >= 0 (m = 0 is a no-op).  m = 1: fp32
  *                expansion and a GEMV with additions only over the codes;
- *                2 <= m <= 16: the expansion quantised to 24-bit fixed point
- *                and an exact int8 x int8 -> int32 matrix-core contraction
- *                against the codes; larger m: the prefill
+ *                2 <= m <= 16: the expansion (for fp16 and bf16 x on the
+ *                matrix cores against E as an fp16 pair hi + lo, ~22 bits)
+ *                quantised to 24-bit fixed point and an exact int8 x int8 ->
+ *                int32 matrix-core contraction against the codes; larger m: the prefill
  *                path (fp16 expansion, fp16 matrix cores).
  *   codes_dev, scales_dev  as written by sdq_quantize for `layout`.
  *   y_dev        fp32 [m x n] output, row-major.
