@@ -62,7 +62,7 @@ POOL_MAX = 16                    # oracle workers: the host share of one GPU
 # were taken with: a source whose hash differs reports traffic null.
 TRAFFIC_FETCH_SCALE = 1.999749
 TRAFFIC_WRITE_SCALE = 1.000000
-TRAFFIC_SOURCES = {"linear_decode.hip": "c7dc13d0288a24b9228e67eca35e58d49c8b00ba1446bcd92e190ca11fc3b9a6"}
+TRAFFIC_SOURCES = {"linear_decode.hip": "48f9d1a35a31d513dedf938e53bffab2145ebb68e109bb7dc100aa4b7f927670"}
 # kernel family -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB) per launch: the mean
 # over the 325 contraction launches of one m = 1 token step through the stack.
 TRAFFIC_KIB = {"gemv_lut_kernel<1,3,*>": ("linear_decode.hip", 64802.0, 6897.9)}
