@@ -37,6 +37,9 @@ PER_FILE = {
     # AGPR copies, 64 moves and a pipeline drain per k step).
     "compensation.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
     "expand_prefill.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
+    # the 2-16-row contractions: without it the integer accumulators rotate
+    # through AGPR copies, 40 moves per 64-code chunk at 5-8 rows
+    "linear_decode.hip": ["-mllvm", "-amdgpu-mfma-vgpr-form"],
 }
 
 

@@ -51,6 +51,10 @@ constexpr int64_t kPlanePairs = 768;   // plane expansion: two blocks per workgr
 // the expansion tables and x_tilde from L2 (measured on MI355X: the 70B stack
 // at m = 1 9.94 -> 9.47 ms per token, at m = 8 16.08 -> 15.55 ms).
 typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void* dec_lds_ptr;
+typedef __attribute__((address_space(1))) const void* dec_gbl_ptr;
+constexpr int kWaitVm0 = 7 << 4;   // s_waitcnt vmcnt(0) lgkmcnt(0), expcnt not waited on
+
 __device__ inline uint4 load_code_chunk(const uint4* p) {
   const u32x4_t v = __builtin_nontemporal_load(reinterpret_cast<const u32x4_t*>(p));
   return make_uint4(v.x, v.y, v.z, v.w);
@@ -211,7 +215,8 @@ __global__ __launch_bounds__(kExpThreads) void expand_decode_row_kernel(
 
 // ---------------------------------------------------------------------------
 // Integer-MFMA decode: x_tilde as 24-bit fixed point in three signed-byte
-// planes, codes expanded to int8 {-1, 0, +1}, exact int32 accumulation.
+// planes, codes expanded to int8 (+-1 binary, 64 x {-1, 0, +1} ternary),
+// exact int32 accumulation (|sum| <= 128 * 64 * M per block).
 //
 // Per (activation row i, block b) the scale is S = max_t |x_b[t]| * e1max / Q
 // with e1max >= max_m sum_t |E[t][m]|, so |x_tilde_b| <= Q * S and the rounded
@@ -226,14 +231,29 @@ __global__ __launch_bounds__(kExpThreads) void expand_decode_row_kernel(
 // block that starts or ends inside a chunk (M not a multiple of the chunk)
 // shares that chunk's codes with its neighbour but not its planes, and every
 // k-step sums one block only; cpb is the most chunks any block touches.
-// Inside a chunk the codes map to (step, kg, dword di, byte beta) as the byte
-// permute produces them from the chunk's word kg:
+// Inside a chunk the codes map to (step, kg, dword di, byte beta) as
+// code_bytes produces them from the chunk's word kg:
 //   ternary  one step per chunk,  code 16 kg + di + 4 beta      (fields di + 4 beta)
 //   binary   two steps s per chunk, code 32 kg + 4 s + di + 8 beta  (bits 4 s + di + 8 beta)
 // A = planes: row p = 4 a + t (activation row a of the plane group, plane t:
 // h, m, l, zero), stored per step and plane group as 64 lanes x 16 bytes.
 constexpr float kQ = 8257536.0f;    // 2^23 - 2^17: leaves |h| <= 126
-constexpr int kStep = 64;           // codes per MFMA k-step
+
+// B-operand bytes of four codes of a chunk word: byte beta holds code field
+// (or bit) d of the word's byte beta.  Ternary fields move to the top two bits
+// of their byte, which as a signed byte is 64 x code (0b01 -> 64, 0b11 -> -64,
+// 0b00 -> 0): a shift and a mask, with the factor 64 (kCodeScale) divided out of
+// the block's sums, exactly, with the plane scale.  Binary bits 0 / 1 map to
+// -1 / +1 through a byte permute.
+template <int LEVELS>
+__device__ inline int code_bytes(uint32_t wv, int d) {
+  if constexpr (LEVELS == 2)
+    return static_cast<int>(__builtin_amdgcn_perm(0u, 0x000001FFu, (wv >> d) & 0x01010101u));
+  else
+    return static_cast<int>((wv << (6 - 2 * d)) & 0xC0C0C0C0u);
+}
+template <int LEVELS>
+constexpr float kCodeScale = LEVELS == 2 ? 1.0f : 64.0f;
 
 template <int LEVELS>
 __device__ inline int chunk_code(int s, int kg, int di, int beta) {
@@ -695,9 +715,6 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
     LinearSet S, const uint4* __restrict__ planes, const float* __restrict__ sx, int m,
     int64_t n_chunks, int64_t nb, int m_up, int cpb, int bpw, int n_split, int accumulate) {
   typedef int v4i __attribute__((ext_vector_type(4)));
-  constexpr uint32_t kTable = LEVELS == 2 ? 0x000001FFu : 0xFF000100u;   // code -> int8
-  constexpr uint32_t kMask = LEVELS == 2 ? 0x01010101u : 0x03030303u;
-  constexpr int kBits = LEVELS == 2 ? 1 : 2;
   constexpr int SPC = LEVELS == 2 ? 2 : 1;          // k-steps per chunk
   constexpr int kCpc = LEVELS == 2 ? 128 : 64;
   __shared__ float red[4][NPG * 4][64];
@@ -732,7 +749,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
     for (int pg = 0; pg < NPG; ++pg) {
       const int a = pg * 4 + kg;
       const float v = sx[static_cast<int64_t>(min(a, m - 1)) * nb + b];
-      sxv[pg] = a < m ? v : 0.0f;
+      sxv[pg] = a < m ? v * (1.0f / kCodeScale<LEVELS>) : 0.0f;
     }
     for (int c0 = 0; c0 < cpb; c0 += CH) {
       uint4 q[CH];
@@ -775,7 +792,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
 #pragma unroll
             for (int di = 0; di < 4; ++di) {
               const int d = LEVELS == 2 ? 4 * s + di : di;
-              bop[di] = static_cast<int>(__builtin_amdgcn_perm(0u, kTable, (wv >> (kBits * d)) & kMask));
+              bop[di] = code_bytes<LEVELS>(wv, d);
             }
 #pragma unroll
             for (int pg = 0; pg < NPG; ++pg) {
@@ -821,7 +838,9 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
 // The same contraction with the planes shared through LDS: one workgroup owns
 // four consecutive 64-row panels of one linear (one per wave) and bpg
 // consecutive blocks; per block it copies the block's planes (cpb * NPG KB)
-// into LDS once, and every wave contracts its own panel's codes against them,
+// into LDS once (global_load_lds, together with the first batch of code
+// chunks: one round trip), and every wave contracts its own panel's codes
+// against them,
 // so each plane byte crosses L2 once per four panels instead of once per
 // panel.  A wave adds its outputs into y itself (one atomic per output and
 // workgroup when K is split).
@@ -831,9 +850,6 @@ __global__ __launch_bounds__(256) void gemv_mfma_lds_kernel(
     int64_t n_chunks, int64_t nb, int m_up, int cpb, int bpg, int n_split, int accumulate) {
   extern __shared__ uint4 pls[];
   typedef int v4i __attribute__((ext_vector_type(4)));
-  constexpr uint32_t kTable = LEVELS == 2 ? 0x000001FFu : 0xFF000100u;   // code -> int8
-  constexpr uint32_t kMask = LEVELS == 2 ? 0x01010101u : 0x03030303u;
-  constexpr int kBits = LEVELS == 2 ? 1 : 2;
   constexpr int SPC = LEVELS == 2 ? 2 : 1;
   constexpr int kCpc = LEVELS == 2 ? 128 : 64;
   const int lane = threadIdx.x % 64;
@@ -858,26 +874,36 @@ __global__ __launch_bounds__(256) void gemv_mfma_lds_kernel(
   const int64_t b_begin = static_cast<int64_t>(blockIdx.x) * bpg;
   const int64_t b_end = min<int64_t>(nb, b_begin + bpg);
   for (int64_t b = b_begin; b < b_end; ++b) {
+    const int64_t c_first = b * m_up / kCpc;
+    // The block's first batch of code chunks, then its planes copied straight
+    // into LDS (global_load_lds, 1 KB per wave and copy, all in flight at
+    // once), then one wait for both.
+    uint4 q[CH];
+#pragma unroll
+    for (int j = 0; j < CH; ++j) q[j] = load_code_chunk(&cpanel[min<int64_t>(c_first + j, n_chunks - 1) * kPanel + lane]);
     const uint4* __restrict__ src = planes + b * per_block;
-    for (int i = threadIdx.x; i < per_block; i += 256) pls[i] = src[i];
+    for (int i0 = wave * 64; i0 < per_block; i0 += 256)
+      __builtin_amdgcn_global_load_lds((dec_gbl_ptr)(src + i0 + lane), (dec_lds_ptr)(pls + i0), 16, 0, 0);
     float sxv[NPG];
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg) {
       const int a = pg * 4 + kg;
       const float v = sx[static_cast<int64_t>(min(a, m - 1)) * nb + b];
-      sxv[pg] = a < m ? v : 0.0f;
+      sxv[pg] = a < m ? v * (1.0f / kCodeScale<LEVELS>) : 0.0f;
     }
+    __builtin_amdgcn_s_waitcnt(kWaitVm0);
     __syncthreads();
     v4i acc[NPG][4];
 #pragma unroll
     for (int pg = 0; pg < NPG; ++pg)
 #pragma unroll
       for (int cg = 0; cg < 4; ++cg) acc[pg][cg] = v4i{0, 0, 0, 0};
-    const int64_t c_first = b * m_up / kCpc;
     for (int c0 = 0; c0 < cpb; c0 += CH) {
-      uint4 q[CH];
+      if (c0 > 0) {
 #pragma unroll
-      for (int j = 0; j < CH; ++j) q[j] = load_code_chunk(&cpanel[min<int64_t>(c_first + c0 + j, n_chunks - 1) * kPanel + lane]);
+        for (int j = 0; j < CH; ++j)
+          q[j] = load_code_chunk(&cpanel[min<int64_t>(c_first + c0 + j, n_chunks - 1) * kPanel + lane]);
+      }
 #pragma unroll
       for (int j = 0; j < CH; ++j) {
         uint32_t r0 = q[j].x, r1 = q[j].y, r2 = q[j].z, r3 = q[j].w;
@@ -899,7 +925,7 @@ __global__ __launch_bounds__(256) void gemv_mfma_lds_kernel(
 #pragma unroll
             for (int di = 0; di < 4; ++di) {
               const int d = LEVELS == 2 ? 4 * s + di : di;
-              bop[di] = static_cast<int>(__builtin_amdgcn_perm(0u, kTable, (wv >> (kBits * d)) & kMask));
+              bop[di] = code_bytes<LEVELS>(wv, d);
             }
 #pragma unroll
             for (int pg = 0; pg < NPG; ++pg) {
@@ -1481,24 +1507,54 @@ int mfma_cpb3(const sdq_layout* L) {
 int mfma_steps3(const sdq_layout* L) { return (mfma_cpb3(L) + kB3Group - 1) / kB3Group * kB3Steps; }
 bool mfma_base3(const sdq_layout* L, int64_t m) { return L->packing == SDQ_PACK_BASE3 && use_mfma(L, m); }
 
+int pick_ch(int cpb, int npg, int levels);
+constexpr int64_t kLdsPlanesWgs = 768;
+
+// Whether a 2-16-row contraction over `panels` panels shares its planes
+// through LDS (gemv_mfma_lds_kernel): for two or three plane groups (5-12
+// rows) on launches of at least kLdsPlanesWgs workgroups of four panels
+// (at one block per wave), when the chunks go in batches of four or the rows
+// are long (64 blocks or more).  Measured on MI355X at m = 8 (70B shapes):
+// gate/up 93 -> 87 us at OSR 3 and 65 -> 62 us at OSR 2 (batches of four),
+// but 78 -> 80 at OSR 2.5 and 51 -> 53 at 1.5 (batches of two); down 2-6 %
+// faster at OSR 1.5-3; the smaller q/k/v and o launches (256-320 workgroups
+// of four panels) ran 21 -> 31 and 17 -> 27 us.  At m = 12 (planes copied
+// with global_load_lds): gate/up 108 -> 89 us at OSR 3, down 59 -> 50.  Four
+// plane groups were slower at every size (m = 16 gate/up 136 -> 144 us).
+// SDQ_MFMA_LDS=0 or 1 forces the choice (a tuning and test aid, read on every
+// call so that a test can take both paths in one process).
+bool mfma_lds(const sdq_layout* L, int64_t m, int64_t panels) {
+  const int npg = npg_for(m);
+  if (mfma_base3(L, m) || (npg != 2 && npg != 3)) return false;
+  const size_t lds_bytes = static_cast<size_t>(mfma_cpb(L)) * (L->levels == 2 ? 2 : 1) * npg * 1024;
+  if (lds_bytes > 65536) return false;
+  const char* env = std::getenv("SDQ_MFMA_LDS");
+  if (env && (std::atoi(env) == 0 || std::atoi(env) == 1)) return std::atoi(env) == 1;
+  const int64_t splits1 = (L->nb + 3) / 4;
+  const int ch = pick_ch(mfma_cpb(L), npg, L->levels);
+  return splits1 * ((panels + kGemvWaves - 1) / kGemvWaves) >= kLdsPlanesWgs && (ch >= 4 || L->nb >= 64);
+}
+
 // Blocks per wave of the MFMA GEMV (each split over K costs one atomic add per
 // output); SDQ_MFMA_BPW overrides.  Measured on MI355X (70B shapes and
 // 8192 x 8192, OSR 2): one block per wave is best up to two plane groups
-// (m <= 8); from three on, the longer-lived waves of two blocks each win
-// (m = 16: 64 -> 56 us on 28672 x 8192, 72 -> 59 us on 8192 x 28672).
-int mfma_bpw(const sdq_layout* L, int64_t m) {
+// (m <= 8) and on the LDS-shared launches; otherwise, from three plane groups
+// on, the longer-lived waves of two blocks each win (m = 16: 64 -> 56 us on
+// 28672 x 8192, 72 -> 59 us on 8192 x 28672; m = 12 o_proj 21.7 -> 19.5 us).
+int mfma_bpw(const sdq_layout* L, int64_t m, int64_t panels) {
   static const char* env = std::getenv("SDQ_MFMA_BPW");
   if (env) {
     const int v = std::atoi(env);
     if (v >= 1) return v;
   }
-  (void)L;
-  return npg_for(m) >= 3 ? 2 : 1;
+  const int npg = npg_for(m);
+  if (npg <= 2) return 1;
+  return npg == 3 && mfma_lds(L, m, panels) ? 1 : 2;
 }
 
 // Workgroups along K per panel (each covers 4 * bpw blocks).
-int mfma_splits(const sdq_layout* L, int64_t m) {
-  const int bpw = mfma_bpw(L, m);
+int mfma_splits(const sdq_layout* L, int64_t m, int64_t panels) {
+  const int bpw = mfma_bpw(L, m, panels);
   return static_cast<int>((L->nb + 4 * bpw - 1) / (4 * bpw));
 }
 
@@ -1554,36 +1610,19 @@ int64_t fill_first(LinearSet& S, F per) {
 }
 
 int64_t panels_of(int64_t n) { return (n + kPanel - 1) / kPanel; }
-constexpr int64_t kLdsPlanesWgs = 768;
 int64_t pgroups_of(int64_t n) { return (panels_of(n) + kGemvWaves - 1) / kGemvWaves; }
 
 template <int LEVELS, int NPG, int CH>
 void launch_mfma_ch(const DecodeWs& w, LinearSet S, const sdq_layout* L, int64_t m, bool accumulate,
                     hipStream_t stream) {
   const int64_t panels = fill_first(S, panels_of);
-  const int bpw = mfma_bpw(L, m);
-  const int splits = mfma_splits(L, m);
-  // K groups fastest: consecutive workgroups sweep one panel's chunks.
-  const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(panels));
-  // Planes shared through LDS by four panels: for two plane groups (5-8 rows)
-  // on launches of at least kLdsPlanesWgs workgroups, when the chunks go in
-  // batches of four or the rows are long (64 blocks or more).  Measured on
-  // MI355X at m = 8 (70B shapes): gate/up 93 -> 87 us at OSR 3 and 65 -> 62 us
-  // at OSR 2 (batches of four), but 78 -> 80 at OSR 2.5 and 51 -> 53 at 1.5
-  // (batches of two); down 2-6 % faster at OSR 1.5-3; the smaller q/k/v and
-  // o launches (256-320 workgroups of four panels) ran 21 -> 31 and
-  // 17 -> 27 us, and one or four plane groups were slower at every size
-  // (m = 2 gate/up 66 -> 72 us, m = 16 140 -> 188 us).
-  // SDQ_MFMA_LDS=0 or 1 forces the choice (a tuning and test aid, read on
-  // every launch so that a test can take both paths in one process).
-  LinearSet S4 = S;
-  const int64_t pgroups = fill_first(S4, pgroups_of);
-  const size_t lds_bytes = static_cast<size_t>(mfma_cpb(L)) * (LEVELS == 2 ? 2 : 1) * NPG * 1024;
-  const char* lds_env = std::getenv("SDQ_MFMA_LDS");
-  bool lds = NPG == 2 && static_cast<int64_t>(splits) * pgroups >= kLdsPlanesWgs && (CH >= 4 || L->nb >= 64);
-  if (lds_env && (std::atoi(lds_env) == 0 || std::atoi(lds_env) == 1)) lds = std::atoi(lds_env) == 1;
-  if constexpr (NPG == 2) {
-    if (lds && lds_bytes <= 65536) {
+  const int bpw = mfma_bpw(L, m, panels);
+  const int splits = mfma_splits(L, m, panels);
+  if constexpr (NPG == 2 || NPG == 3) {
+    if (mfma_lds(L, m, panels)) {
+      LinearSet S4 = S;
+      const int64_t pgroups = fill_first(S4, pgroups_of);
+      const size_t lds_bytes = static_cast<size_t>(mfma_cpb(L)) * (LEVELS == 2 ? 2 : 1) * NPG * 1024;
       const dim3 grid4(static_cast<unsigned>(splits), static_cast<unsigned>(pgroups));
       gemv_mfma_lds_kernel<LEVELS, NPG, CH><<<grid4, dim3(256), lds_bytes, stream>>>(
           S4, reinterpret_cast<const uint4*>(w.planes), w.sx, static_cast<int>(m), L->n_chunks, L->nb,
@@ -1591,6 +1630,8 @@ void launch_mfma_ch(const DecodeWs& w, LinearSet S, const sdq_layout* L, int64_t
       return;
     }
   }
+  // K groups fastest: consecutive workgroups sweep one panel's chunks.
+  const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(panels));
   gemv_mfma_kernel<LEVELS, NPG, CH><<<grid, dim3(256), 0, stream>>>(
       S, reinterpret_cast<const uint4*>(w.planes), w.sx, static_cast<int>(m), L->n_chunks, L->nb, L->m_up,
       mfma_cpb(L), bpw, splits, accumulate ? 1 : 0);
@@ -1691,7 +1732,7 @@ bool decode_reads_base3(const sdq_layout* L, int64_t m) {
 }
 
 bool decode_needs_zero_y(const sdq_layout* L, int64_t m, int64_t panels) {
-  if (use_mfma(L, m)) return mfma_splits(L, m) > 1;
+  if (use_mfma(L, m)) return mfma_splits(L, m, panels) > 1;
   return segs_for(L, pick_seg(L, round_mr(m), panels)) > 1;
 }
 
@@ -1845,8 +1886,8 @@ sdq_status launch_decode_contract(int64_t m, LinearSet S, const sdq_layout* L, b
   }
   if (mfma_base3(L, m)) {
     const int64_t panels = fill_first(S, panels_of);
-    const int bpw = mfma_bpw(L, m);
-    const int splits = mfma_splits(L, m);
+    const int bpw = mfma_bpw(L, m, panels);
+    const int splits = mfma_splits(L, m, panels);
     const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(panels));
 #define SDQ_B3(NPG_)                                                                                  \
   gemv_mfma_b3_kernel<NPG_><<<grid, dim3(256), 0, stream>>>(                                          \

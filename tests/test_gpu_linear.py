@@ -47,10 +47,10 @@ def test_linear_small_f16(n, k, osr, levels, m):
 
 
 @pytest.mark.parametrize("lds", ["0", "1"])
-@pytest.mark.parametrize("m", [5, 8])
+@pytest.mark.parametrize("m", [5, 8, 12])
 @pytest.mark.parametrize("n,k,osr,levels", SHAPES)
 def test_linear_mfma_planes_from_lds_or_l2(n, k, osr, levels, m, lds, monkeypatch):
-    # The 5-8-row contraction has two kernels: planes read per panel from L2,
+    # The 5-12-row contraction has two kernels: planes read per panel from L2,
     # or staged in LDS once per four panels (chosen by launch size; forced
     # here so that both run on every shape).
     torch = require_gpu()
