@@ -16,10 +16,13 @@ last-level cache, so every step streams them.  Steps replay one HIP graph
 --steps replays are timed between HIP events on the replay stream.  The line
 also carries:
 
-* roofline     -- the table GEMV (gemv_lut_kernel, every contraction launch
-                  of the step): the step's code bytes / the time of a graph
-                  holding only those launches (expansions done beforehand),
-                  against 8 TB/s and against the measured streaming-read rate;
+* roofline     -- the step's decode contractions (every contraction launch:
+                  the one-row matrix-core kernel gemv_mfma_kernel<3,1,*,true>
+                  on rows of k_up >= 16384 samples, the table GEMV
+                  gemv_lut_kernel<1,3,*> on shorter ones): the step's code
+                  bytes / the time of a graph holding only those launches
+                  (expansions done beforehand), against 8 TB/s and against
+                  the measured streaming-read rate;
 * config.m8    -- the same stack at eight activation rows (matrix-core decode);
 * phases       -- the LLaMA-7B down_proj decode (workload 2), the LLaMA-7B layer
                   at m = 1, 4, 16 (workload 3), the three LLaMA-70B linears at
@@ -63,9 +66,9 @@ POOL_MAX = 16                    # oracle workers: the host share of one GPU
 TRAFFIC_FETCH_SCALE = 1.999749
 TRAFFIC_WRITE_SCALE = 1.000000
 TRAFFIC_SOURCES = {"linear_decode.hip": "48f9d1a35a31d513dedf938e53bffab2145ebb68e109bb7dc100aa4b7f927670"}
-# kernel family -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB) per launch: the mean
+# launch family -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB) per launch: the mean
 # over the 325 contraction launches of one m = 1 token step through the stack.
-TRAFFIC_KIB = {"gemv_lut_kernel<1,3,*>": ("linear_decode.hip", 64802.0, 6897.9)}
+TRAFFIC_KIB = {"m1_step_contractions": ("linear_decode.hip", 64802.0, 6897.9)}
 
 
 def traffic_bytes(kernel: str):
@@ -890,8 +893,9 @@ def main() -> int:
                                               "groups_per_step", "osr_first_layer", "osr_last_layer")},
         },
         "roofline": {"bound": "hbm", "achieved": gemv_gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-                     "frac": gemv_gbs / HBM_PEAK_GBS, "traffic": traffic_bytes("gemv_lut_kernel<1,3,*>"),
-                     "kernel": "gemv_lut_kernel<1,3,*> (every table-GEMV launch of one token step)",
+                     "frac": gemv_gbs / HBM_PEAK_GBS, "traffic": traffic_bytes("m1_step_contractions"),
+                     "kernel": "every decode contraction launch of one token step: gemv_mfma_kernel<3,1,*,true> "
+                               "(rows of k_up >= 16384 samples) and gemv_lut_kernel<1,3,*> (shorter rows)",
                      "launches": n_gemv, "ms_per_step_of_launches": ms_gemv,
                      "bytes_per_launch": info["code_bytes"] / n_gemv,
                      "frac_of_stream_read_peak": gemv_gbs / peak["gbs"],

@@ -236,7 +236,10 @@ sdq_status sdq_quantize_compensated(const float* w_dev, const sdq_layout* layout
 
 /* Device workspace (bytes) sdq_linear needs for m activation rows: the
  * expanded activations, at offset 0 --
- *   m = 1:        fp32 x_tilde, k_up rounded up to whole chunks;
+ *   m = 1:        fp32 x_tilde, k_up rounded up to whole chunks (binary,
+ *                 base-3, or k_up < 16384); else the planes below in a
+ *                 compact form (192 bytes per 64-code step) and the plane
+ *                 scale of every block;
  *   2 <= m <= 16: x_tilde as 24-bit fixed point (three signed-byte planes,
  *                 rows in groups of four, per block in chunk slots; for
  *                 base-3 codes in the order of their digits: per group of
@@ -257,13 +260,17 @@ size_t sdq_linear_workspace_bytes(const sdq_layout* layout, int64_t m);
  * y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j].  Equivalent to
  * sdq_expand_activations followed by sdq_linear_expanded on the same workspace.
  *   x_dev        [m x k] activations of type xt (F16, BF16 or F32), row-major.
- *   m            activation rows, >= 0 (m = 0 is a no-op).  m = 1: fp32
- *                expansion and a GEMV with additions only over the codes;
- *                2 <= m <= 16: the expansion (for fp16 and bf16 x on the
- *                matrix cores against E as an fp16 pair hi + lo, ~22 bits)
- *                quantised to 24-bit fixed point and an exact int8 x int8 ->
- *                int32 matrix-core contraction against the codes; larger m: the prefill
- *                path (fp16 expansion, fp16 matrix cores).
+ *   m            activation rows, >= 0 (m = 0 is a no-op).  m = 1 with
+ *                binary or base-3 codes or k_up < 16384: fp32 expansion and
+ *                a GEMV with additions only over the codes; 2 <= m <= 16, and
+ *                one row of ternary 2-bit fields with k_up >= 16384: the
+ *                expansion (for fp16 and bf16 x and m >= 2 on the matrix
+ *                cores against E as an fp16 pair hi + lo, ~22 bits; else
+ *                fp32) quantised to 24-bit fixed point and an exact int8 x
+ *                int8 -> int32 matrix-core contraction against the codes
+ *                (each code a +-1 or 0 weight: the products select, negate
+ *                or drop the activations); larger m: the prefill path (fp16
+ *                expansion, fp16 matrix cores).
  *   codes_dev, scales_dev  as written by sdq_quantize for `layout`.
  *   y_dev        fp32 [m x n] output, row-major.
  *   accumulate   0: y = x W_hat^T (y fully overwritten);  nonzero: y += x W_hat^T

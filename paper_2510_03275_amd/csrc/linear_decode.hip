@@ -316,6 +316,33 @@ __device__ inline void store_planes(const int (*qv)[64], int m, int npg, int64_t
   }
 }
 
+// One activation row: the planes h, m, l of the workgroup's 64 code
+// positions in the compact layout of that case, 12 groups of 16 bytes per
+// k-step (k-group kg, plane t at (kg * 3 + t) * 16 bytes) -- the A-operand
+// words of lanes 16 kg + t; the other lanes' rows are zero and not stored.
+// Lanes idx < 48 of one wave store a dword each.
+template <int LEVELS>
+__device__ inline void store_planes_m1(const int* qv, int64_t slot, int half, int idx,
+                                       uint32_t* __restrict__ planes) {
+  if (idx >= 48) return;
+  const int di = idx % 4;
+  const int t = (idx / 4) % 3;
+  int s, kg;
+  if (LEVELS == 2) {
+    kg = 2 * half + (idx / 12) % 2;
+    s = idx / 24;
+  } else {
+    kg = idx / 12;
+    s = 0;
+  }
+  uint32_t word = 0;
+#pragma unroll
+  for (int beta = 0; beta < 4; ++beta)
+    word |= plane_byte(qv[chunk_code<LEVELS>(s, kg, di, beta) - 64 * half], t) << (8 * beta);
+  const int64_t step = LEVELS == 2 ? 2 * slot + s : slot;
+  planes[((step * 12) + kg * 3 + t) * 4 + di] = word;
+}
+
 typedef _Float16 half8_t __attribute__((ext_vector_type(8)));
 typedef float float4_t __attribute__((ext_vector_type(4)));
 
@@ -431,8 +458,11 @@ __device__ inline void planes_qv_mfma(const uint16_t* __restrict__ x, int m, int
 // One workgroup: one 64-code segment u of block b's chunk slots (code
 // positions floor(b M / chunk) * chunk + 64 u + [0, 64)), all m rows; the
 // samples of block b among them by the fp32 expansion, the rest zero; then
-// quantised and written as planes (256 * npg dwords per workgroup).
-template <int B, int LEVELS>
+// quantised and written as planes (256 * npg dwords per workgroup; one row:
+// 48 dwords in the compact layout).  NB = 2 (one activation row, M a multiple
+// of the chunk): blocks b and b + 1 take the places of two rows, sharing the
+// workgroup's columns of E.
+template <int B, int LEVELS, int NB>
 __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
     const void* __restrict__ x, sdq_dtype xt, int m, int npg, int64_t k, int64_t nb, int m_up,
     int m_pad, int cpb, const float4* __restrict__ edec, float e1max, uint32_t* __restrict__ planes,
@@ -446,7 +476,10 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   const int lane = tid % 64;
   const int w = tid / 64;
   constexpr int kCpc = LEVELS == 2 ? 128 : 64;             // codes per chunk
-  const int64_t b = blockIdx.y;
+  static_assert(NB == 1 || NB == 2, "one or two blocks per workgroup");
+  const int64_t b = static_cast<int64_t>(blockIdx.y) * NB;
+  // rows of the workgroup: the m activation rows, or (NB = 2) the blocks
+  const int R = NB == 2 ? static_cast<int>(min<int64_t>(2, nb - b)) : m;
   const int64_t c_first = b * m_up / kCpc;                  // block b's first code chunk
   const int64_t g0 = c_first * kCpc + static_cast<int64_t>(blockIdx.x) * 64;
   const int o = static_cast<int>(g0 + lane - b * m_up);    // this lane's sample within block b
@@ -456,9 +489,10 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   // one global round trip per element), and before the E columns, so that
   // the stores and the max below wait for x alone.
   constexpr int XPT = kMaxDecodeRows * B / kExpThreads;   // elements per thread, at most
-  const int mb = m * B;
+  const int mb = R * B;
   uint32_t xr[XPT];
-  const int k32 = static_cast<int>(k);   // m k < 2^31 on the decode path
+  // row stride: k (activation rows), or B (consecutive blocks of row 0)
+  const int k32 = NB == 2 ? B : static_cast<int>(k);   // m k < 2^31 on the decode path
   if (xt == SDQ_F32) {
     const uint32_t* __restrict__ xp = static_cast<const uint32_t*>(x) + b * B;
 #pragma unroll
@@ -496,13 +530,13 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
   zero_outputs(zero, m, wg, n_wg, tid);
   __syncthreads();
   // max |x_b| per row: wave w handles rows w, w + 4, ...
-  for (int i = w; i < m; i += 4) {
+  for (int i = w; i < R; i += 4) {
     float mx = 0.0f;
     for (int t = lane; t < B; t += 64) mx = fmaxf(mx, fabsf(xs[i][t]));
     mx = wave_max_nonneg(mx);
     if (lane == 0) xmax[i] = mx;
   }
-  for (int i = 0; i < m; ++i) {
+  for (int i = 0; i < R; ++i) {
     const float4* xr = reinterpret_cast<const float4*>(&xs[i][w * TQ]);
     float a0 = 0.f, a1 = 0.f, a2 = 0.f, a3 = 0.f;
 #pragma unroll
@@ -516,17 +550,33 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_kernel(
     red[w][i][lane] = (a0 + a1) + (a2 + a3);
   }
   __syncthreads();
-  for (int idx = tid; idx < m * 64; idx += kExpThreads) {
+  const int64_t u = static_cast<int64_t>(blockIdx.x) / (kCpc / 64);
+  const int half = static_cast<int>(blockIdx.x % (kCpc / 64));
+  if (m == 1) {
+    // wave i finishes row (block) i alone: sum, quantise, compact plane words
+    if (w < R) {
+      const int i = w;
+      const float val = (red[0][i][lane] + red[1][i][lane]) + (red[2][i][lane] + red[3][i][lane]);
+      const float bound = xmax[i] * e1max;
+      qv[i][lane] = bound > 0.0f && in_block ? __float2int_rn(val * (kQ / bound)) : 0;
+      if (blockIdx.x == 0 && lane == 0) sx[NB == 2 ? b + i : b] = bound / kQ;
+      __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+      __builtin_amdgcn_wave_barrier();
+      __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+      store_planes_m1<LEVELS>(qv[i], (b + i) * cpb + u, half, lane, planes);
+    }
+    return;
+  }
+  for (int idx = tid; idx < R * 64; idx += kExpThreads) {
     const int i = idx / 64, l = idx % 64;
     const float val = (red[0][i][l] + red[1][i][l]) + (red[2][i][l] + red[3][i][l]);
     const float bound = xmax[i] * e1max;
-    const int ol = static_cast<int>(g0 + l - b * m_up);
+    const int ol = static_cast<int>(g0 + l - b * m_up);   // (NB = 2: the same for both blocks)
     qv[i][l] = bound > 0.0f && ol >= 0 && ol < m_up ? __float2int_rn(val * (kQ / bound)) : 0;
-    if (blockIdx.x == 0 && l == 0) sx[static_cast<int64_t>(i) * nb + b] = bound / kQ;
+    if (blockIdx.x == 0 && l == 0) sx[NB == 2 ? b + i : static_cast<int64_t>(i) * nb + b] = bound / kQ;
   }
   __syncthreads();
-  store_planes<LEVELS>(qv, m, npg, b * cpb + static_cast<int64_t>(blockIdx.x) / (kCpc / 64),
-                       static_cast<int>(blockIdx.x % (kCpc / 64)), planes);
+  store_planes<LEVELS>(qv, m, npg, b * cpb + u, half, planes);
 }
 
 // Base-3 codes on the integer-MFMA path (read as stored, no unpack pass).
@@ -710,7 +760,7 @@ __global__ __launch_bounds__(kExpThreads) void expand_planes_b3_mfma_kernel(
 // leaves word kg of row 16 cg + c in register cg of lane 16 kg + c: the B
 // operand of the MFMA on column group cg.  The four waves' partial sums meet
 // in LDS and leave with one atomic add (or store) per output.
-template <int LEVELS, int NPG, int CH>
+template <int LEVELS, int NPG, int CH, bool M1>
 __global__ __launch_bounds__(256) void gemv_mfma_kernel(
     LinearSet S, const uint4* __restrict__ planes, const float* __restrict__ sx, int m,
     int64_t n_chunks, int64_t nb, int m_up, int cpb, int bpw, int n_split, int accumulate) {
@@ -767,8 +817,14 @@ __global__ __launch_bounds__(256) void gemv_mfma_kernel(
         for (int s = 0; s < SPC; ++s)
 #pragma unroll
           for (int pg = 0; pg < NPG; ++pg) {
-            const uint4 v = planes[((slot * SPC + s) * NPG + pg) * 64 + lane];
-            av[j][s][pg] = live ? v : make_uint4(0u, 0u, 0u, 0u);
+            if constexpr (M1) {   // compact planes: rows 0-2 stored, the rest zero
+              const int p = lane % 16;
+              const uint4 v = planes[(slot * SPC + s) * 12 + kg * 3 + min(p, 2)];
+              av[j][s][pg] = live && p < 3 ? v : make_uint4(0u, 0u, 0u, 0u);
+            } else {
+              const uint4 v = planes[((slot * SPC + s) * NPG + pg) * 64 + lane];
+              av[j][s][pg] = live ? v : make_uint4(0u, 0u, 0u, 0u);
+            }
           }
       }
 #pragma unroll
@@ -1465,15 +1521,25 @@ int segs_for(const sdq_layout* L, int seg) {
   return static_cast<int>((L->n_chunks + seg - 1) / seg);
 }
 
-// Decode variants: one activation row runs the addition-only table GEMV;
-// 2..16 rows run the integer-MFMA contraction, whose cost hardly grows with
-// the row count.  SDQ_DECODE_PATH=lut or =mfma forces one (a tuning and
-// cross-check aid).
+// Decode variants: 2..16 rows run the integer-MFMA contraction, whose cost
+// hardly grows with the row count; one row of ternary 2-bit fields runs it
+// too on long upsampled rows (compact planes, three operand rows of
+// sixteen), short rows and binary and base-3 codes the addition-only table
+// GEMV (the plane expansion costs ~0.5 us more than the table path's, which
+// the faster contraction repays from ~40 MB of codes per call).  Measured on
+// MI355X at m = 1 (70B shapes, expansion + contraction in graph replay):
+// gate/up OSR 3 69.3 -> 66.2 us, OSR 2 49.4 -> 47.7, down OSR 3 41.3 -> 40.4,
+// q/k/v OSR 3 19.8 -> 19.6 but OSR 1.5 12.1 -> 13.3; the LLaMA-7B binary
+// down_proj 8.2 -> 10.3 and base-3 gate/up 62.6 -> 140 us.  The rule depends
+// on the layout's k, M, levels and packing only, which the linears of one
+// group share.  SDQ_DECODE_PATH=lut or =mfma forces one (a tuning and
+// cross-check aid, read on every call).
+constexpr int64_t kMfmaRowKup = 16384;   // one row: the MFMA path from k * M / B samples
 bool use_mfma(const sdq_layout* L, int64_t m) {
-  static const char* env = std::getenv("SDQ_DECODE_PATH");
+  const char* env = std::getenv("SDQ_DECODE_PATH");
   if (env && std::string(env) == "lut") return false;
   if (env && std::string(env) == "mfma") return true;
-  return m >= 2;
+  return m >= 2 || (L->levels == 3 && L->packing == SDQ_PACK_FIELDS && L->k_up >= kMfmaRowKup);
 }
 
 int npg_for(int64_t m) { return static_cast<int>((m + 3) / 4); }
@@ -1561,6 +1627,7 @@ int mfma_splits(const sdq_layout* L, int64_t m, int64_t panels) {
 struct DecodeWs {
   float* xt;          // table path: x_tilde, m x k_up_pad fp32
   uint32_t* planes;   // MFMA path: fixed-point planes, nb x cpb x (chunk / 64) k-steps x npg x 1 KB
+                      // (one row: 192 bytes per k-step)
   float* sx;          // MFMA path: per (row, block) plane scale, m x nb fp32
   size_t bytes;
 };
@@ -1573,7 +1640,9 @@ DecodeWs carve(const sdq_layout* L, int64_t m, void* base) {
   if (use_mfma(L, m)) {
     const size_t steps = mfma_base3(L, m) ? static_cast<size_t>(L->nb) * mfma_steps3(L)
                                           : static_cast<size_t>(L->nb) * mfma_cpb(L) * (L->levels == 2 ? 2 : 1);
-    const size_t pl = align_up(steps * npg_for(m) * 1024, 256);
+    // (one activation row of 2-bit fields: compact planes, 192 bytes per k-step)
+    const size_t per_step = m == 1 && !mfma_base3(L, m) ? 192 : static_cast<size_t>(npg_for(m)) * 1024;
+    const size_t pl = align_up(steps * per_step, 256);
     w.planes = reinterpret_cast<uint32_t*>(p);
     w.sx = reinterpret_cast<float*>(p + pl);
     w.bytes = pl + align_up(static_cast<size_t>(m) * L->nb * 4, 256);
@@ -1612,13 +1681,13 @@ int64_t fill_first(LinearSet& S, F per) {
 int64_t panels_of(int64_t n) { return (n + kPanel - 1) / kPanel; }
 int64_t pgroups_of(int64_t n) { return (panels_of(n) + kGemvWaves - 1) / kGemvWaves; }
 
-template <int LEVELS, int NPG, int CH>
+template <int LEVELS, int NPG, int CH, bool M1 = false>
 void launch_mfma_ch(const DecodeWs& w, LinearSet S, const sdq_layout* L, int64_t m, bool accumulate,
                     hipStream_t stream) {
   const int64_t panels = fill_first(S, panels_of);
   const int bpw = mfma_bpw(L, m, panels);
   const int splits = mfma_splits(L, m, panels);
-  if constexpr (NPG == 2 || NPG == 3) {
+  if constexpr (!M1 && (NPG == 2 || NPG == 3)) {
     if (mfma_lds(L, m, panels)) {
       LinearSet S4 = S;
       const int64_t pgroups = fill_first(S4, pgroups_of);
@@ -1632,7 +1701,7 @@ void launch_mfma_ch(const DecodeWs& w, LinearSet S, const sdq_layout* L, int64_t
   }
   // K groups fastest: consecutive workgroups sweep one panel's chunks.
   const dim3 grid(static_cast<unsigned>(splits), static_cast<unsigned>(panels));
-  gemv_mfma_kernel<LEVELS, NPG, CH><<<grid, dim3(256), 0, stream>>>(
+  gemv_mfma_kernel<LEVELS, NPG, CH, M1><<<grid, dim3(256), 0, stream>>>(
       S, reinterpret_cast<const uint4*>(w.planes), w.sx, static_cast<int>(m), L->n_chunks, L->nb, L->m_up,
       mfma_cpb(L), bpw, splits, accumulate ? 1 : 0);
 }
@@ -1644,6 +1713,13 @@ void launch_mfma_levels(const DecodeWs& w, const LinearSet& S, const sdq_layout*
   const int ch = pick_ch(mfma_cpb(L), npg, LEVELS);
 #define SDQ_CH(NPG_, CH_)                                                         \
   if (ch == CH_) return launch_mfma_ch<LEVELS, NPG_, CH_>(w, S, L, m, acc, stream)
+#define SDQ_CH1(CH_)                                                              \
+  if (ch == CH_) return launch_mfma_ch<LEVELS, 1, CH_, true>(w, S, L, m, acc, stream)
+  if (m == 1) {   // compact planes
+    SDQ_CH1(8); SDQ_CH1(6); SDQ_CH1(4); SDQ_CH1(3); SDQ_CH1(2);
+    return launch_mfma_ch<LEVELS, 1, 1, true>(w, S, L, m, acc, stream);
+  }
+#undef SDQ_CH1
   switch (npg) {
     case 1:
       SDQ_CH(1, 8); SDQ_CH(1, 6); SDQ_CH(1, 4); SDQ_CH(1, 3); SDQ_CH(1, 2);
@@ -1792,6 +1868,14 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
     if (nbw_env && (std::atoi(nbw_env) == 1 || std::atoi(nbw_env) == 2)) pnb = std::atoi(nbw_env);
     if (L->m_up % cpc != 0) pnb = 1;
     const dim3 pgrid2(pgrid.x, static_cast<unsigned>((L->nb + 1) / 2));
+    // One activation row: the fp32 VALU front end (the matrix-core one would
+    // leave 15 of its 16 operand rows empty), two blocks per workgroup sharing
+    // E when M is a multiple of the chunk and the launch has kExpRowPairs
+    // (segment, block) pairs or more (SDQ_EXP_NBW=1 or 2 overrides).
+    static const char* rnb_env = std::getenv("SDQ_EXP_NBW");
+    int rnb = L->m_up % cpc == 0 && static_cast<int64_t>(pgrid.x) * L->nb >= kExpRowPairs ? 2 : 1;
+    if (rnb_env && (std::atoi(rnb_env) == 1 || std::atoi(rnb_env) == 2)) rnb = std::atoi(rnb_env);
+    if (L->m_up % cpc != 0) rnb = 1;
 #define SDQ_PLANES_M(BB, LV, BF)                                                                 \
   if (pnb == 2)                                                                                  \
     expand_planes_mfma_kernel<BB, LV, BF, 2><<<pgrid2, dim3(kExpThreads), 0, stream>>>(          \
@@ -1801,15 +1885,21 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
     expand_planes_mfma_kernel<BB, LV, BF, 1><<<pgrid, dim3(kExpThreads), 0, stream>>>(           \
         x, static_cast<int>(m), npg, L->k, L->nb, L->m_up, cpb, T->et_hi, T->et_lo, T->e1max,      \
         w.planes, w.sx, z)
+#define SDQ_PLANES_V(BB, LV, NB_, GRID)                                                          \
+  expand_planes_kernel<BB, LV, NB_><<<GRID, dim3(kExpThreads), 0, stream>>>(                     \
+      x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad, cpb,                      \
+      reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, z)
 #define SDQ_PLANES(BB, LV)                                                                       \
-  if (planes_mfma && xt == SDQ_BF16) {                                                           \
+  if (m == 1 && rnb == 2) {                                                                      \
+    SDQ_PLANES_V(BB, LV, 2, pgrid2);                                                             \
+  } else if (m == 1) {                                                                           \
+    SDQ_PLANES_V(BB, LV, 1, pgrid);                                                              \
+  } else if (planes_mfma && xt == SDQ_BF16) {                                                    \
     SDQ_PLANES_M(BB, LV, true);                                                                  \
   } else if (planes_mfma) {                                                                      \
     SDQ_PLANES_M(BB, LV, false);                                                                 \
   } else                                                                                         \
-    expand_planes_kernel<BB, LV><<<pgrid, dim3(kExpThreads), 0, stream>>>(                       \
-        x, xt, static_cast<int>(m), npg, L->k, L->nb, L->m_up, T->m_pad, cpb,                    \
-        reinterpret_cast<const float4*>(T->edec), T->e1max, w.planes, w.sx, z)
+    SDQ_PLANES_V(BB, LV, 1, pgrid)
     if (L->levels == 2) {
       switch (B) {
         case 64: SDQ_PLANES(64, 2); break;
@@ -1824,6 +1914,7 @@ sdq_status launch_decode_expand(const void* x, sdq_dtype xt, int64_t m, const sd
       }
     }
 #undef SDQ_PLANES
+#undef SDQ_PLANES_V
 #undef SDQ_PLANES_M
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return hip_error(e, "decode expansion launch");

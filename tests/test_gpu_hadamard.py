@@ -45,7 +45,7 @@ def test_encoder_bit_exact_for_each_had(mode, n, k, osr, levels, block):
 @pytest.mark.parametrize("n,k,osr,levels,block", SHAPES[:3] + SHAPES[4:])
 def test_linear_for_each_had(mode, n, k, osr, levels, block):
     # Codes from the oracle (so the linear is checked on its own), m covering
-    # the table GEMV (1), the integer-MFMA decode (3, 16) and prefill (40).
+    # the one-row decode (1), the integer-MFMA decode (3, 16) and prefill (40).
     torch = require_gpu()
     import paper_2510_03275_amd as P
     s = _signs(mode, block, 7 * n)

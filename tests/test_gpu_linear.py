@@ -63,6 +63,23 @@ def test_linear_mfma_planes_from_lds_or_l2(n, k, osr, levels, m, lds, monkeypatc
     assert np.all(err <= TOL), err.max()
 
 
+@pytest.mark.parametrize("path", ["lut", "mfma"])
+@pytest.mark.parametrize("m", [1, 2, 7])
+@pytest.mark.parametrize("n,k,osr,levels", SHAPES)
+def test_linear_decode_both_paths(n, k, osr, levels, m, path, monkeypatch):
+    # Both decode contractions on every shape and row count (the choice by
+    # row count and code kind forced here): the addition-only table GEMV and
+    # the integer-MFMA one (compact planes at one row).
+    torch = require_gpu()
+    monkeypatch.setenv("SDQ_DECODE_PATH", path)
+    enc, r = _oracle_codes_on_device(torch, n, k, osr, levels, seed=5 * n + m)
+    x_dev, x64 = to_device_x(synth.activations_f32(m + 3, 0, m, k), "f16", torch)
+    y = _run_linear(torch, enc, x_dev)
+    y_ref = OL.linear_fp64(x64, r.codes, r.scales, 256, r.m_up)
+    err = OL.rel_err_rows(y, y_ref)
+    assert np.all(err <= TOL), err.max()
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("m", [1, 5, 16, 40])
 def test_linear_small_other_dtypes(dtype, m):

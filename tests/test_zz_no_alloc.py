@@ -31,7 +31,8 @@ def _encoded(torch, n, k, osr, levels, seed, packing=0):
 
 
 @pytest.mark.parametrize("n,k,osr,levels,packing,ms", [
-    (768, 4096, 2.0, 3, 0, (1, 1)),           # table GEMV, split over K
+    (256, 8192, 2.0, 3, 0, (1, 1)),           # one row, k_up 16384: matrix-core decode on compact planes
+    (768, 4096, 2.0, 3, 0, (1, 1)),           # one row, k_up 8192: table GEMV, split over K
     (700, 2048, 1.5, 2, 0, (8, 3)),           # matrix-core decode
     (600, 1024, 2.5, 3, 0, (130, 40)),        # prefill
     (600, 2048, 2.0, 3, 1, (1, 1)),           # base-3, one row
