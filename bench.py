@@ -65,10 +65,10 @@ POOL_MAX = 16                    # oracle workers: the host share of one GPU
 # were taken with: a source whose hash differs reports traffic null.
 TRAFFIC_FETCH_SCALE = 1.999749
 TRAFFIC_WRITE_SCALE = 1.000000
-TRAFFIC_SOURCES = {"linear_decode.hip": "48f9d1a35a31d513dedf938e53bffab2145ebb68e109bb7dc100aa4b7f927670"}
+TRAFFIC_SOURCES = {"linear_decode.hip": "8724ec4b804cf456d816d6cdb6b93a23ca13b410045cd3246f527c3dc50dca07"}
 # launch family -> (source, FETCH_SIZE KiB, WRITE_SIZE KiB) per launch: the mean
 # over the 325 contraction launches of one m = 1 token step through the stack.
-TRAFFIC_KIB = {"m1_step_contractions": ("linear_decode.hip", 64802.0, 6897.9)}
+TRAFFIC_KIB = {"m1_step_contractions": ("linear_decode.hip", 65092.0, 1636.6)}
 
 
 def traffic_bytes(kernel: str):
