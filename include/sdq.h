@@ -356,10 +356,11 @@ sdq_status sdq_expand_activations(const void* x_dev, sdq_dtype xt, int64_t m,
 
 /* Second step of sdq_linear: y[i, r] = s_r * sum_j C[r, j] x_tilde[i, j] from
  * the x_tilde that sdq_expand_activations left in the workspace (same m and a
- * layout with the same k, block, m_up and levels).  m = 1: addition-only
- * lookup-table GEMV; 2 <= m <= 16: exact int8 matrix-core contraction against
- * the fixed-point expansion; larger m: fp16 MFMA GEMM.  accumulate as in
- * sdq_linear.  Errors as sdq_linear. */
+ * layout with the same k, block, m_up, levels and packing).  m = 1 (binary,
+ * base-3 or k_up < 16384): addition-only lookup-table GEMV; 2 <= m <= 16 and
+ * one row of ternary 2-bit fields with k_up >= 16384: exact int8 matrix-core
+ * contraction against the fixed-point expansion; larger m: fp16 MFMA GEMM.
+ * accumulate as in sdq_linear.  Errors as sdq_linear. */
 sdq_status sdq_linear_expanded(int64_t m, const void* codes_dev, const float* scales_dev,
                                const sdq_layout* layout, float* y_dev, int32_t accumulate,
                                void* workspace_dev, size_t workspace_bytes, void* stream);
